@@ -1,0 +1,241 @@
+"""ctypes shim for the CPU oracle (test infrastructure).
+
+Only tests, the smoke check and the benchmark's CPU-baseline leg may import
+this module.  It builds and loads ``liboracle.so`` from ``wait_oracle.c`` in
+this directory and shares nothing with the GPU library.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "wait_oracle.c")
+LIB = os.path.join(HERE, "liboracle.so")
+
+POLICY = {"wait": 0, "nested": 1, "fcfs": 2}
+FLAG_CAPACITY, FLAG_STALL, FLAG_OVERFLOW = 1, 2, 4
+
+INT_FIELDS = ["batches", "arrivals", "completions", "completed_tokens",
+              "evictions", "evicted_tokens", "fallback_evictions",
+              "batch_tokens_sum", "peak_mem", "waiting_end", "resident_end",
+              "idle_waits"]
+F64_FIELDS = ["t_end", "busy_time", "lat_area", "ttft_area",
+              "lat_completed_sum", "mem_area"]
+
+
+class _Config(C.Structure):
+    _fields_ = [
+        ("m", C.c_int32), ("l", C.c_void_p), ("lam", C.c_void_p),
+        ("lp", C.c_void_p), ("out_cap", C.c_int32), ("cdf", C.c_void_p),
+        ("d0", C.c_double), ("d1", C.c_double), ("C", C.c_int64),
+        ("edges", C.c_void_p), ("n_edges", C.c_int32),
+        ("record_capacity", C.c_int64), ("tr_time", C.c_void_p),
+        ("tr_type", C.c_void_p), ("tr_L", C.c_void_p), ("n_trace", C.c_int64),
+        ("policy", C.c_int32), ("n", C.c_void_p), ("nseg", C.c_int32),
+        ("seg_end", C.c_void_p), ("reserve", C.c_double),
+    ]
+
+
+class _Result(C.Structure):
+    _fields_ = ([(f, C.c_int64) for f in INT_FIELDS]
+                + [(f, C.c_double) for f in F64_FIELDS]
+                + [("flags", C.c_uint32), ("pad", C.c_uint32)])
+
+
+class _BatchRec(C.Structure):
+    _fields_ = [("t_launch", C.c_double), ("tau", C.c_double)] + [
+        (f, C.c_int64) for f in ("tokens", "prefills", "selected", "completions",
+                                 "evict_pre", "evict_post", "mem_after",
+                                 "waiting_after", "resident_after", "pad")]
+
+
+class _ReqLog(C.Structure):
+    _fields_ = [("arr", C.c_void_p), ("done", C.c_void_p),
+                ("first", C.c_void_p), ("cap", C.c_int64)]
+
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle (plain C, -O2, no FP contraction, no fast-math)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        cmd = ["gcc", "-O2", "-std=gnu11", "-Wall", "-ffp-contract=off",
+               "-fno-fast-math", "-fPIC", "-shared", "-o", LIB + ".tmp", SRC,
+               "-lpthread", "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(LIB + ".tmp", LIB)
+    return LIB
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+            build(force=True)
+        L = C.CDLL(LIB)
+        L.oracle_run.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_uint32,
+                                 C.c_int64, C.POINTER(_Result), C.c_void_p,
+                                 C.c_void_p, C.c_int64, C.c_void_p]
+        L.oracle_run_many.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_void_p,
+                                      C.c_int32, C.c_int64, C.c_void_p,
+                                      C.c_void_p, C.c_int32]
+        L.oracle_philox4x32_10.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
+        L.oracle_uniform.argtypes = [C.c_uint32, C.c_uint32]
+        L.oracle_uniform.restype = C.c_double
+        L.oracle_ln.argtypes = [C.c_double]
+        L.oracle_ln.restype = C.c_double
+        L.oracle_draw.argtypes = [C.c_uint64, C.c_uint32, C.c_int32, C.c_uint32,
+                                  C.c_double, C.c_void_p, C.c_int32,
+                                  C.POINTER(C.c_double), C.POINTER(C.c_int32)]
+        _lib = L
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+class _Pinned:
+    """Keeps the numpy arrays behind a config alive."""
+
+    def __init__(self, wl):
+        self.keep = []
+        c = _Config()
+        c.m = wl.m
+
+        def arr(x, dt):
+            a = np.ascontiguousarray(np.asarray(x, dtype=dt))
+            self.keep.append(a)
+            return a
+
+        c.l = _ptr(arr(wl.prompt_len, np.int32))
+        c.lam = _ptr(arr(wl.lam, np.float64))
+        c.lp = None if wl.out_len is None else _ptr(arr(wl.out_len, np.int32))
+        c.out_cap = int(wl.out_cap)
+        c.cdf = None if wl.out_cdf is None else _ptr(arr(wl.out_cdf, np.uint32))
+        c.d0, c.d1, c.C = float(wl.d0), float(wl.d1), int(wl.C)
+        if wl.hist_edges is None:
+            c.edges, c.n_edges = None, 0
+        else:
+            c.edges = _ptr(arr(wl.hist_edges, np.float64))
+            c.n_edges = len(wl.hist_edges)
+        c.record_capacity = int(wl.record_capacity)
+        if wl.trace is not None:
+            t, ty, L = wl.trace
+            c.tr_time = _ptr(arr(t, np.float64))
+            c.tr_type = _ptr(arr(ty, np.int32))
+            c.tr_L = _ptr(arr(L, np.int32))
+            c.n_trace = len(t)
+        else:
+            c.tr_time = c.tr_type = c.tr_L = None
+            c.n_trace = 0
+        c.policy = POLICY[wl.policy]
+        c.n = _ptr(arr(wl.n if len(wl.n) else [0], np.int32))
+        if wl.seg_end is not None:
+            c.seg_end = _ptr(arr(wl.seg_end, np.int32))
+            c.nseg = len(wl.seg_end)
+        else:
+            c.seg_end, c.nseg = None, 0
+        c.reserve = float(wl.reserve)
+        self.cfg = c
+
+
+def _to_dict(res_arr, hist):
+    out = {}
+    for f in INT_FIELDS:
+        out[f] = np.array([getattr(r, f) for r in res_arr], dtype=np.int64)
+    for f in F64_FIELDS:
+        out[f] = np.array([getattr(r, f) for r in res_arr], dtype=np.float64)
+    out["flags"] = np.array([r.flags for r in res_arr], dtype=np.uint32)
+    out["hist"] = hist
+    return out
+
+
+def run(wl, seed: int, replica_ids, horizon: int, threads: int = 0) -> dict:
+    """Simulate every replica of a workload; returns arrays per field."""
+    L = lib()
+    pin = _Pinned(wl)
+    ids = np.ascontiguousarray(np.asarray(replica_ids, dtype=np.uint32))
+    n = len(ids)
+    res = (_Result * n)()
+    nb = (len(wl.hist_edges) if wl.hist_edges is not None else 0) + 1
+    hist = np.zeros((n, nb), dtype=np.uint32)
+    if threads <= 0:
+        threads = min(os.cpu_count() or 1, 16)
+    L.oracle_run_many(C.byref(pin.cfg), C.c_uint64(seed), ids.ctypes.data, n,
+                      horizon, C.addressof(res), hist.ctypes.data, threads)
+    return _to_dict(res, hist)
+
+
+def run_job(job, horizon: int, threads: int = 0) -> dict:
+    return run(job.wl, job.seed, job.replica_ids, horizon, threads)
+
+
+def run_one(wl, seed: int, replica_id: int, horizon: int, btrace_cap: int = 0,
+            rlog_cap: int = 0) -> dict:
+    """One replica with optional per-batch trace and per-request log."""
+    L = lib()
+    pin = _Pinned(wl)
+    res = _Result()
+    nb = (len(wl.hist_edges) if wl.hist_edges is not None else 0) + 1
+    hist = np.zeros(nb, dtype=np.uint32)
+    bt = (_BatchRec * max(btrace_cap, 1))()
+    rl = None
+    logs = None
+    if rlog_cap > 0:
+        logs = [np.full(rlog_cap, -2.0), np.full(rlog_cap, -2.0),
+                np.full(rlog_cap, -2.0)]
+        rl = _ReqLog(logs[0].ctypes.data, logs[1].ctypes.data,
+                     logs[2].ctypes.data, rlog_cap)
+    L.oracle_run(C.byref(pin.cfg), C.c_uint64(seed), C.c_uint32(replica_id),
+                 horizon, C.byref(res), hist.ctypes.data,
+                 C.addressof(bt) if btrace_cap > 0 else None, btrace_cap,
+                 C.addressof(rl) if rl is not None else None)
+    out = {f: getattr(res, f) for f in INT_FIELDS + F64_FIELDS}
+    out["flags"] = res.flags
+    out["hist"] = hist
+    if btrace_cap > 0:
+        nbt = min(btrace_cap, res.batches)
+        out["batches_trace"] = [
+            {f: getattr(bt[i], f) for f, _ in _BatchRec._fields_ if f != "pad"}
+            for i in range(nbt)]
+    if logs is not None:
+        out["req_arr"], out["req_done"], out["req_first"] = logs
+    return out
+
+
+# -------------------------------------------------------- RNG pieces ----
+
+
+def philox(ctr, key) -> np.ndarray:
+    L = lib()
+    c = np.ascontiguousarray(np.asarray(ctr, dtype=np.uint32))
+    k = np.ascontiguousarray(np.asarray(key, dtype=np.uint32))
+    o = np.zeros(4, dtype=np.uint32)
+    L.oracle_philox4x32_10(c.ctypes.data, k.ctypes.data, o.ctypes.data)
+    return o
+
+
+def uniform(w0: int, w1: int) -> float:
+    return lib().oracle_uniform(w0, w1)
+
+
+def ln(u: float) -> float:
+    return lib().oracle_ln(u)
+
+
+def draw(seed: int, replica_id: int, j: int, k: int, lam: float,
+         cdf_row: Optional[np.ndarray] = None, out_cap: int = 0):
+    L = lib()
+    g = C.c_double()
+    Lout = C.c_int32(0)
+    row = None if cdf_row is None else np.ascontiguousarray(cdf_row, dtype=np.uint32)
+    L.oracle_draw(C.c_uint64(seed), replica_id, j, k, lam, _ptr(row), out_cap,
+                  C.byref(g), C.byref(Lout))
+    return g.value, Lout.value

@@ -1,0 +1,101 @@
+/*
+ * wait_oracle.h -- interface of the CPU oracle (test infrastructure only).
+ *
+ * The oracle is a plain, slow, event-driven simulation of the multi-stage
+ * LLM-inference queueing model of "Optimizing LLM Inference: Fluid-Guided
+ * Online Scheduling with Memory Constraints" (arXiv 2504.11320), Section 2,
+ * under the WAIT policy (Algorithm 1), the Nested WAIT policy (Algorithm 2 and
+ * its full event-driven form, Algorithm 4 of Appendix B.1) and the greedy FCFS
+ * evict-on-overflow baseline (Section 4.1, made exact by the proof of
+ * Proposition 3).  It keeps one record per request and re-derives every
+ * decision from those records each iteration.
+ *
+ * Only tests, the smoke check and the CPU-baseline leg of the benchmark may
+ * load this library.  It shares no code, header or constant with the GPU
+ * library; the two agree only through the written model contract.
+ */
+#ifndef WAIT_ORACLE_H
+#define WAIT_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OR_WAIT 0
+#define OR_NESTED 1
+#define OR_FCFS 2
+
+#define OR_FLAG_CAPACITY 1u
+#define OR_FLAG_STALL 2u
+#define OR_FLAG_OVERFLOW 4u
+
+typedef struct {
+  int32_t m;                /* request types                                   */
+  const int32_t *l;         /* prompt length l_j [m]                           */
+  const double *lambda;     /* Poisson rate lambda_j per ms [m]                */
+  const int32_t *lp;        /* known output length l'_j [m], or NULL           */
+  int32_t out_cap;          /* output-length cap (distribution mode)           */
+  const uint32_t *cdf;      /* [m][out_cap-1] u32 CDF thresholds               */
+  double d0, d1;            /* iteration time d0 + d1 * tokens                 */
+  int64_t C;                /* KV budget in tokens                             */
+  const double *edges;      /* latency histogram edges [n_edges] or NULL       */
+  int32_t n_edges;
+  int64_t record_capacity;  /* external-queue capacity                         */
+  const double *tr_time;    /* trace mode: arrival times [n_trace]             */
+  const int32_t *tr_type;   /* trace mode: types [n_trace]                     */
+  const int32_t *tr_L;      /* trace mode: output lengths [n_trace] or NULL    */
+  int64_t n_trace;
+  int32_t policy;           /* OR_WAIT / OR_NESTED / OR_FCFS                   */
+  const int32_t *n;         /* thresholds: WAIT [m], NESTED [nseg]             */
+  int32_t nseg;             /* NESTED: number of segments                      */
+  const int32_t *seg_end;   /* NESTED: r_1 < ... < r_nseg                      */
+  double reserve;           /* FCFS: admission reserve fraction of C           */
+} or_config;
+
+typedef struct {
+  int64_t batches, arrivals, completions, completed_tokens, evictions,
+      evicted_tokens, fallback_evictions, batch_tokens_sum, peak_mem,
+      waiting_end, resident_end, idle_waits;
+  double t_end, busy_time, lat_area, ttft_area, lat_completed_sum, mem_area;
+  uint32_t flags;
+  uint32_t pad;
+} or_result;
+
+/* One record per batch, for hand-trace tests. */
+typedef struct {
+  double t_launch, tau;
+  int64_t tokens, prefills, selected, completions, evict_pre, evict_post,
+      mem_after, waiting_after, resident_after, pad;
+} or_batch_rec;
+
+/* Optional per-request log (request id = arrival order, 0-based). */
+typedef struct {
+  double *arr;   /* arrival time            [cap] */
+  double *done;  /* completion time or -1   [cap] */
+  double *first; /* first-token time or -1  [cap] */
+  int64_t cap;
+} or_req_log;
+
+int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
+               int64_t horizon, or_result *out, uint32_t *hist,
+               or_batch_rec *btrace, int64_t btrace_cap, or_req_log *rlog);
+
+int oracle_run_many(const or_config *cfg, uint64_t seed,
+                    const uint32_t *replica_ids, int32_t n_replicas,
+                    int64_t horizon, or_result *out, uint32_t *hist,
+                    int32_t n_threads);
+
+/* Building blocks, exported for the pinning tests. */
+void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
+                          uint32_t out[4]);
+double oracle_uniform(uint32_t w0, uint32_t w1);
+double oracle_ln(double u);
+void oracle_draw(uint64_t seed, uint32_t replica_id, int32_t type,
+                 uint32_t k, double lambda, const uint32_t *cdf_row,
+                 int32_t out_cap, double *gap, int32_t *L);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
