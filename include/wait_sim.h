@@ -1,0 +1,196 @@
+/*
+ * wait_sim.h -- C ABI of the batched Monte Carlo simulator (MI355X / gfx950).
+ *
+ * The library simulates many independent replicas of the multi-stage
+ * LLM-inference queueing model of "Optimizing LLM Inference: Fluid-Guided
+ * Online Scheduling with Memory Constraints" (arXiv 2504.11320):
+ *
+ *   - m request types; type j arrives as a Poisson process of rate lambda_j
+ *     (Section 2.1), has prompt length l_j and output length l'_j (known), or
+ *     an output length drawn per request from a CDF table (unknown lengths,
+ *     Section 5.1);
+ *   - a batch B takes tau(B) = d0 + d1 * sum_{i in B} (l_i + s_i) where s_i is
+ *     the stage being processed, 0 for prefill (eq. time_consump, Section 2.2);
+ *   - GPU-resident prompts hold KV cache l_i + s_i and the sum must stay
+ *     <= C (eq. memory_constraint, Section 2.3); overflow evicts the most
+ *     recently admitted prompt, which restarts from prefill;
+ *   - policies: WAIT (Algorithm 1, Section 4.2), Nested WAIT (Algorithm 2,
+ *     Section 5.1; event-driven form Algorithm 4, Appendix B.1) and the greedy
+ *     FCFS evict-on-overflow baseline (Section 4.1);
+ *   - metrics: effective throughput, latency and time to first token
+ *     censored at the horizon T (Section 2.4).
+ *
+ * Units: lengths in tokens, times in milliseconds, rates per millisecond.
+ * One "batch" is one iteration: launch, then completion.  The horizon of a
+ * call counts batches per replica; waiting for arrivals while nothing is
+ * eligible is not a batch.
+ *
+ * Randomness: Philox4x32-10 keyed by the 64-bit stream seed with counter
+ * (k, j, replica_id, 0) for the k-th arrival of type j; uniform
+ * u = (2x+1) 2^-53 from x = (w0 << 20) | (w1 >> 12); inter-arrival gap
+ * -ln(u)/lambda_j; unknown output length = smallest s in 1..cap-1 with
+ * w2 < T_j[s], else cap.  A replica's arrival path therefore depends only on
+ * (seed, replica_id, lambda), identical across policies and thresholds.
+ *
+ * Memory ownership: every pointer in the config structs is HOST memory read
+ * during the call only.  d_workspace and d_results are DEVICE memory owned by
+ * the caller and sized by wait_sim_workspace_bytes / wait_sim_results_bytes.
+ * The library allocates no device memory, keeps no pointer after a call
+ * returns, and launches its kernels on the caller's stream.  Calls on one
+ * workspace must be serialised by the caller (same stream).
+ *
+ * Errors: functions return a ws_status.  Validation failures return
+ * WS_EINVAL before anything is launched; wait_sim_last_error() then holds a
+ * message (thread-local, valid until the next call on the same thread).
+ * Conditions met by individual replicas at run time are reported in that
+ * replica's flags word, never by aborting the launch.
+ */
+#ifndef WAIT_SIM_H
+#define WAIT_SIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WS_ABI_VERSION 1
+
+typedef enum {
+  WS_OK = 0,
+  WS_EINVAL = -1,      /* invalid configuration or arguments              */
+  WS_ENOMEM = -2,      /* host allocation failed                          */
+  WS_EDEVICE = -3,     /* HIP runtime error                               */
+  WS_EWORKSPACE = -4,  /* workspace or result buffer too small            */
+  WS_EUNSUPPORTED = -5 /* valid model, but outside this build's limits    */
+} ws_status;
+
+typedef enum { WS_WAIT = 0, WS_NESTED_WAIT = 1, WS_FCFS = 2 } ws_policy_kind;
+
+/* Per-replica flags (result field "flags"). */
+#define WS_FLAG_CAPACITY 1u /* an external queue exceeded record_capacity;
+                               the replica stopped at its next decision     */
+#define WS_FLAG_STALL 2u    /* nothing eligible and no further arrival       */
+#define WS_FLAG_OVERFLOW 4u /* Nested WAIT launched with a projected state
+                               above C after every allowed eviction          */
+
+/* Limits of this build. */
+#define WS_MAX_TYPES 16
+#define WS_MAX_SEGMENTS 16
+#define WS_MAX_HIST_EDGES 255
+
+/* The model (Section 2). */
+typedef struct {
+  int32_t m;                    /* request types, 1..WS_MAX_TYPES            */
+  const int32_t *prompt_len;    /* l_j >= 1                         [m]      */
+  const double *lambda;         /* lambda_j >= 0, per ms            [m]      */
+  const int32_t *out_len;       /* known output length l'_j >= 1    [m], or
+                                   NULL for the distribution mode below      */
+  int32_t out_cap;              /* distribution mode: largest output length  */
+  const uint32_t *out_cdf_u32;  /* distribution mode: [m][out_cap-1] row j,
+                                   entry s-1 = T_j[s], nondecreasing in s    */
+  double d0;                    /* fixed time per iteration, > 0             */
+  double d1;                    /* time per cached token, >= 0               */
+  int64_t C;                    /* KV-cache budget in tokens, <= 2^30        */
+  const double *hist_edges;     /* latency histogram edges (ms), strictly
+                                   increasing, or NULL                       */
+  int32_t n_hist;               /* number of edges, 0..WS_MAX_HIST_EDGES     */
+  int32_t record_capacity;      /* capacity of each external queue, a power
+                                   of two >= 16                              */
+  /* Trace mode (test hook): if n_trace > 0 these arrivals, in this order,
+     replace the random arrivals of every replica.                          */
+  const double *trace_time;     /* nondecreasing arrival times     [n_trace] */
+  const int32_t *trace_type;    /* type of each arrival            [n_trace] */
+  const int32_t *trace_out_len; /* output length (distribution mode)        */
+  int64_t n_trace;
+} ws_config;
+
+/* The scheduling policy. */
+typedef struct {
+  int32_t kind;          /* ws_policy_kind                                   */
+  const int32_t *n;      /* WAIT: n_j >= 1 [m]; NESTED: n_k >= 1 [L]         */
+  int32_t L;             /* NESTED: number of segments, 1..WS_MAX_SEGMENTS   */
+  const int32_t *seg_end;/* NESTED: r_1 < ... < r_L, r_L = largest output    */
+  double fcfs_reserve;   /* FCFS: fraction of C kept free at admission, [0,1)*/
+} ws_policy;
+
+/* One replica's random stream. */
+typedef struct {
+  uint64_t seed;
+  uint32_t replica_id;
+  uint32_t reserved;
+} ws_stream;
+
+/* A group of replicas sharing a model and a policy. */
+typedef struct {
+  const ws_config *cfg;
+  const ws_policy *pol;
+  const ws_stream *streams; /* [n] */
+  int32_t n;
+} ws_job;
+
+/* Result layout (device buffer, structure of arrays over the R replicas of
+ * all jobs, in job order):
+ *   int64  [WS_NI64][R] : batches, arrivals, completions, completed_tokens,
+ *                         evictions, evicted_tokens, fallback_evictions,
+ *                         batch_tokens_sum, peak_mem, waiting_end,
+ *                         resident_end, idle_waits
+ *   double [WS_NF64][R] : t_end (T), busy_time, lat_area (sum of censored
+ *                         latencies = integral of N dt), ttft_area (sum of
+ *                         censored times to first token), lat_completed_sum,
+ *                         mem_area (integral of launch memory over batches
+ *                         and resident memory while idle)
+ *   uint32 [R]          : flags
+ *   uint32 [R][H]       : latency histogram of completed requests, bin b =
+ *                         number of edges <= latency; H = hist stride
+ *                         returned by wait_sim_results_bytes.
+ * Byte offsets: i64 at 0, f64 at 8*WS_NI64*R, flags at 8*(WS_NI64+WS_NF64)*R,
+ * histogram at that plus 4*R rounded up to a multiple of 8.
+ * Results are cumulative over the calls that advanced the same workspace. */
+#define WS_NI64 12
+#define WS_NF64 6
+
+/* Bytes of device workspace needed for these jobs. */
+int wait_sim_workspace_bytes(const ws_job *jobs, int32_t n_jobs,
+                             size_t *bytes);
+
+/* Bytes of the result buffer and the histogram stride H (>= 1). */
+int wait_sim_results_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes,
+                           int32_t *hist_stride);
+
+/* Validate the jobs and copy their tables into the workspace.  Blocks the
+ * host until the copy on hip_stream (hipStream_t, or NULL for the default
+ * stream) has finished. */
+int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
+                     size_t ws_bytes, void *hip_stream);
+
+/* Advance every replica of a prepared workspace by `horizon` batches.
+ * resume = 0 starts every replica from the empty system at t = 0;
+ * resume = 1 continues from the state the previous call left.  Asynchronous
+ * on hip_stream; `jobs` must be the ones given to wait_sim_prepare. */
+int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                     int32_t resume, void *d_workspace, size_t ws_bytes,
+                     void *d_results, size_t results_bytes, void *hip_stream);
+
+/* prepare + advance(resume = 0) for one job. */
+int wait_sim_run(const ws_config *cfg, const ws_policy *pol,
+                 const ws_stream *streams, int32_t n_replicas, int64_t horizon,
+                 void *d_workspace, size_t ws_bytes, void *d_results,
+                 size_t results_bytes, void *hip_stream);
+
+/* prepare + advance(resume = 0) for several jobs in one launch per policy. */
+int wait_sim_run_batch(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                       void *d_workspace, size_t ws_bytes, void *d_results,
+                       size_t results_bytes, void *hip_stream);
+
+/* Message of the last failure on this thread ("" if none). */
+const char *wait_sim_last_error(void);
+
+/* ABI version compiled into the library (WS_ABI_VERSION). */
+int wait_sim_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

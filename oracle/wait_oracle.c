@@ -774,7 +774,8 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
       out->mem_area += (double)S.Mres * dt;
       S.t = ta;
       /* every arrival at this instant joins before the next decision */
-      while (peek_arrival(&S, &j) == ta) take_arrival(&S);
+      while (!(out->flags & OR_FLAG_CAPACITY) && peek_arrival(&S, &j) == ta)
+        take_arrival(&S);
       out->idle_waits++;
     }
     if (stop) break;
@@ -791,6 +792,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
     int64_t N0 = S.N, U0 = S.U;
     for (;;) {
       int32_t j;
+      if (out->flags & OR_FLAG_CAPACITY) break; /* the replica stops anyway */
       double ta = peek_arrival(&S, &j);
       if (!(ta <= t_end)) break;
       take_arrival(&S);

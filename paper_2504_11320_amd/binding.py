@@ -1,0 +1,249 @@
+"""Python binding of the C ABI in include/wait_sim.h (argument marshalling only).
+
+Every simulation step runs in the HIP library; this module only converts
+workload descriptions into the C structs, allocates device buffers through
+PyTorch and passes the current HIP stream.  It raises if the library is
+missing instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Sequence
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libwait_sim.so")
+
+WS_OK, WS_EINVAL, WS_ENOMEM, WS_EDEVICE, WS_EWORKSPACE, WS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+WS_WAIT, WS_NESTED_WAIT, WS_FCFS = 0, 1, 2
+WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW = 1, 2, 4
+WS_NI64, WS_NF64 = 12, 6
+POLICY = {"wait": WS_WAIT, "nested": WS_NESTED_WAIT, "fcfs": WS_FCFS}
+
+I64_FIELDS = ["batches", "arrivals", "completions", "completed_tokens",
+              "evictions", "evicted_tokens", "fallback_evictions",
+              "batch_tokens_sum", "peak_mem", "waiting_end", "resident_end",
+              "idle_waits"]
+F64_FIELDS = ["t_end", "busy_time", "lat_area", "ttft_area",
+              "lat_completed_sum", "mem_area"]
+
+
+class WsConfig(C.Structure):
+    _fields_ = [
+        ("m", C.c_int32), ("prompt_len", C.c_void_p), ("lam", C.c_void_p),
+        ("out_len", C.c_void_p), ("out_cap", C.c_int32),
+        ("out_cdf_u32", C.c_void_p), ("d0", C.c_double), ("d1", C.c_double),
+        ("C", C.c_int64), ("hist_edges", C.c_void_p), ("n_hist", C.c_int32),
+        ("record_capacity", C.c_int32), ("trace_time", C.c_void_p),
+        ("trace_type", C.c_void_p), ("trace_out_len", C.c_void_p),
+        ("n_trace", C.c_int64),
+    ]
+
+
+class WsPolicy(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("n", C.c_void_p), ("L", C.c_int32),
+                ("seg_end", C.c_void_p), ("fcfs_reserve", C.c_double)]
+
+
+class WsStream(C.Structure):
+    _fields_ = [("seed", C.c_uint64), ("replica_id", C.c_uint32),
+                ("reserved", C.c_uint32)]
+
+
+class WsJob(C.Structure):
+    _fields_ = [("cfg", C.POINTER(WsConfig)), ("pol", C.POINTER(WsPolicy)),
+                ("streams", C.c_void_p), ("n", C.c_int32)]
+
+
+class WaitSimError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"wait_sim error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with paper_2504_11320_amd/build.py")
+        L = C.CDLL(LIB_PATH)
+        jp = C.POINTER(WsJob)
+        L.wait_sim_workspace_bytes.argtypes = [jp, C.c_int32, C.POINTER(C.c_size_t)]
+        L.wait_sim_results_bytes.argtypes = [jp, C.c_int32, C.POINTER(C.c_size_t),
+                                             C.POINTER(C.c_int32)]
+        L.wait_sim_prepare.argtypes = [jp, C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.wait_sim_advance.argtypes = [jp, C.c_int32, C.c_int64, C.c_int32, C.c_void_p,
+                                       C.c_size_t, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.wait_sim_run.argtypes = [C.POINTER(WsConfig), C.POINTER(WsPolicy), C.c_void_p,
+                                   C.c_int32, C.c_int64, C.c_void_p, C.c_size_t,
+                                   C.c_void_p, C.c_size_t, C.c_void_p]
+        L.wait_sim_run_batch.argtypes = [jp, C.c_int32, C.c_int64, C.c_void_p,
+                                         C.c_size_t, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.wait_sim_last_error.restype = C.c_char_p
+        L.wait_sim_abi_version.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != WS_OK:
+        raise WaitSimError(rc, lib().wait_sim_last_error().decode())
+
+
+class JobArray:
+    """C structs for a list of jobs; keeps the host arrays alive."""
+
+    def __init__(self, jobs: Sequence):
+        self.keep = []
+        self.cfgs = []
+        self.pols = []
+        self.n_jobs = len(jobs)
+        self.arr = (WsJob * max(1, len(jobs)))()
+        self.replicas = 0
+        for i, job in enumerate(jobs):
+            wl = job.wl
+            cfg = WsConfig()
+            cfg.m = wl.m
+            cfg.prompt_len = self._a(wl.prompt_len, np.int32)
+            cfg.lam = self._a(wl.lam, np.float64)
+            cfg.out_len = None if wl.out_len is None else self._a(wl.out_len, np.int32)
+            cfg.out_cap = int(wl.out_cap)
+            cfg.out_cdf_u32 = None if wl.out_cdf is None else self._a(wl.out_cdf, np.uint32)
+            cfg.d0, cfg.d1, cfg.C = float(wl.d0), float(wl.d1), int(wl.C)
+            if wl.hist_edges is None:
+                cfg.hist_edges, cfg.n_hist = None, 0
+            else:
+                cfg.hist_edges = self._a(wl.hist_edges, np.float64)
+                cfg.n_hist = len(wl.hist_edges)
+            cfg.record_capacity = int(wl.record_capacity)
+            if wl.trace is not None:
+                t, ty, L = wl.trace
+                cfg.trace_time = self._a(t, np.float64)
+                cfg.trace_type = self._a(ty, np.int32)
+                cfg.trace_out_len = self._a(L, np.int32)
+                cfg.n_trace = len(t)
+            else:
+                cfg.trace_time = cfg.trace_type = cfg.trace_out_len = None
+                cfg.n_trace = 0
+            pol = WsPolicy()
+            pol.kind = POLICY[wl.policy]
+            pol.n = self._a(wl.n if len(wl.n) else [0], np.int32)
+            pol.L = len(wl.seg_end) if wl.seg_end is not None else 0
+            pol.seg_end = None if wl.seg_end is None else self._a(wl.seg_end, np.int32)
+            pol.fcfs_reserve = float(wl.reserve)
+            ids = np.asarray(job.replica_ids, dtype=np.uint32)
+            st = (WsStream * max(1, len(ids)))()
+            for x, rid in enumerate(ids):
+                st[x].seed = int(job.seed)
+                st[x].replica_id = int(rid)
+                st[x].reserved = 0
+            self.keep.append(st)
+            self.cfgs.append(cfg)
+            self.pols.append(pol)
+            self.arr[i].cfg = C.pointer(cfg)
+            self.arr[i].pol = C.pointer(pol)
+            self.arr[i].streams = C.addressof(st)
+            self.arr[i].n = len(ids)
+            self.replicas += len(ids)
+
+    def _a(self, x, dt):
+        a = np.ascontiguousarray(np.asarray(x, dtype=dt))
+        self.keep.append(a)
+        return a.ctypes.data
+
+    @property
+    def ptr(self):
+        return C.cast(self.arr, C.POINTER(WsJob))
+
+
+def workspace_bytes(ja: JobArray) -> int:
+    b = C.c_size_t()
+    _check(lib().wait_sim_workspace_bytes(ja.ptr, ja.n_jobs, C.byref(b)))
+    return int(b.value)
+
+
+def results_bytes(ja: JobArray):
+    b = C.c_size_t()
+    h = C.c_int32()
+    _check(lib().wait_sim_results_bytes(ja.ptr, ja.n_jobs, C.byref(b), C.byref(h)))
+    return int(b.value), int(h.value)
+
+
+def _stream_handle(torch, device):
+    return C.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+class Simulation:
+    """Device buffers for one set of jobs, advanced through the C ABI."""
+
+    def __init__(self, jobs: Sequence, device: str = "cuda:0"):
+        import torch
+        self.torch = torch
+        self.device = torch.device(device)
+        self.ja = JobArray(jobs)
+        self.ws_bytes = workspace_bytes(self.ja)
+        self.res_bytes, self.hist_stride = results_bytes(self.ja)
+        self.R = self.ja.replicas
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        self.res = torch.zeros(self.res_bytes, dtype=torch.uint8, device=self.device)
+        self.prepared = False
+
+    def prepare(self):
+        with self.torch.cuda.device(self.device):
+            _check(lib().wait_sim_prepare(self.ja.ptr, self.ja.n_jobs, self.ws.data_ptr(),
+                                          self.ws_bytes, _stream_handle(self.torch, self.device)))
+        self.prepared = True
+
+    def advance(self, horizon: int, resume: bool = False):
+        if not self.prepared:
+            self.prepare()
+        with self.torch.cuda.device(self.device):
+            _check(lib().wait_sim_advance(self.ja.ptr, self.ja.n_jobs, int(horizon),
+                                          1 if resume else 0, self.ws.data_ptr(),
+                                          self.ws_bytes, self.res.data_ptr(), self.res_bytes,
+                                          _stream_handle(self.torch, self.device)))
+
+    def results(self) -> dict:
+        """Per-replica results as numpy arrays (synchronises the stream)."""
+        host = self.res.cpu().numpy()
+        R = self.R
+        out = {}
+        i64 = host[: 8 * WS_NI64 * R].view(np.int64).reshape(WS_NI64, R)
+        for k, f in enumerate(I64_FIELDS):
+            out[f] = i64[k].copy()
+        f64 = host[8 * WS_NI64 * R: 8 * (WS_NI64 + WS_NF64) * R].view(np.float64)
+        f64 = f64.reshape(WS_NF64, R)
+        for k, f in enumerate(F64_FIELDS):
+            out[f] = f64[k].copy()
+        off = 8 * (WS_NI64 + WS_NF64) * R
+        out["flags"] = host[off: off + 4 * R].view(np.uint32).copy()
+        hoff = (off + 4 * R + 7) // 8 * 8
+        out["hist"] = host[hoff: hoff + 4 * R * self.hist_stride].view(np.uint32).reshape(
+            R, self.hist_stride).copy()
+        return out
+
+
+def run_batch(jobs: Sequence, horizon: int, device: str = "cuda:0") -> dict:
+    """prepare + advance for a list of jobs; returns per-replica results."""
+    sim = Simulation(jobs, device)
+    sim.prepare()
+    sim.advance(horizon, resume=False)
+    return sim.results()
+
+
+def split_by_job(res: dict, jobs: Sequence) -> list:
+    """Split per-replica result arrays into one dict per job."""
+    out = []
+    start = 0
+    for job in jobs:
+        n = len(job.replica_ids)
+        out.append({k: v[start:start + n] for k, v in res.items()})
+        start += n
+    return out

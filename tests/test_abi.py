@@ -1,0 +1,70 @@
+"""The C-ABI library: loads, exports every declared symbol, validates input.
+
+These run without a GPU: sizing and validation are host-only."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "wait_sim.h")).read()
+    return sorted(set(re.findall(r"^\w[\w\s\*]*?\b(wait_sim_\w+)\s*\(", src, re.M)))
+
+
+def test_library_exports_header_symbols():
+    from paper_2504_11320_amd import binding as B
+    lib = B.lib()
+    names = _declared()
+    assert "wait_sim_run" in names and "wait_sim_advance" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.wait_sim_abi_version() == 1
+
+
+def _err(jobs):
+    from paper_2504_11320_amd import binding as B
+    with pytest.raises(B.WaitSimError) as e:
+        B.workspace_bytes(B.JobArray(jobs))
+    return e.value
+
+
+def _job(**kw):
+    wl = W.config2(replicas=2, rate_index=[3])[0].wl
+    for k, v in kw.items():
+        setattr(wl, k, v)
+    return [W.Job(wl, 0, W.ids(2))]
+
+
+def test_validation_errors():
+    from paper_2504_11320_amd import binding as B
+    assert _err(_job(d0=0.0)).code == B.WS_EINVAL
+    assert _err(_job(d1=-1.0)).code == B.WS_EINVAL
+    assert _err(_job(prompt_len=[0, 512, 1024])).code == B.WS_EINVAL
+    assert _err(_job(lam=[-1.0, 0.1, 0.1])).code == B.WS_EINVAL
+    assert _err(_job(n=[0, 1, 1])).code == B.WS_EINVAL
+    assert _err(_job(record_capacity=1000)).code == B.WS_EINVAL
+    # atomic feasibility: l_j + l'_j <= C
+    assert _err(_job(C=1500)).code == B.WS_EINVAL
+    assert _err(_job(hist_edges=np.array([1.0, 1.0]))).code == B.WS_EINVAL
+    e = _err(_job(policy="nested", seg_end=[64, 256, 512]))
+    assert e.code in (B.WS_EINVAL, B.WS_EUNSUPPORTED)
+    # a well-formed job sizes without error
+    ja = B.JobArray(_job())
+    assert B.workspace_bytes(ja) > 0
+    nb, hs = B.results_bytes(ja)
+    assert hs == 193 and nb >= 2 * (8 * 18 + 4 + 4 * 193)
+
+
+def test_fcfs_reserve_validation():
+    from paper_2504_11320_amd import binding as B
+    jobs = W.config4(replicas=1, grid=1, n_rates=2)
+    fc = [j for j in jobs if j.wl.policy == "fcfs"][:1]
+    fc[0].wl.reserve = 1.0
+    assert _err(fc).code == B.WS_EINVAL

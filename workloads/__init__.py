@@ -128,7 +128,7 @@ def c2_rates(n_rates: int = 32) -> List[float]:
 
 
 def config2(replicas: int = 1024, n_rates: int = 32, rate_index=None,
-            record_capacity: int = 1 << 14) -> List[Job]:
+            record_capacity: int = 1 << 15) -> List[Job]:
     """WAIT, Llama-2-7B-shaped synthetic: 3 types, prompts (128, 512, 1024),
     outputs (64, 256, 512), mix (0.5, 0.3, 0.2), C = 131072,
     15 ms + 0.05 ms/token, thresholds (1, 1, 1), rates spanning 0.5-1.2x the
