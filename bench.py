@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark: simulated replica-iterations per second on one MI355X.
+
+One step is one pass of the whole simulation over the benchmark workload:
+the Llama-2-7B-shaped WAIT workload (3 request types, prompts 128/512/1024,
+outputs 64/256/512, mix 0.5/0.3/0.2, KV budget 131072 tokens, iteration time
+15 ms + 0.05 ms/token, thresholds (1,1,1)) at 32 arrival rates spanning
+0.5-1.2x the fluid stability boundary, 1024 replicas per rate, 1e5 batches
+per replica: 3.2768e9 replica-iterations per step.  Inputs (job tables) are
+copied to HBM before the timed region; every replica starts from the empty
+system in every step.
+
+Prints one JSON line.  The roofline object prices the simulation kernel
+against the ALU peak with an explicit operation model (lane-operations the
+method needs per arrival, batch, completion, eviction and idle wait; see the
+design notes), using the event counts the kernel itself returns.  The
+cpu_baseline object times the CPU oracle on a bounded sample of the same
+workload (2 rates x 64 replicas x the full horizon) on the host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "simulated replica-iterations/sec (1 GPU) + % of VALU/HBM roofline"
+UNIT = "replica-iterations/s"
+
+# MI355X: 256 compute units x 4 SIMD x 16 lanes per clock at 2.4 GHz = 64
+# lane-operations per CU per clock (full-rate VALU, fp64 included).
+CUS, LANES_PER_CU_CLK, CLOCK_HZ = 256, 64, 2.4e9
+ALU_PEAK = CUS * LANES_PER_CU_CLK * CLOCK_HZ          # 3.93e13 lane-ops/s
+HBM_PEAK = 8.0e12                                     # bytes/s
+
+KERNEL_SRC = os.path.join(ROOT, "paper_2504_11320_amd", "csrc", "wait_sim.hip")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_kernel_wait_config2_hbm.md")
+
+
+def op_model(m: int) -> dict:
+    """Algorithmic lane-operations per event (full-rate VALU instruction
+    equivalents; a 32x32->64-bit multiply counts 4)."""
+    philox = 10 * (2 * 4 + 4 + 2)     # 2 wide multiplies, 4 xor, 2 key adds per round
+    uniform = 10                      # 52-bit assembly, int->fp64, scale
+    ln = 50                           # reduction, one fp64 division, 12-term Horner, e*ln2
+    gap = 14                          # fp64 division by lambda, add to the clock
+    book = 12                         # queue push, counters, area terms
+    return {
+        "arrival": philox + uniform + ln + gap + book + 2 * m,
+        "batch": 24 + 6 * m,          # eligibility, tokens, tau, clock, areas, peak
+        "completion": 35,             # latency, sum, histogram search and update
+        "eviction": 14 + 3 * m,       # LIFO choice, stage, memory, re-queue
+        "idle": 15 + 4 * m,           # next arrival, area terms, eligibility
+    }
+
+
+def algorithmic_ops(res: dict, m: int) -> float:
+    c = op_model(m)
+    return float(c["batch"] * res["batches"].sum() + c["arrival"] * res["arrivals"].sum()
+                 + c["completion"] * res["completions"].sum()
+                 + c["eviction"] * res["evictions"].sum() + c["idle"] * res["idle_waits"].sum())
+
+
+def algorithmic_bytes(res: dict) -> float:
+    """Record traffic the method needs: 16 B written and read per queued
+    request (arrival and re-queue) and per admission/completion."""
+    ev = res["arrivals"].sum() + res["evictions"].sum()
+    return float(16 * 2 * ev + 16 * res["completions"].sum())
+
+
+def source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_profile():
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    txt = open(PMC_SUMMARY).read()
+    h = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt)
+    b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not h or not b or h.group(1) != source_hash():
+        return None
+    return float(b.group(1))
+
+
+def cpu_baseline(horizon: int, replicas: int, threads: int) -> dict:
+    from oracle import oracle as O
+    import workloads as W
+    jobs = W.config2(replicas=replicas, rate_index=[0, 31])
+    t0 = time.perf_counter()
+    total = 0
+    for job in jobs:
+        r = O.run_job(job, horizon, threads=threads)
+        total += int(r["batches"].sum())
+    dt = time.perf_counter() - t0
+    return {"value": total / dt, "unit": UNIT, "cores": threads, "kind": "oracle",
+            "sample": f"rates 0 and 31 of 32 x {replicas} replicas x {horizon} batches "
+                      f"({total} replica-iterations, {dt:.1f} s)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--horizon", type=int, default=100000)
+    ap.add_argument("--replicas", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-replicas", type=int, default=64)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (used to "
+                         "scale the HBM byte counters)")
+    args = ap.parse_args()
+
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration << 20
+        a = torch.ones(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "launches": 3}))
+        return 0
+
+    if args.gpus != 1:
+        print(f"bench.py: this simulator runs on one GPU; --gpus {args.gpus} is not "
+              f"supported (replicas shard across GPUs with no communication, but this "
+              f"build measures a single MI355X)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2504_11320_amd import binding as B
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    B.lib()  # fails loudly if the HIP library is missing
+
+    jobs = W.config2(replicas=args.replicas)
+    m = jobs[0].wl.m
+    sim = B.Simulation(jobs)
+    sim.prepare()
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        sim.advance(args.horizon, resume=False)
+    torch.cuda.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        sim.advance(args.horizon, resume=False)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = ev0.elapsed_time(ev1)
+    ms_step = ms_total / args.steps
+
+    res = sim.results()
+    rep_its = int(res["batches"].sum())
+    if rep_its != len(res["batches"]) * args.horizon or np.any(res["flags"]):
+        print("bench.py: some replicas stopped early (flags set)", file=sys.stderr)
+    value = rep_its / (ms_step / 1e3)
+
+    ops = algorithmic_ops(res, m)
+    achieved = ops / (ms_step / 1e3)
+    traffic = traffic_from_profile()
+    roofline = {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK,
+                "unit": "lane-ops/s", "frac": achieved / ALU_PEAK,
+                "traffic": traffic,
+                "algorithmic_ops_per_replica_iteration": ops / rep_its,
+                "algorithmic_bytes_per_launch": algorithmic_bytes(res),
+                "kernel": "sim_known_kernel<4, WAIT>"}
+
+    out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f64", "data": "synthetic",
+           "config": {"workload": "WAIT, Llama-2-7B-shaped 3-type synthetic mix, "
+                                  "32 rates 0.5-1.2x fluid boundary",
+                      "replicas": len(res["batches"]), "rates": len(jobs),
+                      "replicas_per_rate": args.replicas, "horizon_batches": args.horizon,
+                      "replica_iterations_per_step": rep_its, "policy": "wait",
+                      "kv_budget_tokens": 131072},
+           "roofline": roofline,
+           "wall_s_timed": wall}
+    if not args.no_cpu_baseline:
+        threads = max(1, min(os.cpu_count() or 1, 16))
+        out["cpu_baseline"] = cpu_baseline(args.horizon, args.cpu_replicas, threads)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
