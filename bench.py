@@ -39,7 +39,7 @@ CUS, LANES_PER_CU_CLK, CLOCK_HZ = 256, 64, 2.4e9
 ALU_PEAK = CUS * LANES_PER_CU_CLK * CLOCK_HZ          # 3.93e13 lane-ops/s
 HBM_PEAK = 8.0e12                                     # bytes/s
 
-KERNEL_SRC = os.path.join(ROOT, "paper_2504_11320_amd", "csrc", "wait_sim.hip")
+KERNEL_SRC = os.path.join(ROOT, "paper_2504_11320_amd", "csrc", "sim_known.hip")
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_kernel_wait_config2_hbm.md")
 
 

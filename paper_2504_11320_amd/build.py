@@ -7,7 +7,8 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRC = os.path.join(PKG, "csrc", "wait_sim.hip")
+CSRC = os.path.join(PKG, "csrc")
+SRCS = [os.path.join(CSRC, f) for f in ("wait_sim_host.hip", "sim_known.hip", "sim_nested.hip")]
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libwait_sim.so")
 
@@ -29,7 +30,7 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INC, "-o", LIB + ".tmp", SRC]
+    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INC, "-I", CSRC, "-o", LIB + ".tmp"] + SRCS
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -1,0 +1,238 @@
+// sim_common.h -- definitions shared by the simulation kernels and the host
+// library: the device job descriptor, the per-replica state slots, the
+// launch arguments, the random-number pieces and the request records.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "wait_sim.h"
+
+namespace wsim {
+
+constexpr int kMaxTypes = WS_MAX_TYPES;
+constexpr int kMaxSeg = WS_MAX_SEGMENTS;
+constexpr uint32_t kFlagCap = WS_FLAG_CAPACITY;
+constexpr uint32_t kFlagStall = WS_FLAG_STALL;
+constexpr uint32_t kFlagOverflow = WS_FLAG_OVERFLOW;
+constexpr uint32_t kNil = 0xFFFFFFFFu;
+
+// One job (a model + policy shared by a group of replicas), in device memory.
+struct JobDev {
+  int32_t m, policy, n_hist, out_cap;
+  int32_t nseg, known, qcap_log2, rec_cap;
+  double d0, d1;
+  int64_t C, reserve_tok;
+  int64_t n_trace;
+  int64_t replica_begin;
+  int32_t l[kMaxTypes], lp[kMaxTypes], n[kMaxTypes];
+  int32_t dcap_log2[kMaxTypes];
+  double lambda[kMaxTypes];
+  // Nested WAIT segments (index k = 0..nseg-1 is the paper's segment k+1)
+  int32_t seg_end[kMaxSeg];    // r_k
+  int32_t seg_n[kMaxSeg];      // n_k
+  int32_t seg_entry[kMaxSeg];  // processing stage of an entering prompt
+  int32_t seg_delta[kMaxSeg];  // number of processing stages (cohort slots)
+  int32_t vcap_log2[kMaxSeg];  // boundary-queue ring size (k >= 1)
+  uint64_t off_edges, off_cdf, off_tr_time, off_tr_type, off_tr_len;
+  uint64_t off_ring, ring_stride;
+  uint64_t off_q[kMaxTypes];    // queue rings inside a replica block
+  uint64_t off_d[kMaxTypes];    // resident deques inside a replica block
+  uint64_t off_rec[kMaxSeg];    // Nested: interior records [delta][n]
+  uint64_t off_bkt[kMaxSeg];    // Nested: calendar bucket heads [delta]
+  uint64_t off_meta[kMaxSeg];   // Nested: cohort-slot live count and sum of l
+  uint64_t off_v[kMaxSeg];      // Nested: boundary-queue rings (k >= 1)
+};
+
+// Per-replica state slots (8 bytes each), stored [slot][R].
+enum Slot : int {
+  S_T = 0, S_LAT, S_TTFT, S_LATSUM, S_MEM, S_BUSY,          // f64
+  S_BATCHES, S_ARR, S_COMP, S_CTOK, S_EVICT, S_ETOK, S_FALLBACK, S_BTOK,
+  S_PEAK, S_IDLE, S_N, S_U, S_MRES, S_TRIDX, S_FLAGS, S_PENDFT,
+  S_TNEXT,                           // + kMaxTypes f64: next arrival time
+  S_K = S_TNEXT + kMaxTypes,         // arrival index of the pending arrival
+  S_LNEXT = S_K + kMaxTypes,         // output length of the pending arrival
+  S_QH = S_LNEXT + kMaxTypes,        // queue heads
+  S_QT = S_QH + kMaxTypes,           // queue tails
+  S_DH = S_QT + kMaxTypes,           // deque heads
+  S_DT = S_DH + kMaxTypes,           // deque tails
+  S_SVC = S_DT + kMaxTypes,          // services per type (WAIT)
+  S_MJ = S_SVC + kMaxTypes,          // resident memory per type
+  S_KSVC = S_MJ + kMaxTypes,         // Nested: services per segment
+  S_KI = S_KSVC + kMaxSeg,           // Nested: interior residents per segment
+  S_KM = S_KI + kMaxSeg,             // Nested: interior memory per segment
+  S_KB = S_KM + kMaxSeg,             // Nested: boundary-queue memory
+  S_KVH = S_KB + kMaxSeg,            // Nested: boundary-queue heads
+  S_KVT = S_KVH + kMaxSeg,           // Nested: boundary-queue tails
+  S_COUNT = S_KVT + kMaxSeg
+};
+
+struct KArgs {
+  uint8_t *ws;
+  uint64_t off_jobs, off_seed, off_rid, off_job_of, off_list, off_state,
+      off_hist;
+  int64_t R;           // total replicas
+  int32_t n_list;      // replicas in this launch
+  int32_t hist_stride;
+  int64_t horizon;
+  int32_t resume;
+};
+
+__device__ __forceinline__ int64_t slot_i(const KArgs &A, int s, int64_t r) {
+  return ((const int64_t *)(A.ws + A.off_state))[s * A.R + r];
+}
+__device__ __forceinline__ double slot_f(const KArgs &A, int s, int64_t r) {
+  return ((const double *)(A.ws + A.off_state))[s * A.R + r];
+}
+__device__ __forceinline__ void put_i(const KArgs &A, int s, int64_t r, int64_t v) {
+  ((int64_t *)(A.ws + A.off_state))[s * A.R + r] = v;
+}
+__device__ __forceinline__ void put_f(const KArgs &A, int s, int64_t r, double v) {
+  ((double *)(A.ws + A.off_state))[s * A.R + r] = v;
+}
+
+// ------------------------------------------------------------------ RNG --
+
+__device__ __forceinline__ void philox10(uint32_t c0, uint32_t c1, uint32_t c2,
+                                         uint32_t c3, uint32_t k0, uint32_t k1,
+                                         uint32_t w[4]) {
+  // Philox4x32-10 (Salmon et al., SC'11).
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c1 = (uint32_t)p1;
+    c3 = (uint32_t)p0;
+    c0 = n0;
+    c2 = n2;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  w[0] = c0;
+  w[1] = c1;
+  w[2] = c2;
+  w[3] = c3;
+}
+
+// Natural logarithm of u in (0,1) from IEEE basic operations only:
+// u = f 2^e, f in [sqrt(1/2), sqrt(2)), ln f = 2 atanh(z), z = (f-1)/(f+1),
+// atanh(z) = z sum_{i=0}^{11} z^{2i}/(2i+1) in Horner form, plus e ln 2 with
+// ln 2 split into a head with zero low bits and a tail.
+__device__ __forceinline__ double ln_unit(double u) {
+  const uint64_t bits = (uint64_t)__double_as_longlong(u);
+  int e = (int)((bits >> 52) & 0x7ff) - 1022;
+  double f = __longlong_as_double(
+      (long long)((bits & 0x000fffffffffffffull) | 0x3fe0000000000000ull));
+  if (f < 0x1.6a09e667f3bcdp-1) {
+    f = f + f;
+    e = e - 1;
+  }
+  const double z = (f - 1.0) / (f + 1.0);
+  const double w = z * z;
+  double p = 1.0 / 23.0;
+  p = p * w + 1.0 / 21.0;
+  p = p * w + 1.0 / 19.0;
+  p = p * w + 1.0 / 17.0;
+  p = p * w + 1.0 / 15.0;
+  p = p * w + 1.0 / 13.0;
+  p = p * w + 1.0 / 11.0;
+  p = p * w + 1.0 / 9.0;
+  p = p * w + 1.0 / 7.0;
+  p = p * w + 1.0 / 5.0;
+  p = p * w + 1.0 / 3.0;
+  p = p * w + 1.0;
+  const double lnf = (z + z) * p;
+  const double de = (double)e;
+  return de * 0x1.62e42fefa3800p-1 + (de * 0x1.ef35793c7673p-45 + lnf);
+}
+
+// Gap to the k-th arrival of type j, and its output length when a CDF row is
+// given (smallest s in 1..cap-1 with w2 < T[s], else cap).
+__device__ __forceinline__ double draw_gap(uint64_t seed, uint32_t rid,
+                                           uint32_t j, uint32_t k, double lam,
+                                           const uint32_t *row, int32_t cap,
+                                           int32_t *L) {
+  uint32_t w[4];
+  philox10(k, j, rid, 0u, (uint32_t)seed, (uint32_t)(seed >> 32), w);
+  const uint64_t x = ((uint64_t)w[0] << 20) | (uint64_t)(w[1] >> 12);
+  const double u = (double)(2 * x + 1) * 0x1p-53;
+  if (row != nullptr) {
+    int32_t lo = 1, hi = cap;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (w[2] < row[mid - 1])
+        hi = mid;
+      else
+        lo = mid + 1;
+    }
+    *L = lo;
+  }
+  return -ln_unit(u) / lam;
+}
+
+// Histogram bin of a latency: number of edges <= lat.
+__device__ __forceinline__ int hist_bin(const double *edges, int n, double lat) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (edges[mid] <= lat)
+      lo = mid + 1;
+    else
+      hi = mid;
+  }
+  return lo;
+}
+
+// ------------------------------------------------------------- records --
+
+// The first-token flag travels in the sign bit of the arrival time.
+__device__ __forceinline__ double with_ft(double a) { return -fabs(a); }
+__device__ __forceinline__ bool has_ft(double a_ft) { return __builtin_signbit(a_ft); }
+__device__ __forceinline__ double arrival_of(double a_ft) { return fabs(a_ft); }
+
+struct DRec {   // known-length resident record, 16 bytes
+  double a_ft;  // arrival time, sign = first token produced
+  uint32_t kb;  // admission batch
+  uint32_t kc;  // WAIT: admission service of its type; FCFS: position p
+};
+
+struct QRec {   // shared FIFO record, 16 bytes
+  double a_ft;
+  int32_t j;
+  int32_t L;
+};
+
+struct NRec {   // Nested WAIT boundary / interior record, 32 bytes
+  double a_ft;  // arrival time, sign = first token produced
+  uint32_t kb;  // admission batch of the last prefill
+  uint32_t kp;  // position within that batch
+  int32_t j;    // type
+  int32_t L;    // output length; 0 marks an evicted interior slot
+  uint32_t c;   // service of its segment at which it entered
+  uint32_t next;// calendar-bucket link
+};
+
+template <typename T, int MT>
+__device__ __forceinline__ T pick(const T (&a)[MT], int j) {
+  T v = a[0];
+#pragma unroll
+  for (int i = 1; i < MT; ++i)
+    if (i == j) v = a[i];
+  return v;
+}
+
+template <typename T, int MT>
+__device__ __forceinline__ void place(T (&a)[MT], int j, T v) {
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+    if (i == j) a[i] = v;
+}
+
+// Launchers, one per kernel family (defined next to their kernels).
+hipError_t launch_known(int policy, int max_m, const KArgs &A, hipStream_t s);
+hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s);
+
+}  // namespace wsim

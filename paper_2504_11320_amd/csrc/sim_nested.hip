@@ -1,0 +1,612 @@
+// sim_nested.hip -- simulation kernel for Nested WAIT (arXiv 2504.11320:
+// Algorithm 2, Section 5.1; event-driven form Algorithm 4, Appendix B.1;
+// coarse segments with heterogeneous prompts, Appendix A).
+//
+// One lane per replica.  Per-type arrival state and per-segment counters
+// live in the lane's own column of LDS; request records live in HBM:
+//   - the external queue Q_{1,0} (FIFO ring);
+//   - for segment k >= 2 the resident boundary queue (a ring kept in
+//     admission-key order, so FIFO selection pops the front and LIFO eviction
+//     pops the back);
+//   - for every segment a ring of cohort slots indexed by the segment's
+//     service number modulo delta_k (its number of processing stages).  All
+//     prompts that entered the segment at one service form one cohort of at
+//     most n_k prompts and share a stage, so each stage holds one cohort (the
+//     stage-cap invariant of the Nested WAIT analysis) and every interior
+//     prompt of a served segment is selected.
+// A prompt's exit from its segment (completion at its own output length, or
+// survival to the next boundary queue at r_k) happens at a known service, so
+// each segment keeps a calendar: bucket (service mod delta_k) heads a linked
+// list of the prompts that exit at that service.  Cohorts are linked in
+// reverse admission order, so a bucket is traversed youngest cohort first and
+// in admission order within a cohort: the same (stage, key) order as the
+// oracle's selection list, which fixes the order of floating-point sums and
+// of survivors joining the next boundary queue.
+//
+// The projected state Q+ of the pre-launch repair (apply the selected moves
+// with no early completion) is computed from per-segment counts and the live
+// count and prompt-length sum of the terminal cohort slot.
+#include "sim_common.h"
+
+namespace wsim {
+namespace {
+
+struct SlotMeta {
+  uint32_t live;  // prompts of the cohort still in the segment
+  uint32_t suml;  // sum of their prompt lengths
+};
+
+template <int MT, int LT>
+__global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
+  __shared__ double s_tnext[MT][64];
+  __shared__ uint32_t s_k[MT][64];
+  __shared__ int32_t s_Ln[MT][64];
+  __shared__ uint32_t s_svc[LT][64], s_I[LT][64], s_vh[LT][64], s_vt[LT][64];
+  __shared__ int64_t s_M[LT][64], s_B[LT][64];
+
+  const int tx = threadIdx.x;
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tx;
+  if (gid >= A.n_list) return;  // lanes use only their own LDS column
+  const int64_t r = ((const int32_t *)(A.ws + A.off_list))[gid];
+  const uint32_t jix = ((const uint32_t *)(A.ws + A.off_job_of))[r];
+  const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
+  const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
+  const uint32_t rid = ((const uint32_t *)(A.ws + A.off_rid))[r];
+
+  const int m = J.m;
+  const int L = J.nseg;
+  const double d0 = J.d0, d1 = J.d1;
+  const int64_t C = J.C;
+  const int n_hist = J.n_hist;
+  const double *edges = (const double *)(A.ws + J.off_edges);
+  const bool trace = J.n_trace > 0;
+  const bool known = J.known != 0;
+  const int32_t cap = J.out_cap;
+  const uint32_t *cdf = (const uint32_t *)(A.ws + J.off_cdf);
+  const double *tr_time = (const double *)(A.ws + J.off_tr_time);
+  const int32_t *tr_type = (const int32_t *)(A.ws + J.off_tr_type);
+  const int32_t *tr_len = (const int32_t *)(A.ws + J.off_tr_len);
+  const uint32_t qmask = (1u << J.qcap_log2) - 1u;
+  const uint32_t rec_cap = (uint32_t)J.rec_cap;
+  uint8_t *blk = A.ws + J.off_ring + (uint64_t)(r - J.replica_begin) * J.ring_stride;
+  QRec *q10 = (QRec *)(blk + J.off_q[0]);
+  uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
+
+  auto recs = [&](int k) { return (NRec *)(blk + J.off_rec[k]); };
+  auto bkts = [&](int k) { return (uint32_t *)(blk + J.off_bkt[k]); };
+  auto metas = [&](int k) { return (SlotMeta *)(blk + J.off_meta[k]); };
+  auto vring = [&](int k) { return (NRec *)(blk + J.off_v[k]); };
+  auto vmask = [&](int k) { return (1u << J.vcap_log2[k]) - 1u; };
+  auto row_of = [&](int j) -> const uint32_t * {
+    return (known || cap <= 1) ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
+  };
+
+  double t, lat_area, ttft_area, lat_sum, mem_area, busy;
+  int64_t batches, arrivals, comps, ctok, evicts, etok, fallback, btok, peak, idle, N, U,
+      Mres, tridx, pendft;
+  uint32_t flags, qh, qt;
+
+  if (!A.resume) {
+    t = lat_area = ttft_area = lat_sum = mem_area = busy = 0.0;
+    batches = arrivals = comps = ctok = evicts = etok = fallback = btok = peak = idle = 0;
+    N = U = Mres = tridx = pendft = 0;
+    flags = 0;
+    qh = qt = 0;
+    for (int j = 0; j < MT; ++j) {
+      s_k[j][tx] = 0;
+      s_tnext[j][tx] = INFINITY;
+      s_Ln[j][tx] = 1;
+      if (j < m && !trace) {
+        int32_t Lj = 1;
+        const double g = draw_gap(seed, rid, (uint32_t)j, 0u, J.lambda[j], row_of(j), cap, &Lj);
+        s_tnext[j][tx] = 0.0 + g;
+        s_Ln[j][tx] = known ? J.lp[j] : (cap <= 1 ? 1 : Lj);
+      }
+    }
+    for (int k = 0; k < LT; ++k) {
+      s_svc[k][tx] = s_I[k][tx] = s_vh[k][tx] = s_vt[k][tx] = 0;
+      s_M[k][tx] = s_B[k][tx] = 0;
+      if (k < L) {
+        uint32_t *bk = bkts(k);
+        SlotMeta *mt = metas(k);
+        for (int x = 0; x < J.seg_delta[k]; ++x) {
+          bk[x] = kNil;
+          mt[x].live = 0;
+          mt[x].suml = 0;
+        }
+      }
+    }
+    for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
+  } else {
+    t = slot_f(A, S_T, r);
+    lat_area = slot_f(A, S_LAT, r);
+    ttft_area = slot_f(A, S_TTFT, r);
+    lat_sum = slot_f(A, S_LATSUM, r);
+    mem_area = slot_f(A, S_MEM, r);
+    busy = slot_f(A, S_BUSY, r);
+    batches = slot_i(A, S_BATCHES, r);
+    arrivals = slot_i(A, S_ARR, r);
+    comps = slot_i(A, S_COMP, r);
+    ctok = slot_i(A, S_CTOK, r);
+    evicts = slot_i(A, S_EVICT, r);
+    etok = slot_i(A, S_ETOK, r);
+    fallback = slot_i(A, S_FALLBACK, r);
+    btok = slot_i(A, S_BTOK, r);
+    peak = slot_i(A, S_PEAK, r);
+    idle = slot_i(A, S_IDLE, r);
+    N = slot_i(A, S_N, r);
+    U = slot_i(A, S_U, r);
+    Mres = slot_i(A, S_MRES, r);
+    tridx = slot_i(A, S_TRIDX, r);
+    pendft = slot_i(A, S_PENDFT, r);
+    flags = (uint32_t)slot_i(A, S_FLAGS, r);
+    qh = (uint32_t)slot_i(A, S_QH, r);
+    qt = (uint32_t)slot_i(A, S_QT, r);
+    for (int j = 0; j < MT; ++j) {
+      s_tnext[j][tx] = slot_f(A, S_TNEXT + j, r);
+      s_k[j][tx] = (uint32_t)slot_i(A, S_K + j, r);
+      s_Ln[j][tx] = (int32_t)slot_i(A, S_LNEXT + j, r);
+    }
+    for (int k = 0; k < LT; ++k) {
+      s_svc[k][tx] = (uint32_t)slot_i(A, S_KSVC + k, r);
+      s_I[k][tx] = (uint32_t)slot_i(A, S_KI + k, r);
+      s_M[k][tx] = slot_i(A, S_KM + k, r);
+      s_B[k][tx] = slot_i(A, S_KB + k, r);
+      s_vh[k][tx] = (uint32_t)slot_i(A, S_KVH + k, r);
+      s_vt[k][tx] = (uint32_t)slot_i(A, S_KVT + k, r);
+    }
+  }
+
+  // ---- arrivals ------------------------------------------------------------
+  auto peek = [&](int &jn) -> double {
+    if (trace) {
+      if (tridx >= J.n_trace) {
+        jn = 0;
+        return INFINITY;
+      }
+      jn = tr_type[tridx];
+      return tr_time[tridx];
+    }
+    double best = s_tnext[0][tx];
+    jn = 0;
+    for (int j = 1; j < m; ++j) {
+      const double v = s_tnext[j][tx];
+      if (v < best) {
+        best = v;
+        jn = j;
+      }
+    }
+    return best;
+  };
+
+  auto push_q10 = [&](double a_ft, int32_t j, int32_t Lr) {
+    if (qt - qh >= rec_cap) {
+      flags |= kFlagCap;
+    } else {
+      QRec rec;
+      rec.a_ft = a_ft;
+      rec.j = j;
+      rec.L = Lr;
+      q10[qt & qmask] = rec;
+    }
+    qt++;
+  };
+
+  auto take = [&](int jn, double a) {
+    int32_t Lr;
+    if (trace) {
+      Lr = known ? J.lp[jn] : tr_len[tridx];
+      tridx++;
+    } else {
+      Lr = s_Ln[jn][tx];
+      const uint32_t k = s_k[jn][tx] + 1u;
+      s_k[jn][tx] = k;
+      int32_t Lj = 1;
+      const double g = draw_gap(seed, rid, (uint32_t)jn, k, J.lambda[jn], row_of(jn), cap, &Lj);
+      s_tnext[jn][tx] = s_tnext[jn][tx] + g;
+      s_Ln[jn][tx] = known ? J.lp[jn] : (cap <= 1 ? 1 : Lj);
+    }
+    arrivals++;
+    N++;
+    U++;
+    push_q10(a, jn, Lr);
+  };
+
+  // ---- evictions -------------------------------------------------------------
+  // Evict the back (most recently admitted) prompt of boundary queue h >= 1.
+  auto evict_boundary = [&](int h) -> int64_t {
+    NRec *v = vring(h);
+    const uint32_t vt = s_vt[h][tx] - 1u;
+    const NRec rec = v[vt & vmask(h)];
+    s_vt[h][tx] = vt;
+    const int32_t rprev = J.seg_end[h - 1];
+    const int64_t ch = (int64_t)J.l[rec.j] + rprev;
+    s_B[h][tx] -= ch;
+    Mres -= ch;
+    evicts++;
+    etok += rprev;
+    push_q10(with_ft(rec.a_ft), rec.j, rec.L);  // it has produced r_{h-1} >= 1 tokens
+    return ch;
+  };
+
+  // Most recently admitted live interior prompt of segment k: the newest
+  // non-empty cohort slot, its highest live index.  Returns the record index
+  // or kNil.
+  auto youngest_interior = [&](int k, uint32_t &kb, uint32_t &kp) -> uint32_t {
+    if (s_I[k][tx] == 0) return kNil;
+    const int32_t delta = J.seg_delta[k];
+    const int32_t nk = J.seg_n[k];
+    const uint32_t svc = s_svc[k][tx];
+    const SlotMeta *mt = metas(k);
+    const NRec *rc = recs(k);
+    for (int32_t back = 0; back < delta && (int64_t)svc - back >= 1; ++back) {
+      const uint32_t slot = (svc - (uint32_t)back) % (uint32_t)delta;
+      if (mt[slot].live == 0) continue;
+      for (int32_t i = nk - 1; i >= 0; --i) {
+        const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
+        const NRec rec = rc[idx];
+        if (rec.L != 0) {
+          kb = rec.kb;
+          kp = rec.kp;
+          return idx;
+        }
+      }
+    }
+    return kNil;
+  };
+
+  auto evict_interior = [&](int k, uint32_t idx) -> int64_t {
+    NRec *rc = recs(k);
+    NRec rec = rc[idx];
+    const int32_t delta = J.seg_delta[k];
+    const int32_t nk = J.seg_n[k];
+    const int64_t stage = (int64_t)J.seg_entry[k] + (int64_t)(s_svc[k][tx] - rec.c) + 1;
+    const int64_t ch = (int64_t)J.l[rec.j] + stage;
+    const uint32_t slot = idx / (uint32_t)nk;
+    (void)delta;
+    SlotMeta *mt = metas(k);
+    mt[slot].live -= 1u;
+    mt[slot].suml -= (uint32_t)J.l[rec.j];
+    const int32_t Lr = rec.L;
+    rec.L = 0;  // leaves a hole; the calendar skips it
+    rc[idx] = rec;
+    s_I[k][tx] -= 1u;
+    s_M[k][tx] -= ch;
+    Mres -= ch;
+    evicts++;
+    fallback++;
+    etok += stage - 1;
+    const bool ft = has_ft(rec.a_ft) || stage >= 2;
+    if (stage == 1 && !ft) pendft--;
+    push_q10(ft ? with_ft(rec.a_ft) : arrival_of(rec.a_ft), rec.j, Lr);
+    return ch;
+  };
+
+  // Evict the most recently admitted prompt among boundary queues
+  // h in [hlo, L) and, if fallback is set and none exists, among the interior
+  // of segments [klo, L).  Returns the memory freed, 0 if nothing was left.
+  auto evict_lifo = [&](int klo, bool allow_interior) -> int64_t {
+    int hb = -1;
+    uint32_t bkb = 0, bkp = 0;
+    for (int h = 1; h < L; ++h) {
+      if (s_vt[h][tx] == s_vh[h][tx]) continue;
+      const NRec rec = vring(h)[(s_vt[h][tx] - 1u) & vmask(h)];
+      if (hb < 0 || rec.kb > bkb || (rec.kb == bkb && rec.kp > bkp)) {
+        hb = h;
+        bkb = rec.kb;
+        bkp = rec.kp;
+      }
+    }
+    if (hb >= 0) return evict_boundary(hb);
+    if (!allow_interior) return 0;
+    int kbest = -1;
+    uint32_t ibest = kNil;
+    for (int k = klo; k < L; ++k) {
+      uint32_t kb = 0, kp = 0;
+      const uint32_t idx = youngest_interior(k, kb, kp);
+      if (idx == kNil) continue;
+      if (kbest < 0 || kb > bkb || (kb == bkb && kp > bkp)) {
+        kbest = k;
+        ibest = idx;
+        bkb = kb;
+        bkp = kp;
+      }
+    }
+    if (kbest < 0) return 0;
+    return evict_interior(kbest, ibest);
+  };
+
+  bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
+
+  for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
+    // ---- decision: largest prefix of segments meeting their thresholds -----
+    int kmax = 0;
+    for (;;) {
+      if (flags & kFlagCap) {
+        stopped = true;
+        break;
+      }
+      if ((int64_t)(qt - qh) >= J.seg_n[0]) {
+        kmax = 1;
+        while (kmax < L && (int64_t)(s_vt[kmax][tx] - s_vh[kmax][tx]) >= J.seg_n[kmax]) kmax++;
+        break;
+      }
+      int jn;
+      const double ta = peek(jn);
+      if (!(ta < INFINITY)) {
+        flags |= kFlagStall;
+        stopped = true;
+        break;
+      }
+      const double dtm = ta - t;
+      lat_area += (double)N * dtm;
+      ttft_area += (double)U * dtm;
+      mem_area += (double)Mres * dtm;
+      t = ta;
+      for (;;) {
+        if (flags & kFlagCap) break;
+        int j2;
+        const double a2 = peek(j2);
+        if (a2 != ta) break;
+        take(j2, a2);
+      }
+      idle++;
+    }
+    if (stopped) break;
+
+    // ---- launch: entering cohorts, calendar links, batch tokens -----------
+    const uint32_t bidx = (uint32_t)batches;
+    int64_t tokens = 0, prefill_l = 0, mplus = Mres;
+    int64_t pend_new = 0;
+    for (int k = 0; k < kmax; ++k) {
+      const int32_t delta = J.seg_delta[k];
+      const int32_t nk = J.seg_n[k];
+      const int32_t rk = J.seg_end[k];
+      const int32_t ent = J.seg_entry[k];
+      const uint32_t x = s_svc[k][tx] + 1u;
+      const uint32_t slot = x % (uint32_t)delta;
+      NRec *rc = recs(k);
+      uint32_t *bk = bkts(k);
+      tokens += s_M[k][tx];
+      uint32_t suml = 0;
+      // link in reverse selection order: traversal is then in key order
+      for (int32_t i = nk - 1; i >= 0; --i) {
+        NRec e;
+        if (k == 0) {
+          const QRec qr = q10[(qh + (uint32_t)i) & qmask];
+          e.a_ft = qr.a_ft;
+          e.j = qr.j;
+          e.L = qr.L;
+          e.kb = bidx;
+          e.kp = (uint32_t)i;
+          tokens += J.l[qr.j];
+          prefill_l += J.l[qr.j];
+          if (!has_ft(qr.a_ft)) pend_new++;
+        } else {
+          e = vring(k)[(s_vh[k][tx] + (uint32_t)i) & vmask(k)];
+          tokens += (int64_t)J.l[e.j] + J.seg_end[k - 1] + 1;
+        }
+        e.c = x;
+        const int32_t pexit = e.L < rk ? e.L : rk;
+        const uint32_t b = (x + (uint32_t)(pexit - ent)) % (uint32_t)delta;
+        const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
+        e.next = bk[b];
+        bk[b] = idx;
+        rc[idx] = e;
+        suml += (uint32_t)J.l[e.j];
+      }
+      SlotMeta sm;
+      sm.live = (uint32_t)nk;
+      sm.suml = suml;
+      metas(k)[slot] = sm;
+      if (k == 0)
+        qh += (uint32_t)nk;
+      else
+        s_vh[k][tx] += (uint32_t)nk;  // still charged in s_B until the completion
+      // projected change of the segment's memory (no early completion)
+      if (delta >= 2) {
+        uint32_t T = 0, Tl = 0;
+        if ((int64_t)x - (delta - 1) >= 1) {
+          const SlotMeta tm = metas(k)[(x - (uint32_t)(delta - 1)) % (uint32_t)delta];
+          T = tm.live;
+          Tl = tm.suml;
+        }
+        mplus += (int64_t)s_I[k][tx] - T;
+        if (k == L - 1) mplus -= (int64_t)Tl + (int64_t)T * rk;
+        if (k == 0)
+          mplus += (int64_t)suml + nk;  // prefills land at stage 1
+        else
+          mplus += 2ll * nk;            // l + r_{k-1} -> l + r_{k-1} + 2
+      } else {                          // entering prompts are processed at r_k
+        if (k < L - 1)
+          mplus += nk;                  // l + r_{k-1} -> l + r_k
+        else
+          mplus -= (int64_t)suml + (int64_t)nk * J.seg_end[k - 1];
+      }
+    }
+
+    // ---- pre-launch repair on the projected state ----------------------------
+    while (mplus > C) {
+      const int64_t freed = evict_lifo(kmax, false);
+      if (freed == 0) break;
+      mplus -= freed;
+    }
+    while (mplus > C) {  // unselected interior prompts (segments after the prefix)
+      const int64_t freed = evict_lifo(kmax, true);
+      if (freed == 0) break;
+      mplus -= freed;
+    }
+    if (mplus > C) flags |= kFlagOverflow;
+
+    const int64_t m_launch = Mres + prefill_l;
+    if (m_launch > peak) peak = m_launch;
+    const double tau = d0 + d1 * (double)tokens;
+    const double t_end = t + tau;
+    const int64_t N0 = N, U0 = U;
+
+    // ---- arrivals during the batch -----------------------------------------
+    for (;;) {
+      if (flags & kFlagCap) break;
+      int jn;
+      const double ta = peek(jn);
+      if (!(ta <= t_end)) break;
+      take(jn, ta);
+      lat_area += t_end - ta;
+      ttft_area += t_end - ta;
+    }
+    lat_area += (double)N0 * tau;
+    ttft_area += (double)U0 * tau;
+    mem_area += (double)m_launch * tau;
+    busy += tau;
+    t = t_end;
+
+    // ---- completion transition, segment by segment ---------------------------
+    for (int k = 0; k < kmax; ++k) {
+      const int32_t delta = J.seg_delta[k];
+      const int32_t nk = J.seg_n[k];
+      const int32_t rk = J.seg_end[k];
+      const int32_t ent = J.seg_entry[k];
+      const uint32_t x = s_svc[k][tx] + 1u;
+      s_svc[k][tx] = x;
+      const uint32_t slot = x % (uint32_t)delta;
+      NRec *rc = recs(k);
+      SlotMeta *mt = metas(k);
+      if (k == 0) {  // the stage-1 cohort produces its first tokens
+        U -= pendft;
+        pendft = pend_new;
+      }
+      int64_t Mk = s_M[k][tx] + (int64_t)s_I[k][tx];  // every interior prompt advances
+      uint32_t Ik = s_I[k][tx];
+      // entering prompts: leave the entry queue, stay unless they exit now
+      for (int32_t i = 0; i < nk; ++i) {
+        const NRec e = rc[slot * (uint32_t)nk + (uint32_t)i];
+        const int64_t le = J.l[e.j];
+        if (k > 0) {
+          s_B[k][tx] -= le + J.seg_end[k - 1];
+          Mres -= le + J.seg_end[k - 1];
+        }
+        const int32_t pexit = e.L < rk ? e.L : rk;
+        if (pexit > ent) {
+          Ik += 1u;
+          Mk += le + ent + 1;
+        }
+      }
+      // prompts whose exit is at this service
+      uint32_t *bk = bkts(k);
+      const uint32_t b = x % (uint32_t)delta;
+      uint32_t idx = bk[b];
+      bk[b] = kNil;
+      while (idx != kNil) {
+        const NRec rec = rc[idx];
+        const uint32_t nxt = rec.next;
+        if (rec.L != 0) {  // holes left by evictions are skipped
+          const int64_t le = J.l[rec.j];
+          const int32_t p = rec.L < rk ? rec.L : rk;
+          if (rec.c != x) {  // an interior prompt: it had advanced to p + 1
+            Mk -= le + p + 1;
+            Ik -= 1u;
+          }
+          SlotMeta &sm = mt[idx / (uint32_t)nk];
+          sm.live -= 1u;
+          sm.suml -= (uint32_t)le;
+          if (rec.L == p) {  // completion at its own output length
+            const double lat = t_end - arrival_of(rec.a_ft);
+            lat_sum += lat;
+            __hip_atomic_fetch_add(&hist[hist_bin(edges, n_hist, lat)], 1u,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            comps++;
+            ctok += rec.L;
+            N--;
+          } else {  // survivor joins the boundary queue of segment k+1
+            const int h = k + 1;
+            NRec v = rec;
+            v.a_ft = with_ft(rec.a_ft);
+            const uint32_t vt = s_vt[h][tx];
+            if (vt - s_vh[h][tx] <= vmask(h)) {
+              vring(h)[vt & vmask(h)] = v;
+              s_vt[h][tx] = vt + 1u;
+            } else {
+              flags |= kFlagCap;  // bounded by construction; guards the ring
+            }
+            s_B[h][tx] += le + rk;
+            Mres += le + rk;
+          }
+          rc[idx].L = 0;  // no longer in the segment
+        }
+        idx = nxt;
+      }
+      Mres += Mk - s_M[k][tx];
+      s_M[k][tx] = Mk;
+      s_I[k][tx] = Ik;
+    }
+    if (Mres > peak) peak = Mres;
+
+    // ---- repair: boundary prompts first, then interior prompts -------------
+    while (Mres > C) {
+      if (evict_lifo(0, true) == 0) break;
+    }
+    batches++;
+    btok += tokens;
+  }
+
+  // ---- save state ------------------------------------------------------------
+  put_f(A, S_T, r, t);
+  put_f(A, S_LAT, r, lat_area);
+  put_f(A, S_TTFT, r, ttft_area);
+  put_f(A, S_LATSUM, r, lat_sum);
+  put_f(A, S_MEM, r, mem_area);
+  put_f(A, S_BUSY, r, busy);
+  put_i(A, S_BATCHES, r, batches);
+  put_i(A, S_ARR, r, arrivals);
+  put_i(A, S_COMP, r, comps);
+  put_i(A, S_CTOK, r, ctok);
+  put_i(A, S_EVICT, r, evicts);
+  put_i(A, S_ETOK, r, etok);
+  put_i(A, S_FALLBACK, r, fallback);
+  put_i(A, S_BTOK, r, btok);
+  put_i(A, S_PEAK, r, peak);
+  put_i(A, S_IDLE, r, idle);
+  put_i(A, S_N, r, N);
+  put_i(A, S_U, r, U);
+  put_i(A, S_MRES, r, Mres);
+  put_i(A, S_TRIDX, r, tridx);
+  put_i(A, S_PENDFT, r, pendft);
+  put_i(A, S_FLAGS, r, (int64_t)flags);
+  put_i(A, S_QH, r, qh);
+  put_i(A, S_QT, r, qt);
+  for (int j = 0; j < MT; ++j) {
+    put_f(A, S_TNEXT + j, r, s_tnext[j][tx]);
+    put_i(A, S_K + j, r, s_k[j][tx]);
+    put_i(A, S_LNEXT + j, r, s_Ln[j][tx]);
+  }
+  for (int k = 0; k < LT; ++k) {
+    put_i(A, S_KSVC + k, r, s_svc[k][tx]);
+    put_i(A, S_KI + k, r, s_I[k][tx]);
+    put_i(A, S_KM + k, r, s_M[k][tx]);
+    put_i(A, S_KB + k, r, s_B[k][tx]);
+    put_i(A, S_KVH + k, r, s_vh[k][tx]);
+    put_i(A, S_KVT + k, r, s_vt[k][tx]);
+  }
+}
+
+template <int MT, int LT>
+hipError_t launch_ml(const KArgs &A, hipStream_t s) {
+  const int threads = 64;
+  const int blocks = (A.n_list + threads - 1) / threads;
+  hipLaunchKernelGGL((sim_nested_kernel<MT, LT>), dim3(blocks), dim3(threads), 0, s, A);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s) {
+  if (max_m <= 4) {
+    if (max_seg <= 4) return launch_ml<4, 4>(A, s);
+    if (max_seg <= 8) return launch_ml<4, 8>(A, s);
+    return launch_ml<4, 16>(A, s);
+  }
+  if (max_seg <= 8) return launch_ml<16, 8>(A, s);
+  return launch_ml<16, 16>(A, s);
+}
+
+}  // namespace wsim

@@ -1,0 +1,498 @@
+// wait_sim_host.hip -- host side of the simulator library: validation of the
+// model and policy (arXiv 2504.11320, Sections 2, 4 and 5), workspace layout,
+// table upload, kernel launches and the C ABI declared in include/wait_sim.h.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "sim_common.h"
+
+namespace {
+
+using namespace wsim;
+
+// Copy the per-replica state of a workspace into the result layout.
+__global__ void __launch_bounds__(256) export_kernel(KArgs A, uint8_t *out) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= A.R) return;
+  const int64_t R = A.R;
+  int64_t *oi = (int64_t *)out;
+  double *of = (double *)(out + 8 * WS_NI64 * R);
+  uint32_t *ofl = (uint32_t *)(out + 8 * (WS_NI64 + WS_NF64) * R);
+  const uint32_t jix = ((const uint32_t *)(A.ws + A.off_job_of))[r];
+  const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
+  const int fi[WS_NI64] = {S_BATCHES, S_ARR, S_COMP, S_CTOK, S_EVICT, S_ETOK,
+                           S_FALLBACK, S_BTOK, S_PEAK, -1, -1, S_IDLE};
+  for (int f = 0; f < WS_NI64; ++f)
+    if (fi[f] >= 0) oi[f * R + r] = slot_i(A, fi[f], r);
+  // waiting and resident counts at T
+  int64_t waiting = 0, resident = 0;
+  const int nq = (J.policy == WS_WAIT) ? J.m : 1;
+  for (int j = 0; j < nq; ++j) waiting += slot_i(A, S_QT + j, r) - slot_i(A, S_QH + j, r);
+  if (J.policy == WS_NESTED_WAIT) {
+    for (int k = 0; k < J.nseg; ++k) {
+      resident += slot_i(A, S_KI + k, r);
+      if (k > 0) resident += slot_i(A, S_KVT + k, r) - slot_i(A, S_KVH + k, r);
+    }
+  } else {
+    for (int j = 0; j < J.m; ++j) resident += slot_i(A, S_DT + j, r) - slot_i(A, S_DH + j, r);
+  }
+  oi[9 * R + r] = waiting;
+  oi[10 * R + r] = resident;
+  const int ff[WS_NF64] = {S_T, S_BUSY, S_LAT, S_TTFT, S_LATSUM, S_MEM};
+  for (int f = 0; f < WS_NF64; ++f) of[f * R + r] = slot_f(A, ff[f], r);
+  ofl[r] = (uint32_t)slot_i(A, S_FLAGS, r);
+}
+
+// ------------------------------------------------------------- host -----
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string &msg) {
+  g_err = msg;
+  return code;
+}
+
+int ceil_log2(uint64_t x) {
+  int k = 0;
+  while ((1ull << k) < x) ++k;
+  return k;
+}
+
+uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+struct JobHost {
+  JobDev d;
+  int64_t reserve_tok;
+  uint64_t edges_bytes, cdf_bytes, trace_bytes;
+};
+
+struct Layout {
+  int64_t R = 0;
+  int32_t hist_stride = 1;
+  uint64_t off_jobs = 0, off_seed = 0, off_rid = 0, off_job_of = 0,
+           off_list = 0, off_tables = 0, off_state = 0, off_hist = 0,
+           off_rings = 0, total = 0;
+  std::vector<JobHost> jobs;
+  int32_t list_count[3] = {0, 0, 0};
+  uint64_t list_off[3] = {0, 0, 0};
+  int32_t max_m[3] = {0, 0, 0};
+  int32_t max_seg = 0;
+};
+
+int validate_job(const ws_job &jb, int idx, JobHost &H) {
+  const std::string at = "job " + std::to_string(idx) + ": ";
+  if (!jb.cfg || !jb.pol) return fail(WS_EINVAL, at + "cfg and pol must be non-NULL");
+  if (jb.n < 0) return fail(WS_EINVAL, at + "negative replica count");
+  if (jb.n > 0 && !jb.streams) return fail(WS_EINVAL, at + "streams must be non-NULL");
+  const ws_config &c = *jb.cfg;
+  const ws_policy &p = *jb.pol;
+  if (c.m < 1 || c.m > WS_MAX_TYPES)
+    return fail(WS_EINVAL, at + "m must be in 1.." + std::to_string(WS_MAX_TYPES));
+  if (!c.prompt_len || !c.lambda) return fail(WS_EINVAL, at + "prompt_len and lambda required");
+  for (int j = 0; j < c.m; ++j) {
+    if (c.prompt_len[j] < 1) return fail(WS_EINVAL, at + "prompt lengths must be >= 1");
+    if (!(c.lambda[j] >= 0.0) || !std::isfinite(c.lambda[j]))
+      return fail(WS_EINVAL, at + "rates must be finite and >= 0");
+  }
+  if (!(c.d0 > 0.0) || !std::isfinite(c.d0)) return fail(WS_EINVAL, at + "d0 must be > 0");
+  if (!(c.d1 >= 0.0) || !std::isfinite(c.d1)) return fail(WS_EINVAL, at + "d1 must be >= 0");
+  if (c.C < 1 || c.C > (int64_t(1) << 30)) return fail(WS_EINVAL, at + "C must be in 1..2^30");
+  const bool known = c.out_len != nullptr;
+  int64_t maxL = 0;
+  if (known) {
+    for (int j = 0; j < c.m; ++j) {
+      if (c.out_len[j] < 1) return fail(WS_EINVAL, at + "output lengths must be >= 1");
+      maxL = std::max<int64_t>(maxL, c.out_len[j]);
+    }
+  } else {
+    if (c.out_cap < 1) return fail(WS_EINVAL, at + "out_cap must be >= 1 without out_len");
+    maxL = c.out_cap;
+    if (c.n_trace == 0) {
+      if (c.out_cap > 1 && !c.out_cdf_u32) return fail(WS_EINVAL, at + "out_cdf_u32 required");
+      for (int j = 0; j < c.m; ++j)
+        for (int s = 1; s + 1 < c.out_cap; ++s)
+          if (c.out_cdf_u32[(size_t)j * (c.out_cap - 1) + s] <
+              c.out_cdf_u32[(size_t)j * (c.out_cap - 1) + s - 1])
+            return fail(WS_EINVAL, at + "CDF table rows must be nondecreasing");
+    }
+  }
+  if (c.n_hist < 0 || c.n_hist > WS_MAX_HIST_EDGES)
+    return fail(WS_EINVAL, at + "n_hist out of range");
+  if (c.n_hist > 0) {
+    if (!c.hist_edges) return fail(WS_EINVAL, at + "hist_edges required");
+    for (int b = 0; b < c.n_hist; ++b) {
+      if (!std::isfinite(c.hist_edges[b])) return fail(WS_EINVAL, at + "edges must be finite");
+      if (b > 0 && !(c.hist_edges[b] > c.hist_edges[b - 1]))
+        return fail(WS_EINVAL, at + "edges must be strictly increasing");
+    }
+  }
+  if (c.record_capacity < 16 || c.record_capacity > (1 << 26) ||
+      (c.record_capacity & (c.record_capacity - 1)) != 0)
+    return fail(WS_EINVAL, at + "record_capacity must be a power of two in 16..2^26");
+  if (c.n_trace < 0) return fail(WS_EINVAL, at + "n_trace must be >= 0");
+  if (c.n_trace > 0) {
+    if (!c.trace_time || !c.trace_type) return fail(WS_EINVAL, at + "trace arrays required");
+    if (!known && !c.trace_out_len) return fail(WS_EINVAL, at + "trace_out_len required");
+    for (int64_t i = 0; i < c.n_trace; ++i) {
+      if (!(c.trace_time[i] >= 0.0) || !std::isfinite(c.trace_time[i]))
+        return fail(WS_EINVAL, at + "trace times must be finite and >= 0");
+      if (i > 0 && c.trace_time[i] < c.trace_time[i - 1])
+        return fail(WS_EINVAL, at + "trace times must be nondecreasing");
+      if (c.trace_type[i] < 0 || c.trace_type[i] >= c.m)
+        return fail(WS_EINVAL, at + "trace type out of range");
+      if (!known && (c.trace_out_len[i] < 1 || c.trace_out_len[i] > c.out_cap))
+        return fail(WS_EINVAL, at + "trace output length out of range");
+    }
+  }
+  int64_t reserve_tok = 0;
+  if (p.kind == WS_WAIT) {
+    if (!known) return fail(WS_EINVAL, at + "WAIT needs known output lengths");
+    if (!p.n) return fail(WS_EINVAL, at + "thresholds required");
+    for (int j = 0; j < c.m; ++j)
+      if (p.n[j] < 1) return fail(WS_EINVAL, at + "thresholds must be >= 1");
+  } else if (p.kind == WS_FCFS) {
+    if (!(p.fcfs_reserve >= 0.0 && p.fcfs_reserve < 1.0))
+      return fail(WS_EINVAL, at + "fcfs_reserve must be in [0,1)");
+    reserve_tok = (int64_t)std::ceil(p.fcfs_reserve * (double)c.C);
+    for (int j = 0; j < c.m; ++j)
+      if (c.prompt_len[j] > c.C - reserve_tok)
+        return fail(WS_EINVAL, at + "a prompt does not fit below the FCFS reserve");
+    if (!known) return fail(WS_EUNSUPPORTED, at + "FCFS with unknown lengths is not in this build");
+  } else if (p.kind == WS_NESTED_WAIT) {
+    if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail(WS_EINVAL, at + "L out of range");
+    if (!p.n || !p.seg_end) return fail(WS_EINVAL, at + "thresholds and seg_end required");
+    for (int k = 0; k < p.L; ++k) {
+      if (p.n[k] < 1) return fail(WS_EINVAL, at + "thresholds must be >= 1");
+      if (p.seg_end[k] < 1 || (k > 0 && p.seg_end[k] <= p.seg_end[k - 1]))
+        return fail(WS_EINVAL, at + "seg_end must be strictly increasing and >= 1");
+    }
+    if (p.seg_end[p.L - 1] != maxL)
+      return fail(WS_EINVAL, at + "last segment must end at the largest output length");
+  } else {
+    return fail(WS_EINVAL, at + "unknown policy kind");
+  }
+  for (int j = 0; j < c.m; ++j) {
+    const int64_t Lj = known ? c.out_len[j] : c.out_cap;
+    if (c.prompt_len[j] + Lj > c.C)
+      return fail(WS_EINVAL, at + "a single prompt does not fit in C (atomic feasibility)");
+  }
+
+  JobDev &d = H.d;
+  std::memset(&d, 0, sizeof(d));
+  d.m = c.m;
+  d.policy = p.kind;
+  d.n_hist = c.n_hist;
+  d.out_cap = c.out_cap;
+  d.nseg = p.kind == WS_NESTED_WAIT ? p.L : 0;
+  d.known = known ? 1 : 0;
+  d.qcap_log2 = ceil_log2((uint64_t)c.record_capacity);
+  d.rec_cap = c.record_capacity;
+  d.d0 = c.d0;
+  d.d1 = c.d1;
+  d.C = c.C;
+  d.reserve_tok = reserve_tok;
+  d.n_trace = c.n_trace;
+  for (int j = 0; j < c.m; ++j) {
+    d.l[j] = c.prompt_len[j];
+    d.lp[j] = known ? c.out_len[j] : c.out_cap;
+    d.lambda[j] = c.lambda[j];
+    d.n[j] = (p.kind == WS_WAIT) ? p.n[j] : 0;
+    uint64_t dcap;
+    if (p.kind == WS_WAIT)  // launch holds <= (l'_j + 1) n_j records
+      dcap = (uint64_t)(c.out_len[j] + 1) * (uint64_t)p.n[j];
+    else                    // residents of type j charge >= l_j each
+      dcap = (uint64_t)(c.C / c.prompt_len[j]) + 2;
+    if (p.kind == WS_NESTED_WAIT) dcap = 2;
+    d.dcap_log2[j] = ceil_log2(std::max<uint64_t>(dcap, 2));
+  }
+  if (p.kind == WS_NESTED_WAIT) {
+    int32_t lmin = c.prompt_len[0];
+    for (int j = 1; j < c.m; ++j) lmin = std::min(lmin, c.prompt_len[j]);
+    for (int k = 0; k < p.L; ++k) {
+      const int32_t prev = k == 0 ? 0 : p.seg_end[k - 1];
+      d.seg_end[k] = p.seg_end[k];
+      d.seg_n[k] = p.n[k];
+      d.seg_entry[k] = k == 0 ? 0 : prev + 1;
+      d.seg_delta[k] = p.seg_end[k] - d.seg_entry[k] + 1;
+      if (k > 0) {
+        // boundary queue k holds <= C/(l_min + r_{k-1}) prompts after any
+        // repair, plus one batch of survivors from segment k-1
+        const uint64_t vcap = (uint64_t)(c.C / (lmin + prev)) + 2ull * (uint64_t)p.n[k - 1] + 2;
+        d.vcap_log2[k] = ceil_log2(vcap);
+      }
+    }
+  }
+  H.reserve_tok = reserve_tok;
+  H.edges_bytes = align_up(8ull * (uint64_t)std::max(c.n_hist, 1), 256);
+  H.cdf_bytes = (!known && c.n_trace == 0 && c.out_cap > 1)
+                    ? align_up(4ull * (uint64_t)c.m * (uint64_t)(c.out_cap - 1), 256)
+                    : 0;
+  H.trace_bytes = c.n_trace > 0 ? align_up(16ull * (uint64_t)c.n_trace, 256) : 0;
+  // ring block of one replica
+  uint64_t off = 0;
+  const uint64_t qrec = (p.kind == WS_WAIT) ? 8 : 16;
+  const int nq = (p.kind == WS_WAIT) ? c.m : 1;
+  for (int j = 0; j < nq; ++j) {
+    d.off_q[j] = off;
+    off += align_up(qrec << d.qcap_log2, 256);
+  }
+  if (p.kind == WS_NESTED_WAIT) {
+    for (int k = 0; k < p.L; ++k) {
+      const uint64_t slots = (uint64_t)d.seg_delta[k];
+      d.off_rec[k] = off;
+      off += align_up(sizeof(NRec) * slots * (uint64_t)p.n[k], 256);
+      d.off_bkt[k] = off;
+      off += align_up(4ull * slots, 256);
+      d.off_meta[k] = off;
+      off += align_up(8ull * slots, 256);
+      if (k > 0) {
+        d.off_v[k] = off;
+        off += align_up(sizeof(NRec) << d.vcap_log2[k], 256);
+      }
+    }
+  } else {
+    for (int j = 0; j < c.m; ++j) {
+      d.off_d[j] = off;
+      off += align_up(16ull << d.dcap_log2[j], 256);
+    }
+  }
+  d.ring_stride = off;
+  return WS_OK;
+}
+
+int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
+  if (n_jobs < 1 || !jobs) return fail(WS_EINVAL, "need at least one job");
+  Lo = Layout();
+  Lo.jobs.resize(n_jobs);
+  int64_t R = 0;
+  int32_t hmax = 0;
+  for (int i = 0; i < n_jobs; ++i) {
+    int rc = validate_job(jobs[i], i, Lo.jobs[i]);
+    if (rc != WS_OK) return rc;
+    Lo.jobs[i].d.replica_begin = R;
+    R += jobs[i].n;
+    hmax = std::max(hmax, jobs[i].cfg->n_hist + 1);
+    const int pk = jobs[i].pol->kind;
+    Lo.list_count[pk] += jobs[i].n;
+    Lo.max_m[pk] = std::max(Lo.max_m[pk], jobs[i].cfg->m);
+    if (pk == WS_NESTED_WAIT) Lo.max_seg = std::max(Lo.max_seg, jobs[i].pol->L);
+  }
+  if (R < 1) return fail(WS_EINVAL, "no replicas");
+  if (R > (int64_t(1) << 30)) return fail(WS_EINVAL, "too many replicas");
+  Lo.R = R;
+  Lo.hist_stride = hmax;
+  uint64_t off = 256;
+  Lo.off_jobs = off;
+  off = align_up(off + sizeof(JobDev) * (uint64_t)n_jobs, 256);
+  Lo.off_seed = off;
+  off = align_up(off + 8ull * R, 256);
+  Lo.off_rid = off;
+  off = align_up(off + 4ull * R, 256);
+  Lo.off_job_of = off;
+  off = align_up(off + 4ull * R, 256);
+  Lo.off_list = off;
+  for (int pk = 0; pk < 3; ++pk) {
+    Lo.list_off[pk] = off;
+    off = align_up(off + 4ull * (uint64_t)Lo.list_count[pk], 256);
+  }
+  Lo.off_tables = off;
+  for (int i = 0; i < n_jobs; ++i) {
+    JobHost &H = Lo.jobs[i];
+    H.d.off_edges = off;
+    off += H.edges_bytes;
+    H.d.off_cdf = off;
+    off += H.cdf_bytes;
+    H.d.off_tr_time = off;
+    H.d.off_tr_type = off + 8ull * (uint64_t)jobs[i].cfg->n_trace;
+    H.d.off_tr_len = off + 12ull * (uint64_t)jobs[i].cfg->n_trace;
+    off += H.trace_bytes;
+  }
+  off = align_up(off, 256);
+  Lo.off_state = off;
+  off = align_up(off + 8ull * S_COUNT * (uint64_t)R, 256);
+  Lo.off_hist = off;
+  off = align_up(off + 4ull * (uint64_t)hmax * (uint64_t)R, 256);
+  Lo.off_rings = off;
+  for (int i = 0; i < n_jobs; ++i) {
+    JobHost &H = Lo.jobs[i];
+    H.d.off_ring = off;
+    off += H.d.ring_stride * (uint64_t)jobs[i].n;
+    off = align_up(off, 256);
+  }
+  Lo.total = off;
+  return WS_OK;
+}
+
+uint64_t results_size(const Layout &Lo) {
+  const uint64_t R = (uint64_t)Lo.R;
+  uint64_t off = 8ull * (WS_NI64 + WS_NF64) * R + 4ull * R;
+  off = align_up(off, 8);
+  return off + 4ull * (uint64_t)Lo.hist_stride * R;
+}
+
+uint64_t results_hist_offset(const Layout &Lo) {
+  const uint64_t R = (uint64_t)Lo.R;
+  return align_up(8ull * (WS_NI64 + WS_NF64) * R + 4ull * R, 8);
+}
+
+#define HIP_TRY(expr)                                                       \
+  do {                                                                      \
+    hipError_t e_ = (expr);                                                 \
+    if (e_ != hipSuccess)                                                   \
+      return fail(WS_EDEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+KArgs base_args(const Layout &Lo, void *d_ws) {
+  KArgs A;
+  std::memset(&A, 0, sizeof(A));
+  A.ws = (uint8_t *)d_ws;
+  A.off_jobs = Lo.off_jobs;
+  A.off_seed = Lo.off_seed;
+  A.off_rid = Lo.off_rid;
+  A.off_job_of = Lo.off_job_of;
+  A.off_state = Lo.off_state;
+  A.off_hist = Lo.off_hist;
+  A.R = Lo.R;
+  A.hist_stride = Lo.hist_stride;
+  return A;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- C ABI --
+
+extern "C" {
+
+const char *wait_sim_last_error(void) { return g_err.c_str(); }
+
+int wait_sim_abi_version(void) { return WS_ABI_VERSION; }
+
+int wait_sim_workspace_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes) {
+  g_err.clear();
+  if (!bytes) return fail(WS_EINVAL, "bytes must be non-NULL");
+  Layout Lo;
+  int rc = make_layout(jobs, n_jobs, Lo);
+  if (rc != WS_OK) return rc;
+  *bytes = (size_t)Lo.total;
+  return WS_OK;
+}
+
+int wait_sim_results_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes,
+                           int32_t *hist_stride) {
+  g_err.clear();
+  if (!bytes) return fail(WS_EINVAL, "bytes must be non-NULL");
+  Layout Lo;
+  int rc = make_layout(jobs, n_jobs, Lo);
+  if (rc != WS_OK) return rc;
+  *bytes = (size_t)results_size(Lo);
+  if (hist_stride) *hist_stride = Lo.hist_stride;
+  return WS_OK;
+}
+
+int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
+                     size_t ws_bytes, void *hip_stream) {
+  g_err.clear();
+  Layout Lo;
+  int rc = make_layout(jobs, n_jobs, Lo);
+  if (rc != WS_OK) return rc;
+  if (!d_workspace) return fail(WS_EINVAL, "workspace must be non-NULL");
+  if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
+  hipStream_t s = (hipStream_t)hip_stream;
+  // host image of everything up to the state region
+  std::vector<uint8_t> img(Lo.off_state, 0);
+  for (int i = 0; i < n_jobs; ++i)
+    std::memcpy(img.data() + Lo.off_jobs + sizeof(JobDev) * i, &Lo.jobs[i].d, sizeof(JobDev));
+  int64_t r = 0;
+  std::vector<int32_t> lists[3];
+  for (int i = 0; i < n_jobs; ++i) {
+    const ws_job &jb = jobs[i];
+    for (int x = 0; x < jb.n; ++x, ++r) {
+      std::memcpy(img.data() + Lo.off_seed + 8 * r, &jb.streams[x].seed, 8);
+      std::memcpy(img.data() + Lo.off_rid + 4 * r, &jb.streams[x].replica_id, 4);
+      const uint32_t ji = (uint32_t)i;
+      std::memcpy(img.data() + Lo.off_job_of + 4 * r, &ji, 4);
+      lists[jb.pol->kind].push_back((int32_t)r);
+    }
+    const ws_config &c = *jb.cfg;
+    const JobDev &d = Lo.jobs[i].d;
+    if (c.n_hist > 0) std::memcpy(img.data() + d.off_edges, c.hist_edges, 8ull * c.n_hist);
+    if (Lo.jobs[i].cdf_bytes)
+      std::memcpy(img.data() + d.off_cdf, c.out_cdf_u32, 4ull * c.m * (c.out_cap - 1));
+    if (c.n_trace > 0) {
+      std::memcpy(img.data() + d.off_tr_time, c.trace_time, 8ull * c.n_trace);
+      std::memcpy(img.data() + d.off_tr_type, c.trace_type, 4ull * c.n_trace);
+      if (c.trace_out_len)
+        std::memcpy(img.data() + d.off_tr_len, c.trace_out_len, 4ull * c.n_trace);
+    }
+  }
+  for (int pk = 0; pk < 3; ++pk)
+    if (!lists[pk].empty())
+      std::memcpy(img.data() + Lo.list_off[pk], lists[pk].data(), 4 * lists[pk].size());
+  HIP_TRY(hipMemcpyAsync(d_workspace, img.data(), img.size(), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return WS_OK;
+}
+
+int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                     int32_t resume, void *d_workspace, size_t ws_bytes,
+                     void *d_results, size_t results_bytes, void *hip_stream) {
+  g_err.clear();
+  Layout Lo;
+  int rc = make_layout(jobs, n_jobs, Lo);
+  if (rc != WS_OK) return rc;
+  if (horizon < 0) return fail(WS_EINVAL, "horizon must be >= 0");
+  if (!d_workspace || !d_results) return fail(WS_EINVAL, "device buffers must be non-NULL");
+  if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
+  if (results_bytes < results_size(Lo)) return fail(WS_EWORKSPACE, "result buffer too small");
+  hipStream_t s = (hipStream_t)hip_stream;
+  KArgs A = base_args(Lo, d_workspace);
+  A.horizon = horizon;
+  A.resume = resume ? 1 : 0;
+  for (int pk = 0; pk < 3; ++pk) {
+    if (Lo.list_count[pk] == 0) continue;
+    KArgs B = A;
+    B.off_list = Lo.list_off[pk];
+    B.n_list = Lo.list_count[pk];
+    hipError_t e = hipSuccess;
+    if (pk == WS_NESTED_WAIT)
+      e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, s);
+    else
+      e = launch_known(pk, Lo.max_m[pk], B, s);
+    if (e != hipSuccess) return fail(WS_EDEVICE, std::string("launch: ") + hipGetErrorString(e));
+  }
+  const int tb = 256;
+  hipLaunchKernelGGL(export_kernel, dim3((unsigned)((Lo.R + tb - 1) / tb)), dim3(tb), 0, s, A,
+                     (uint8_t *)d_results);
+  HIP_TRY(hipGetLastError());
+  HIP_TRY(hipMemcpyAsync((uint8_t *)d_results + results_hist_offset(Lo),
+                         (uint8_t *)d_workspace + Lo.off_hist,
+                         4ull * (uint64_t)Lo.hist_stride * (uint64_t)Lo.R,
+                         hipMemcpyDeviceToDevice, s));
+  return WS_OK;
+}
+
+int wait_sim_run_batch(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                       void *d_workspace, size_t ws_bytes, void *d_results,
+                       size_t results_bytes, void *hip_stream) {
+  int rc = wait_sim_prepare(jobs, n_jobs, d_workspace, ws_bytes, hip_stream);
+  if (rc != WS_OK) return rc;
+  return wait_sim_advance(jobs, n_jobs, horizon, 0, d_workspace, ws_bytes, d_results,
+                          results_bytes, hip_stream);
+}
+
+int wait_sim_run(const ws_config *cfg, const ws_policy *pol, const ws_stream *streams,
+                 int32_t n_replicas, int64_t horizon, void *d_workspace, size_t ws_bytes,
+                 void *d_results, size_t results_bytes, void *hip_stream) {
+  ws_job jb;
+  jb.cfg = cfg;
+  jb.pol = pol;
+  jb.streams = streams;
+  jb.n = n_replicas;
+  return wait_sim_run_batch(&jb, 1, horizon, d_workspace, ws_bytes, d_results, results_bytes,
+                            hip_stream);
+}
+
+}  // extern "C"

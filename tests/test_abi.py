@@ -53,8 +53,9 @@ def test_validation_errors():
     # atomic feasibility: l_j + l'_j <= C
     assert _err(_job(C=1500)).code == B.WS_EINVAL
     assert _err(_job(hist_edges=np.array([1.0, 1.0]))).code == B.WS_EINVAL
-    e = _err(_job(policy="nested", seg_end=[64, 256, 512]))
-    assert e.code in (B.WS_EINVAL, B.WS_EUNSUPPORTED)
+    # Nested: the last segment must end at the largest output length
+    assert _err(_job(policy="nested", seg_end=[64, 256])).code == B.WS_EINVAL
+    assert _err(_job(policy="nested", seg_end=[64, 64, 512])).code == B.WS_EINVAL
     # a well-formed job sizes without error
     ja = B.JobArray(_job())
     assert B.workspace_bytes(ja) > 0

@@ -147,7 +147,7 @@ def config2(replicas: int = 1024, n_rates: int = 32, rate_index=None,
 
 
 def config3(replicas: int = 1024, n_rates: int = 32, rate_index=None,
-            record_capacity: int = 1 << 14) -> List[Job]:
+            record_capacity: int = 1 << 15) -> List[Job]:
     """Nested WAIT, unknown outputs: C2's prompts and mix, outputs geometric
     with means (64, 256, 512) capped at 2048, segments (64, 256, 1024, 2048),
     thresholds 1 per segment, C = 131072."""
@@ -195,7 +195,7 @@ def config4(replicas: int = 16, grid: int = 16, n_rates: int = 16,
     return jobs
 
 
-def config5(replicas: int = 8192, record_capacity: int = 1 << 14) -> List[Job]:
+def config5(replicas: int = 8192, record_capacity: int = 1 << 18) -> List[Job]:
     """Heavy-tailed 10-type mix: prompts = decile medians of LogNormal(6, 0.8),
     outputs clamp(ceil(LogNormal(5.5, 1.0)), 1, 4096), Nested WAIT with
     segments (128, 256, 512, 1024, 2048, 4096), thresholds 1, C = 262144,
