@@ -77,6 +77,7 @@ struct KArgs {
   int32_t hist_stride;
   int64_t horizon;
   int32_t resume;
+  int32_t any_trace;   // some job of this launch replays a fixed arrival list
 };
 
 __device__ __forceinline__ int64_t slot_i(const KArgs &A, int s, int64_t r) {
@@ -215,20 +216,29 @@ struct NRec {   // Nested WAIT boundary / interior record, 32 bytes
   uint32_t next;// calendar-bucket link
 };
 
+// Opaque copy: stops the compiler from turning a chain of selects over the
+// elements of a register array back into a dynamically indexed access (which
+// would move the array to scratch memory).
+template <typename T>
+__device__ __forceinline__ T opaque(T x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// a[j] for a lane-dependent j, as selects over the elements.
 template <typename T, int MT>
 __device__ __forceinline__ T pick(const T (&a)[MT], int j) {
-  T v = a[0];
+  T v = opaque(a[0]);
 #pragma unroll
-  for (int i = 1; i < MT; ++i)
-    if (i == j) v = a[i];
+  for (int i = 1; i < MT; ++i) v = (i == j) ? opaque(a[i]) : v;
   return v;
 }
 
+// a[j] = v for a lane-dependent j, as selects over the elements.
 template <typename T, int MT>
 __device__ __forceinline__ void place(T (&a)[MT], int j, T v) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
-    if (i == j) a[i] = v;
+  for (int i = 0; i < MT; ++i) a[i] = opaque((i == j) ? v : a[i]);
 }
 
 // Launchers, one per kernel family (defined next to their kernels).

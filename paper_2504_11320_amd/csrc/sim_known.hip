@@ -14,6 +14,14 @@
 // matrix: admissions push at the back, completions pop at the front, LIFO
 // evictions pop at the back, and each step costs O(events), not O(stages).
 //
+// Latency: the hot ends of every ring (queue head, deque front and back) are
+// cached in registers, so a pop needs no load; the refill of the cache is
+// issued at the pop and consumed later.  First tokens are counted per cohort
+// (how many prompts of the newest cohort have not produced one yet), so
+// resident records are never rewritten.  All lanes of a wavefront belong to
+// one job (the replica lists are padded per job), so the job's constants are
+// wavefront-uniform and live in scalar registers.
+//
 // Arithmetic follows the model contract exactly (same IEEE operations in the
 // same order, no FMA contraction), so integer state is bit-identical to the
 // oracle's and floating sums agree to rounding.
@@ -22,58 +30,80 @@
 namespace wsim {
 namespace {
 
-// ------------------------------------------------------- the kernel ------
-//
-// POL = WS_WAIT or WS_FCFS, known output lengths.  MT = compile-time bound on
-// the number of types (loops over types are unrolled so per-type state
-// stays in registers).
-
-template <int MT, int POL>
-__global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
+template <int MT, int POL, bool TRACE>
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
+sim_known_kernel(KArgs A) {
+  constexpr bool WAIT = POL == WS_WAIT;
+  __shared__ double s_edges[WS_MAX_HIST_EDGES];
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (gid >= A.n_list) return;
-  const int64_t r = ((const int32_t *)(A.ws + A.off_list))[gid];
-  const uint32_t jix = ((const uint32_t *)(A.ws + A.off_job_of))[r];
-  const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
+  // replica of this lane, or -1 for padding (padding only ends a job's last
+  // wavefront, so lane 0 of every wavefront holds a replica)
+  const int32_t r32 = gid < A.n_list ? ((const int32_t *)(A.ws + A.off_list))[gid] : -1;
+  const int64_t r = r32 < 0 ? 0 : r32;
+  // every lane of a wavefront belongs to the same job
+  const uint32_t jix =
+      __builtin_amdgcn_readfirstlane(((const uint32_t *)(A.ws + A.off_job_of))[r]);
+  const JobDev *J = ((const JobDev *)(A.ws + A.off_jobs)) + jix;
+
+  const int m = J->m;
+  const double d0 = J->d0, d1 = J->d1;
+  const int32_t C = (int32_t)J->C;  // <= 2^30
+  const int32_t cap_adm = (int32_t)(J->C - J->reserve_tok);
+  const int n_hist = J->n_hist;
+  // the latency histogram's edges, searched at every completion, staged in
+  // LDS by all lanes of the block (one wavefront, one job)
+  {
+    const double *edges_g = (const double *)(A.ws + J->off_edges);
+    for (int b = threadIdx.x; b < n_hist; b += 64) s_edges[b] = edges_g[b];
+    __syncthreads();
+  }
+  const double *edges = s_edges;
+  if (r32 < 0) return;  // padding lane
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
   const uint32_t rid = ((const uint32_t *)(A.ws + A.off_rid))[r];
-
-  const int m = J.m;
-  const double d0 = J.d0, d1 = J.d1;
-  const int64_t C = J.C;
-  const int64_t cap_adm = J.C - J.reserve_tok;
-  const int n_hist = J.n_hist;
-  const double *edges = (const double *)(A.ws + J.off_edges);
-  const bool trace = J.n_trace > 0;
-  const double *tr_time = (const double *)(A.ws + J.off_tr_time);
-  const int32_t *tr_type = (const int32_t *)(A.ws + J.off_tr_type);
-  const uint32_t qmask = (1u << J.qcap_log2) - 1u;
-  const uint32_t rec_cap = (uint32_t)J.rec_cap;
-  uint8_t *blk = A.ws + J.off_ring + (uint64_t)(r - J.replica_begin) * J.ring_stride;
+  const bool trace = TRACE && J->n_trace > 0;  // compiled out of the common kernel
+  const int64_t n_trace = J->n_trace;
+  const double *tr_time = (const double *)(A.ws + J->off_tr_time);
+  const int32_t *tr_type = (const int32_t *)(A.ws + J->off_tr_type);
+  const uint32_t qmask = (1u << J->qcap_log2) - 1u;
+  const uint32_t rec_cap = (uint32_t)J->rec_cap;
+  uint8_t *blk = A.ws + J->off_ring + (uint64_t)(r - J->replica_begin) * J->ring_stride;
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
 
   int32_t l[MT], lp[MT], nth[MT];
   double lam[MT];
   uint32_t dmask[MT];
   uint32_t qoff[MT], doff[MT];  // ring offsets inside the replica block
-  double tnext[MT];
-  uint32_t kk[MT], qh[MT], qt[MT], dh[MT], dt[MT], svc[MT];
-  int64_t Mj[MT];
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
     const bool on = j < m;
-    l[j] = on ? J.l[j] : 0;
-    lp[j] = on ? J.lp[j] : 1;
-    nth[j] = on ? J.n[j] : 0;
-    lam[j] = on ? J.lambda[j] : 0.0;
-    dmask[j] = on ? (1u << J.dcap_log2[j]) - 1u : 0u;
-    qoff[j] = (uint32_t)J.off_q[on ? j : 0];
-    doff[j] = (uint32_t)J.off_d[on ? j : 0];
+    l[j] = on ? J->l[j] : 0;
+    lp[j] = on ? J->lp[j] : 1;
+    nth[j] = on ? J->n[j] : 0;
+    lam[j] = on ? J->lambda[j] : 0.0;
+    dmask[j] = on ? (1u << J->dcap_log2[j]) - 1u : 0u;
+    qoff[j] = (uint32_t)J->off_q[on && WAIT ? j : 0];
+    doff[j] = (uint32_t)J->off_d[on ? j : 0];
   }
+
+  // per-type state
+  double tnext[MT];
+  uint32_t kk[MT], qh[MT], qt[MT], dh[MT], dt[MT], svc[MT], pend[MT];
+  int64_t Mj[MT];
+  double qhead[MT];      // WAIT: record at each queue's head
+  QRec qhead0;           // FCFS: record at the shared queue's head
+  // cached deque ends, one array per field (arrays of structs would be
+  // indexed as memory by the compiler)
+  double fa[MT], ba[MT];
+  uint32_t fkb[MT], fkc[MT], bkb[MT], bkc[MT];
 
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
   int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, N, U, Mres, tridx;
   uint32_t flags;
+
+  auto qring = [&](int j) __attribute__((always_inline)) { return (double *)(blk + qoff[j]); };
+  auto qring0 = [&]() __attribute__((always_inline)) { return (QRec *)(blk + qoff[0]); };
+  auto dring = [&](int j) __attribute__((always_inline)) { return (DRec *)(blk + doff[j]); };
 
   if (!A.resume) {
     t = lat_area = ttft_area = lat_sum = mem_area = busy = 0.0;
@@ -82,13 +112,11 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
     flags = 0;
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-      kk[j] = qh[j] = qt[j] = dh[j] = dt[j] = svc[j] = 0;
+      kk[j] = qh[j] = qt[j] = dh[j] = dt[j] = svc[j] = pend[j] = 0;
       Mj[j] = 0;
       tnext[j] = INFINITY;
-      if (j < m && !trace) {
-        int32_t dummy;
-        tnext[j] = 0.0 + draw_gap(seed, rid, (uint32_t)j, 0u, lam[j], nullptr, 0, &dummy);
-      }
+      if (j < m && !trace)
+        tnext[j] = 0.0 + draw_gap(seed, rid, (uint32_t)j, 0u, lam[j], nullptr, 0, nullptr);
     }
     for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
   } else {
@@ -122,13 +150,119 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
       dt[j] = (uint32_t)slot_i(A, S_DT + j, r);
       svc[j] = (uint32_t)slot_i(A, S_SVC + j, r);
       Mj[j] = slot_i(A, S_MJ + j, r);
+      pend[j] = (uint32_t)slot_i(A, S_LNEXT + j, r);
     }
   }
+  // caches of the ring ends
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    if (WAIT && qt[j] != qh[j]) qhead[j] = qring(j)[qh[j] & qmask];
+    if (dt[j] != dh[j]) {
+      const DRec f = dring(j)[dh[j] & dmask[j]];
+      const DRec b = dring(j)[(dt[j] - 1u) & dmask[j]];
+      fa[j] = f.a_ft;
+      fkb[j] = f.kb;
+      fkc[j] = f.kc;
+      ba[j] = b.a_ft;
+      bkb[j] = b.kb;
+      bkc[j] = b.kc;
+    }
+  }
+  if (!WAIT && qt[0] != qh[0]) qhead0 = qring0()[qh[0] & qmask];
 
+  // ---- ring operations ------------------------------------------------------
+  // Operations with a compile-time type index j (inside unrolled loops).
+  auto dpush = [&](int j, double a_ft, uint32_t kb, uint32_t kc) __attribute__((always_inline)) {
+    DRec rec;
+    rec.a_ft = a_ft;
+    rec.kb = kb;
+    rec.kc = kc;
+    dring(j)[dt[j] & dmask[j]] = rec;
+    if (dt[j] == dh[j]) {
+      fa[j] = a_ft;
+      fkb[j] = kb;
+      fkc[j] = kc;
+    }
+    ba[j] = a_ft;
+    bkb[j] = kb;
+    bkc[j] = kc;
+    dt[j]++;
+  };
+  auto dpop_front = [&](int j) __attribute__((always_inline)) {
+    dh[j]++;
+    if (dh[j] + 1u == dt[j]) {
+      fa[j] = ba[j];
+      fkb[j] = bkb[j];
+      fkc[j] = bkc[j];
+    } else if (dh[j] != dt[j]) {
+      const DRec f = dring(j)[dh[j] & dmask[j]];
+      fa[j] = f.a_ft;
+      fkb[j] = f.kb;
+      fkc[j] = f.kc;
+    }
+  };
+  // Operations with a lane-dependent type index: every per-type array is
+  // read and written through selects (pick / place).
+  auto push_wait_dyn = [&](int j, double a_ft) __attribute__((always_inline)) {
+    const uint32_t h = pick(qh, j), tq = pick(qt, j);
+    if (tq - h >= rec_cap) {
+      flags |= kFlagCap;  // the replica stops at its next decision
+    } else {
+      ((double *)(blk + pick(qoff, j)))[tq & qmask] = a_ft;
+      if (tq == h) place(qhead, j, a_ft);
+    }
+    place(qt, j, tq + 1u);
+  };
+  auto push_fcfs = [&](double a_ft, int32_t j, int32_t L) __attribute__((always_inline)) {
+    if (qt[0] - qh[0] >= rec_cap) {
+      flags |= kFlagCap;
+    } else {
+      QRec rec;
+      rec.a_ft = a_ft;
+      rec.j = j;
+      rec.L = L;
+      qring0()[qt[0] & qmask] = rec;
+      if (qt[0] == qh[0]) qhead0 = rec;
+    }
+    qt[0]++;
+  };
+  auto dpush_dyn = [&](int j, double a_ft, uint32_t kb, uint32_t kc) __attribute__((always_inline)) {
+    const uint32_t tq = pick(dt, j);
+    DRec rec;
+    rec.a_ft = a_ft;
+    rec.kb = kb;
+    rec.kc = kc;
+    ((DRec *)(blk + pick(doff, j)))[tq & pick(dmask, j)] = rec;
+    if (tq == pick(dh, j)) {
+      place(fa, j, a_ft);
+      place(fkb, j, kb);
+      place(fkc, j, kc);
+    }
+    place(ba, j, a_ft);
+    place(bkb, j, kb);
+    place(bkc, j, kc);
+    place(dt, j, tq + 1u);
+  };
+  auto dpop_back_dyn = [&](int j) __attribute__((always_inline)) {
+    const uint32_t tq = pick(dt, j) - 1u, h = pick(dh, j);
+    place(dt, j, tq);
+    if (tq - 1u == h) {
+      place(ba, j, pick(fa, j));
+      place(bkb, j, pick(fkb, j));
+      place(bkc, j, pick(fkc, j));
+    } else if (tq != h) {
+      const DRec b = ((const DRec *)(blk + pick(doff, j)))[(tq - 1u) & pick(dmask, j)];
+      place(ba, j, b.a_ft);
+      place(bkb, j, b.kb);
+      place(bkc, j, b.kc);
+    }
+  };
+
+  // ---- arrivals ---------------------------------------------------------------
   // Next exogenous arrival (ties: lowest type); trace mode reads the list.
-  auto peek = [&](int &jn) -> double {
+  auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
     if (trace) {
-      if (tridx >= J.n_trace) {
+      if (tridx >= n_trace) {
         jn = 0;
         return INFINITY;
       }
@@ -146,64 +280,46 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
     return best;
   };
 
-  // Append the pending arrival of type jn (time a) to its external queue
-  // and draw that type's next arrival.
-  auto take = [&](int jn, double a) {
+  // Append the pending arrival of type jn (time a) to its external queue and
+  // draw that type's next arrival.
+  auto take = [&](int jn, double a) __attribute__((always_inline)) {
     if (trace) {
       tridx++;
     } else {
-      uint32_t k = pick(kk, jn) + 1u;
+      const uint32_t k = pick(kk, jn) + 1u;
       place(kk, jn, k);
-      int32_t dummy;
-      const double g = draw_gap(seed, rid, (uint32_t)jn, k, pick(lam, jn), nullptr, 0, &dummy);
+      const double g = draw_gap(seed, rid, (uint32_t)jn, k, pick(lam, jn), nullptr, 0, nullptr);
       place(tnext, jn, pick(tnext, jn) + g);
     }
     arrivals++;
     N++;
     U++;
-    if (POL == WS_WAIT) {
-      const uint32_t h = pick(qh, jn), tt = pick(qt, jn);
-      if (tt - h >= rec_cap)
-        flags |= kFlagCap;
-      else
-        ((double *)(blk + pick(qoff, jn)))[tt & qmask] = a;
-      place(qt, jn, tt + 1u);
-    } else {
-      const uint32_t h = qh[0], tt = qt[0];
-      if (tt - h >= rec_cap) {
-        flags |= kFlagCap;
-      } else {
-        QRec rec;
-        rec.a_ft = a;
-        rec.j = jn;
-        rec.L = pick(lp, jn);
-        ((QRec *)(blk + qoff[0]))[tt & qmask] = rec;
-      }
-      qt[0] = tt + 1u;
-    }
+    if (WAIT)
+      push_wait_dyn(jn, a);
+    else
+      push_fcfs(a, jn, pick(lp, jn));
   };
 
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
-  uint32_t newcnt[MT];
+  uint32_t fresh[MT], pendnew[MT];
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- decision: form a batch or wait for the next arrival ------------
     uint32_t elig = 0;
-    int64_t tokens = 0, prefill_l = 0;
     for (;;) {
       if (flags & kFlagCap) {
         stopped = true;
         break;
       }
       elig = 0;
-      if (POL == WS_WAIT) {
+      if (WAIT) {
 #pragma unroll
         for (int j = 0; j < MT; ++j)
           if (j < m && (qt[j] - qh[j]) >= (uint32_t)nth[j]) elig |= 1u << j;
       } else {
-        int64_t resident = 0;
+        uint32_t resident = 0;
 #pragma unroll
-        for (int j = 0; j < MT; ++j) resident += (int64_t)(dt[j] - dh[j]);
+        for (int j = 0; j < MT; ++j) resident += dt[j] - dh[j];
         if (resident > 0 || qt[0] != qh[0]) elig = 1;
       }
       if (elig) break;
@@ -233,51 +349,39 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
     if (stopped) break;
 
     // ---- launch: admissions and batch tokens --------------------------
-#pragma unroll
-    for (int j = 0; j < MT; ++j) newcnt[j] = 0;
     const uint32_t bidx = (uint32_t)batches;
-    if (POL == WS_WAIT) {
+    int64_t tokens = 0, prefill_l = 0;
+#pragma unroll
+    for (int j = 0; j < MT; ++j) fresh[j] = pendnew[j] = 0;
+    if (WAIT) {
 #pragma unroll
       for (int j = 0; j < MT; ++j) {
         if (!(elig & (1u << j))) continue;
-        const double *q = (const double *)(blk + qoff[j]);
-        DRec *d = (DRec *)(blk + doff[j]);
         const uint32_t c = svc[j] + 1u;
         for (int x = 0; x < nth[j]; ++x) {
-          DRec rec;
-          rec.a_ft = q[qh[j] & qmask];
-          rec.kb = bidx;
-          rec.kc = c;
-          d[dt[j] & dmask[j]] = rec;
+          const double a_ft = qhead[j];
           qh[j]++;
-          dt[j]++;
+          if (qt[j] != qh[j]) qhead[j] = qring(j)[qh[j] & qmask];
+          dpush(j, a_ft, bidx, c);
+          pendnew[j] += has_ft(a_ft) ? 0u : 1u;
         }
-        newcnt[j] = (uint32_t)nth[j];
+        fresh[j] = (uint32_t)nth[j];
         tokens += (int64_t)nth[j] * l[j] + Mj[j];
         prefill_l += (int64_t)nth[j] * l[j];
       }
     } else {
       tokens = Mres;
-      const QRec *q = (const QRec *)(blk + qoff[0]);
       uint32_t p = 0;
       while (qt[0] != qh[0]) {
-        const QRec head = q[qh[0] & qmask];
+        const QRec head = qhead0;
         const int hj = head.j;
         const int64_t hl = pick(l, hj);
         if (Mres + prefill_l + hl > cap_adm) break;
         qh[0]++;
-        DRec rec;
-        rec.a_ft = head.a_ft;
-        rec.kb = bidx;
-        rec.kc = p++;
-#pragma unroll
-        for (int j = 0; j < MT; ++j)
-          if (j == hj) {
-            DRec *d = (DRec *)(blk + doff[j]);
-            d[dt[j] & dmask[j]] = rec;
-            dt[j]++;
-            newcnt[j]++;
-          }
+        if (qt[0] != qh[0]) qhead0 = qring0()[qh[0] & qmask];
+        dpush_dyn(hj, head.a_ft, bidx, p++);
+        place(fresh, hj, pick(fresh, hj) + 1u);
+        place(pendnew, hj, pick(pendnew, hj) + (has_ft(head.a_ft) ? 0u : 1u));
         prefill_l += hl;
       }
       tokens += prefill_l;
@@ -308,60 +412,32 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
     // ---- completion transition ------------------------------------------
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-      const bool served = (POL == WS_WAIT) ? ((elig >> j) & 1u) != 0
-                                           : (j < m && (dt[j] - dh[j]) > 0);
+      const bool served = WAIT ? ((elig >> j) & 1u) != 0 : j < m;
       if (!served) continue;
-      DRec *d = (DRec *)(blk + doff[j]);
-      // stage reached by a record: WAIT counts services of its type, FCFS
-      // counts batches
-      const uint32_t now = (POL == WS_WAIT) ? svc[j] + 1u : bidx;
-      if (POL == WS_WAIT) svc[j] = now;
-      const uint32_t fresh = newcnt[j];
-      const uint32_t before = (dt[j] - dh[j]) - fresh;  // residents at launch
-      // completions: processed at stage l'_j
+      // the stage-1 cohort produces its first tokens
+      U -= pend[j];
+      pend[j] = pendnew[j];
+      // stage reached: WAIT counts services of the type, FCFS counts batches
+      const uint32_t now = WAIT ? svc[j] + 1u : bidx;
+      if (WAIT) svc[j] = now;
+      const uint32_t before = (dt[j] - dh[j]) - fresh[j];  // residents at launch
       uint32_t done = 0;
+      // completions: processed at stage l'_j (fresh records never qualify)
       while (done < before) {
-        const DRec rec = d[dh[j] & dmask[j]];
-        const uint32_t adm = rec.kc;
-        const uint32_t admb = (POL == WS_WAIT) ? adm : rec.kb;
+        const uint32_t admb = WAIT ? fkc[j] : fkb[j];
         if (admb + (uint32_t)lp[j] != now) break;
-        if (!has_ft(rec.a_ft)) U--;  // l'_j = 1: first token at completion
-        const double lat = t_end - arrival_of(rec.a_ft);
+        const double lat = t_end - arrival_of(fa[j]);
         lat_sum += lat;
-        int lo = 0, hi = n_hist;
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          if (edges[mid] <= lat)
-            lo = mid + 1;
-          else
-            hi = mid;
-        }
-        hist[lo] += 1u;
+        __hip_atomic_fetch_add(&hist[hist_bin(edges, n_hist, lat)], 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
         comps++;
         ctok += lp[j];
         N--;
-        Mj[j] -= (int64_t)l[j] + lp[j];
-        dh[j]++;
+        dpop_front(j);
         done++;
       }
-      // first tokens: residents processed at stage 1 (admitted one service
-      // earlier), located just before this launch's admissions
-      if (lp[j] > 1) {
-        uint32_t idx = dt[j] - fresh;
-        uint32_t left = before - done;
-        while (left > 0) {
-          DRec *pr = &d[(idx - 1u) & dmask[j]];
-          const uint32_t admb = (POL == WS_WAIT) ? pr->kc : pr->kb;
-          if (admb + 1u != now) break;
-          if (!has_ft(pr->a_ft)) {
-            pr->a_ft = with_ft(pr->a_ft);
-            U--;
-          }
-          idx--;
-          left--;
-        }
-      }
-      Mj[j] += (int64_t)(before - done) + (int64_t)fresh * (l[j] + 1);
+      Mj[j] += (int64_t)(before - done) + (int64_t)fresh[j] * (l[j] + 1) -
+               (int64_t)done * ((int64_t)l[j] + lp[j]);
     }
     Mres = 0;
 #pragma unroll
@@ -375,51 +451,32 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
 #pragma unroll
       for (int j = 0; j < MT; ++j) {
         if (j >= m || dt[j] == dh[j]) continue;
-        const DRec *d = (const DRec *)(blk + doff[j]);
-        const DRec rec = d[(dt[j] - 1u) & dmask[j]];
-        const uint32_t pb = (POL == WS_WAIT) ? (uint32_t)j : rec.kc;
-        if (jb < 0 || rec.kb > bb || (rec.kb == bb && pb > bp)) {
+        const uint32_t pb = WAIT ? (uint32_t)j : bkc[j];
+        if (jb < 0 || bkb[j] > bb || (bkb[j] == bb && pb > bp)) {
           jb = j;
-          bb = rec.kb;
+          bb = bkb[j];
           bp = pb;
         }
       }
       if (jb < 0) break;
-#pragma unroll
-      for (int j = 0; j < MT; ++j) {
-        if (j != jb) continue;
-        DRec *d = (DRec *)(blk + doff[j]);
-        const DRec rec = d[(dt[j] - 1u) & dmask[j]];
-        dt[j]--;
-        const uint32_t admb = (POL == WS_WAIT) ? rec.kc : rec.kb;
-        const uint32_t now = (POL == WS_WAIT) ? svc[j] : bidx;
-        const int64_t stage = (int64_t)(now - admb) + 1;
-        Mj[j] -= (int64_t)l[j] + stage;
-        Mres -= (int64_t)l[j] + stage;
-        evicts++;
-        etok += stage - 1;
-        // back to the tail of the external queue
-        if (POL == WS_WAIT) {
-          double *q = (double *)(blk + qoff[j]);
-          if (qt[j] - qh[j] >= rec_cap)
-            flags |= kFlagCap;
-          else
-            q[qt[j] & qmask] = rec.a_ft;
-          qt[j]++;
-        } else {
-          QRec *q = (QRec *)(blk + qoff[0]);
-          if (qt[0] - qh[0] >= rec_cap) {
-            flags |= kFlagCap;
-          } else {
-            QRec qr;
-            qr.a_ft = rec.a_ft;
-            qr.j = j;
-            qr.L = lp[j];
-            q[qt[0] & qmask] = qr;
-          }
-          qt[0]++;
-        }
-      }
+      const double ra = pick(ba, jb);
+      const uint32_t rkb = pick(bkb, jb), rkc = pick(bkc, jb);
+      dpop_back_dyn(jb);
+      const uint32_t admb = WAIT ? rkc : rkb;
+      const uint32_t now = WAIT ? pick(svc, jb) : bidx;
+      const int64_t stage = (int64_t)(now - admb) + 1;
+      const int64_t ch = (int64_t)pick(l, jb) + stage;
+      place(Mj, jb, pick(Mj, jb) - ch);
+      Mres -= ch;
+      evicts++;
+      etok += stage - 1;
+      const bool ft = has_ft(ra);
+      if (stage == 1 && !ft) place(pend, jb, pick(pend, jb) - 1u);
+      const double a_ft = (ft || stage >= 2) ? with_ft(ra) : ra;
+      if (WAIT)
+        push_wait_dyn(jb, a_ft);
+      else
+        push_fcfs(a_ft, jb, pick(lp, jb));
     }
     batches++;
     btok += tokens;
@@ -457,6 +514,7 @@ __global__ void __launch_bounds__(64) sim_known_kernel(KArgs A) {
     put_i(A, S_DT + j, r, dt[j]);
     put_i(A, S_SVC + j, r, svc[j]);
     put_i(A, S_MJ + j, r, Mj[j]);
+    put_i(A, S_LNEXT + j, r, pend[j]);
   }
 }
 
@@ -464,7 +522,10 @@ template <int MT, int POL>
 hipError_t launch_mt(const KArgs &A, hipStream_t s) {
   const int threads = 64;
   const int blocks = (A.n_list + threads - 1) / threads;
-  hipLaunchKernelGGL((sim_known_kernel<MT, POL>), dim3(blocks), dim3(threads), 0, s, A);
+  if (A.any_trace)
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, true>), dim3(blocks), dim3(threads), 0, s, A);
+  else
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false>), dim3(blocks), dim3(threads), 0, s, A);
   return hipGetLastError();
 }
 

@@ -47,7 +47,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tx;
   if (gid >= A.n_list) return;  // lanes use only their own LDS column
-  const int64_t r = ((const int32_t *)(A.ws + A.off_list))[gid];
+  const int32_t r32 = ((const int32_t *)(A.ws + A.off_list))[gid];
+  if (r32 < 0) return;  // padding lane
+  const int64_t r = r32;
   const uint32_t jix = ((const uint32_t *)(A.ws + A.off_job_of))[r];
   const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
@@ -72,12 +74,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   QRec *q10 = (QRec *)(blk + J.off_q[0]);
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
 
-  auto recs = [&](int k) { return (NRec *)(blk + J.off_rec[k]); };
-  auto bkts = [&](int k) { return (uint32_t *)(blk + J.off_bkt[k]); };
-  auto metas = [&](int k) { return (SlotMeta *)(blk + J.off_meta[k]); };
-  auto vring = [&](int k) { return (NRec *)(blk + J.off_v[k]); };
-  auto vmask = [&](int k) { return (1u << J.vcap_log2[k]) - 1u; };
-  auto row_of = [&](int j) -> const uint32_t * {
+  auto recs = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + J.off_rec[k]); };
+  auto bkts = [&](int k) __attribute__((always_inline)) { return (uint32_t *)(blk + J.off_bkt[k]); };
+  auto metas = [&](int k) __attribute__((always_inline)) { return (SlotMeta *)(blk + J.off_meta[k]); };
+  auto vring = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + J.off_v[k]); };
+  auto vmask = [&](int k) __attribute__((always_inline)) { return (1u << J.vcap_log2[k]) - 1u; };
+  auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
     return (known || cap <= 1) ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
   };
 
@@ -158,7 +160,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   }
 
   // ---- arrivals ------------------------------------------------------------
-  auto peek = [&](int &jn) -> double {
+  auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
     if (trace) {
       if (tridx >= J.n_trace) {
         jn = 0;
@@ -179,7 +181,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return best;
   };
 
-  auto push_q10 = [&](double a_ft, int32_t j, int32_t Lr) {
+  auto push_q10 = [&](double a_ft, int32_t j, int32_t Lr) __attribute__((always_inline)) {
     if (qt - qh >= rec_cap) {
       flags |= kFlagCap;
     } else {
@@ -192,7 +194,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     qt++;
   };
 
-  auto take = [&](int jn, double a) {
+  auto take = [&](int jn, double a) __attribute__((always_inline)) {
     int32_t Lr;
     if (trace) {
       Lr = known ? J.lp[jn] : tr_len[tridx];
@@ -214,7 +216,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
   // ---- evictions -------------------------------------------------------------
   // Evict the back (most recently admitted) prompt of boundary queue h >= 1.
-  auto evict_boundary = [&](int h) -> int64_t {
+  auto evict_boundary = [&](int h) __attribute__((always_inline)) -> int64_t {
     NRec *v = vring(h);
     const uint32_t vt = s_vt[h][tx] - 1u;
     const NRec rec = v[vt & vmask(h)];
@@ -232,7 +234,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // Most recently admitted live interior prompt of segment k: the newest
   // non-empty cohort slot, its highest live index.  Returns the record index
   // or kNil.
-  auto youngest_interior = [&](int k, uint32_t &kb, uint32_t &kp) -> uint32_t {
+  auto youngest_interior = [&](int k, uint32_t &kb, uint32_t &kp) __attribute__((always_inline)) -> uint32_t {
     if (s_I[k][tx] == 0) return kNil;
     const int32_t delta = J.seg_delta[k];
     const int32_t nk = J.seg_n[k];
@@ -255,7 +257,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return kNil;
   };
 
-  auto evict_interior = [&](int k, uint32_t idx) -> int64_t {
+  auto evict_interior = [&](int k, uint32_t idx) __attribute__((always_inline)) -> int64_t {
     NRec *rc = recs(k);
     NRec rec = rc[idx];
     const int32_t delta = J.seg_delta[k];
@@ -285,7 +287,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // Evict the most recently admitted prompt among boundary queues
   // h in [hlo, L) and, if fallback is set and none exists, among the interior
   // of segments [klo, L).  Returns the memory freed, 0 if nothing was left.
-  auto evict_lifo = [&](int klo, bool allow_interior) -> int64_t {
+  auto evict_lifo = [&](int klo, bool allow_interior) __attribute__((always_inline)) -> int64_t {
     int hb = -1;
     uint32_t bkb = 0, bkp = 0;
     for (int h = 1; h < L; ++h) {

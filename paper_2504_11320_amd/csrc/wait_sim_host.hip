@@ -276,7 +276,8 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     R += jobs[i].n;
     hmax = std::max(hmax, jobs[i].cfg->n_hist + 1);
     const int pk = jobs[i].pol->kind;
-    Lo.list_count[pk] += jobs[i].n;
+    // each job starts a new wavefront: its constants are wavefront-uniform
+    Lo.list_count[pk] += (jobs[i].n + 63) / 64 * 64;
     Lo.max_m[pk] = std::max(Lo.max_m[pk], jobs[i].cfg->m);
     if (pk == WS_NESTED_WAIT) Lo.max_seg = std::max(Lo.max_seg, jobs[i].pol->L);
   }
@@ -416,6 +417,7 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
       std::memcpy(img.data() + Lo.off_job_of + 4 * r, &ji, 4);
       lists[jb.pol->kind].push_back((int32_t)r);
     }
+    while (lists[jb.pol->kind].size() % 64 != 0) lists[jb.pol->kind].push_back(-1);
     const ws_config &c = *jb.cfg;
     const JobDev &d = Lo.jobs[i].d;
     if (c.n_hist > 0) std::memcpy(img.data() + d.off_edges, c.hist_edges, 8ull * c.n_hist);
@@ -456,6 +458,9 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     KArgs B = A;
     B.off_list = Lo.list_off[pk];
     B.n_list = Lo.list_count[pk];
+    B.any_trace = 0;
+    for (int i = 0; i < n_jobs; ++i)
+      if (jobs[i].pol->kind == pk && jobs[i].cfg->n_trace > 0) B.any_trace = 1;
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)
       e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, s);
