@@ -174,17 +174,18 @@ __device__ __forceinline__ double draw_gap(uint64_t seed, uint32_t rid,
   return -ln_unit(u) / lam;
 }
 
-// Histogram bin of a latency: number of edges <= lat.
+// Histogram bin of a latency: number of edges <= lat (edges strictly
+// increasing, n <= 255).  Branch-free: a fixed sequence of 8 halving steps
+// over the virtual array padded with +infinity up to 255 entries.
 __device__ __forceinline__ int hist_bin(const double *edges, int n, double lat) {
-  int lo = 0, hi = n;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (edges[mid] <= lat)
-      lo = mid + 1;
-    else
-      hi = mid;
+  int pos = 0;  // number of edges known to be <= lat
+#pragma unroll
+  for (int step = 128; step >= 1; step >>= 1) {
+    const int probe = pos + step;  // 1-based candidate count
+    const bool le = probe <= n && edges[probe <= n ? probe - 1 : 0] <= lat;
+    pos = le ? probe : pos;
   }
-  return lo;
+  return pos;
 }
 
 // ------------------------------------------------------------- records --
@@ -228,9 +229,13 @@ __device__ __forceinline__ T opaque(T x) {
 // a[j] for a lane-dependent j, as selects over the elements.
 template <typename T, int MT>
 __device__ __forceinline__ T pick(const T (&a)[MT], int j) {
-  T v = opaque(a[0]);
+  // the barriers run unconditionally so the choice stays a select
+  T e[MT];
 #pragma unroll
-  for (int i = 1; i < MT; ++i) v = (i == j) ? opaque(a[i]) : v;
+  for (int i = 0; i < MT; ++i) e[i] = opaque(a[i]);
+  T v = e[0];
+#pragma unroll
+  for (int i = 1; i < MT; ++i) v = (i == j) ? e[i] : v;
   return v;
 }
 

@@ -34,7 +34,21 @@ template <int MT, int POL, bool TRACE>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 sim_known_kernel(KArgs A) {
   constexpr bool WAIT = POL == WS_WAIT;
+  // Inter-arrival gaps are drawn ahead of use by the whole wavefront at once
+  // (64 draws per pass, no divergence) into a ring of GR gaps per type and
+  // lane; a lane whose ring runs dry draws the gap itself.
+  constexpr int GR = MT <= 4 ? 16 : 4;  // ring size per (type, lane)
+  constexpr int GU = GR / 2;            // gaps added per refill
+  constexpr uint32_t kLow = GU / 2;     // a lane below this triggers a refill
   __shared__ double s_edges[WS_MAX_HIST_EDGES];
+  __shared__ double s_gap[MT][GR][64];
+  __shared__ uint64_t s_seed[64];
+  __shared__ uint32_t s_rid[64], s_req_lane[64], s_req_k[64];
+  // The last WB records pushed on each resident deque are also kept in LDS,
+  // so LIFO evictions (which pop the back) rarely read HBM.
+  constexpr int WB = MT <= 4 ? 8 : 2;
+  __shared__ DRec s_win[MT][WB][64];
+  const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   // replica of this lane, or -1 for padding (padding only ends a job's last
   // wavefront, so lane 0 of every wavefront holds a replica)
@@ -61,6 +75,8 @@ sim_known_kernel(KArgs A) {
   if (r32 < 0) return;  // padding lane
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
   const uint32_t rid = ((const uint32_t *)(A.ws + A.off_rid))[r];
+  s_seed[tx] = seed;
+  s_rid[tx] = rid;
   const bool trace = TRACE && J->n_trace > 0;  // compiled out of the common kernel
   const int64_t n_trace = J->n_trace;
   const double *tr_time = (const double *)(A.ws + J->off_tr_time);
@@ -89,6 +105,8 @@ sim_known_kernel(KArgs A) {
   // per-type state
   double tnext[MT];
   uint32_t kk[MT], qh[MT], qt[MT], dh[MT], dt[MT], svc[MT], pend[MT];
+  uint32_t gend[MT];  // gaps of arrivals kk+1 .. gend-1 are in the ring
+  uint32_t lv[MT];    // deque records lv .. dt-1 are also in the LDS window
   int64_t Mj[MT];
   double qhead[MT];      // WAIT: record at each queue's head
   QRec qhead0;           // FCFS: record at the shared queue's head
@@ -153,9 +171,11 @@ sim_known_kernel(KArgs A) {
       pend[j] = (uint32_t)slot_i(A, S_LNEXT + j, r);
     }
   }
-  // caches of the ring ends
+  // caches of the ring ends; the gap rings start empty
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
+    gend[j] = kk[j] + 1u;
+    lv[j] = dt[j];
     if (WAIT && qt[j] != qh[j]) qhead[j] = qring(j)[qh[j] & qmask];
     if (dt[j] != dh[j]) {
       const DRec f = dring(j)[dh[j] & dmask[j]];
@@ -178,6 +198,8 @@ sim_known_kernel(KArgs A) {
     rec.kb = kb;
     rec.kc = kc;
     dring(j)[dt[j] & dmask[j]] = rec;
+    s_win[j][dt[j] % WB][tx] = rec;
+    if (dt[j] + 1u > (uint32_t)WB && dt[j] + 1u - WB > lv[j]) lv[j] = dt[j] + 1u - WB;
     if (dt[j] == dh[j]) {
       fa[j] = a_ft;
       fkb[j] = kb;
@@ -195,7 +217,7 @@ sim_known_kernel(KArgs A) {
       fkb[j] = bkb[j];
       fkc[j] = bkc[j];
     } else if (dh[j] != dt[j]) {
-      const DRec f = dring(j)[dh[j] & dmask[j]];
+      const DRec f = dh[j] >= lv[j] ? s_win[j][dh[j] % WB][tx] : dring(j)[dh[j] & dmask[j]];
       fa[j] = f.a_ft;
       fkb[j] = f.kb;
       fkc[j] = f.kc;
@@ -233,6 +255,9 @@ sim_known_kernel(KArgs A) {
     rec.kb = kb;
     rec.kc = kc;
     ((DRec *)(blk + pick(doff, j)))[tq & pick(dmask, j)] = rec;
+    s_win[j][tq % WB][tx] = rec;
+    const uint32_t lvj = pick(lv, j);
+    if (tq + 1u > (uint32_t)WB && tq + 1u - WB > lvj) place(lv, j, tq + 1u - WB);
     if (tq == pick(dh, j)) {
       place(fa, j, a_ft);
       place(fkb, j, kb);
@@ -251,7 +276,9 @@ sim_known_kernel(KArgs A) {
       place(bkb, j, pick(fkb, j));
       place(bkc, j, pick(fkc, j));
     } else if (tq != h) {
-      const DRec b = ((const DRec *)(blk + pick(doff, j)))[(tq - 1u) & pick(dmask, j)];
+      const DRec b = (tq - 1u >= pick(lv, j))
+                         ? s_win[j][(tq - 1u) % WB][tx]
+                         : ((const DRec *)(blk + pick(doff, j)))[(tq - 1u) & pick(dmask, j)];
       place(ba, j, b.a_ft);
       place(bkb, j, b.kb);
       place(bkc, j, b.kc);
@@ -288,7 +315,13 @@ sim_known_kernel(KArgs A) {
     } else {
       const uint32_t k = pick(kk, jn) + 1u;
       place(kk, jn, k);
-      const double g = draw_gap(seed, rid, (uint32_t)jn, k, pick(lam, jn), nullptr, 0, nullptr);
+      double g;
+      if (k < pick(gend, jn)) {
+        g = s_gap[jn][k % GR][tx];
+      } else {
+        g = draw_gap(seed, rid, (uint32_t)jn, k, pick(lam, jn), nullptr, 0, nullptr);
+        place(gend, jn, k + 1u);
+      }
       place(tnext, jn, pick(tnext, jn) + g);
     }
     arrivals++;
@@ -304,6 +337,42 @@ sim_known_kernel(KArgs A) {
   uint32_t fresh[MT], pendnew[MT];
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
+    // ---- refill the gap rings, all active lanes together ----------------
+    if (!TRACE) {
+      const uint64_t act = __ballot(1);
+      const int nact = __popcll(act);
+      const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)act, 0u));
+#pragma unroll
+      for (int j = 0; j < MT; ++j) {
+        if (j >= m) continue;
+        const uint32_t avail = gend[j] - kk[j] - 1u;
+        if (__ballot(avail < kLow) == 0) continue;
+        const bool room = avail <= (uint32_t)(GR - GU);
+        const uint64_t need = __ballot(room);
+        const int p = __popcll(need);
+        if (room) {
+          const int rk = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(need >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
+          s_req_lane[rk] = (uint32_t)tx;
+          s_req_k[rk] = gend[j];
+        }
+        __syncthreads();
+        const int total = p * GU;
+        for (int base = 0; base < total; base += nact) {
+          const int w = base + wrank;
+          if (w < total) {
+            const int ln = (int)s_req_lane[w / GU];
+            const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
+            s_gap[j][k % GR][ln] =
+                draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lam[j], nullptr, 0, nullptr);
+          }
+        }
+        __syncthreads();
+        if (room) gend[j] += GU;
+      }
+    }
+
     // ---- decision: form a batch or wait for the next arrival ------------
     uint32_t elig = 0;
     for (;;) {
