@@ -246,6 +246,13 @@ __device__ __forceinline__ void place(T (&a)[MT], int j, T v) {
   for (int i = 0; i < MT; ++i) a[i] = opaque((i == j) ? v : a[i]);
 }
 
+// if (c) a[j] = v, without a branch.
+template <typename T, int MT>
+__device__ __forceinline__ void place_if(T (&a)[MT], int j, bool c, T v) {
+#pragma unroll
+  for (int i = 0; i < MT; ++i) a[i] = opaque((c && i == j) ? v : a[i]);
+}
+
 // Launchers, one per kernel family (defined next to their kernels).
 hipError_t launch_known(int policy, int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s);

@@ -107,7 +107,7 @@ sim_known_kernel(KArgs A) {
   uint32_t kk[MT], qh[MT], qt[MT], dh[MT], dt[MT], svc[MT], pend[MT];
   uint32_t gend[MT];  // gaps of arrivals kk+1 .. gend-1 are in the ring
   uint32_t lv[MT];    // deque records lv .. dt-1 are also in the LDS window
-  int64_t Mj[MT];
+  int32_t Mj[MT];  // resident memory per type (< 2C <= 2^31)
   double qhead[MT];      // WAIT: record at each queue's head
   QRec qhead0;           // FCFS: record at the shared queue's head
   // cached deque ends, one array per field (arrays of structs would be
@@ -116,7 +116,8 @@ sim_known_kernel(KArgs A) {
   uint32_t fkb[MT], fkc[MT], bkb[MT], bkc[MT];
 
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
-  int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, N, U, Mres, tridx;
+  int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, Mres, tridx;
+  int32_t N, U;  // requests in system, and those without a first token
   uint32_t flags;
 
   auto qring = [&](int j) __attribute__((always_inline)) { return (double *)(blk + qoff[j]); };
@@ -153,8 +154,8 @@ sim_known_kernel(KArgs A) {
     btok = slot_i(A, S_BTOK, r);
     peak = slot_i(A, S_PEAK, r);
     idle = slot_i(A, S_IDLE, r);
-    N = slot_i(A, S_N, r);
-    U = slot_i(A, S_U, r);
+    N = (int32_t)slot_i(A, S_N, r);
+    U = (int32_t)slot_i(A, S_U, r);
     Mres = slot_i(A, S_MRES, r);
     tridx = slot_i(A, S_TRIDX, r);
     flags = (uint32_t)slot_i(A, S_FLAGS, r);
@@ -167,7 +168,7 @@ sim_known_kernel(KArgs A) {
       dh[j] = (uint32_t)slot_i(A, S_DH + j, r);
       dt[j] = (uint32_t)slot_i(A, S_DT + j, r);
       svc[j] = (uint32_t)slot_i(A, S_SVC + j, r);
-      Mj[j] = slot_i(A, S_MJ + j, r);
+      Mj[j] = (int32_t)slot_i(A, S_MJ + j, r);
       pend[j] = (uint32_t)slot_i(A, S_LNEXT + j, r);
     }
   }
@@ -217,7 +218,11 @@ sim_known_kernel(KArgs A) {
       fkb[j] = bkb[j];
       fkc[j] = bkc[j];
     } else if (dh[j] != dt[j]) {
-      const DRec f = dh[j] >= lv[j] ? s_win[j][dh[j] % WB][tx] : dring(j)[dh[j] & dmask[j]];
+      DRec f;
+      if (dh[j] >= lv[j])
+        f = s_win[j][dh[j] % WB][tx];
+      else
+        f = dring(j)[dh[j] & dmask[j]];
       fa[j] = f.a_ft;
       fkb[j] = f.kb;
       fkc[j] = f.kc;
@@ -231,7 +236,7 @@ sim_known_kernel(KArgs A) {
       flags |= kFlagCap;  // the replica stops at its next decision
     } else {
       ((double *)(blk + pick(qoff, j)))[tq & qmask] = a_ft;
-      if (tq == h) place(qhead, j, a_ft);
+      place_if(qhead, j, tq == h, a_ft);
     }
     place(qt, j, tq + 1u);
   };
@@ -257,12 +262,11 @@ sim_known_kernel(KArgs A) {
     ((DRec *)(blk + pick(doff, j)))[tq & pick(dmask, j)] = rec;
     s_win[j][tq % WB][tx] = rec;
     const uint32_t lvj = pick(lv, j);
-    if (tq + 1u > (uint32_t)WB && tq + 1u - WB > lvj) place(lv, j, tq + 1u - WB);
-    if (tq == pick(dh, j)) {
-      place(fa, j, a_ft);
-      place(fkb, j, kb);
-      place(fkc, j, kc);
-    }
+    place_if(lv, j, tq + 1u > (uint32_t)WB && tq + 1u - WB > lvj, tq + 1u - WB);
+    const bool empty = tq == pick(dh, j);
+    place_if(fa, j, empty, a_ft);
+    place_if(fkb, j, empty, kb);
+    place_if(fkc, j, empty, kc);
     place(ba, j, a_ft);
     place(bkb, j, kb);
     place(bkc, j, kc);
@@ -276,9 +280,11 @@ sim_known_kernel(KArgs A) {
       place(bkb, j, pick(fkb, j));
       place(bkc, j, pick(fkc, j));
     } else if (tq != h) {
-      const DRec b = (tq - 1u >= pick(lv, j))
-                         ? s_win[j][(tq - 1u) % WB][tx]
-                         : ((const DRec *)(blk + pick(doff, j)))[(tq - 1u) & pick(dmask, j)];
+      DRec b;
+      if (tq - 1u >= pick(lv, j))
+        b = s_win[j][(tq - 1u) % WB][tx];
+      else
+        b = ((const DRec *)(blk + pick(doff, j)))[(tq - 1u) & pick(dmask, j)];
       place(ba, j, b.a_ft);
       place(bkb, j, b.kb);
       place(bkc, j, b.kc);
@@ -505,8 +511,8 @@ sim_known_kernel(KArgs A) {
         dpop_front(j);
         done++;
       }
-      Mj[j] += (int64_t)(before - done) + (int64_t)fresh[j] * (l[j] + 1) -
-               (int64_t)done * ((int64_t)l[j] + lp[j]);
+      Mj[j] += (int32_t)(before - done) + (int32_t)fresh[j] * (l[j] + 1) -
+               (int32_t)done * (l[j] + lp[j]);
     }
     Mres = 0;
 #pragma unroll
@@ -533,8 +539,8 @@ sim_known_kernel(KArgs A) {
       dpop_back_dyn(jb);
       const uint32_t admb = WAIT ? rkc : rkb;
       const uint32_t now = WAIT ? pick(svc, jb) : bidx;
-      const int64_t stage = (int64_t)(now - admb) + 1;
-      const int64_t ch = (int64_t)pick(l, jb) + stage;
+      const int32_t stage = (int32_t)(now - admb) + 1;
+      const int32_t ch = pick(l, jb) + stage;
       place(Mj, jb, pick(Mj, jb) - ch);
       Mres -= ch;
       evicts++;
