@@ -1,19 +1,27 @@
-"""Build the HIP library (gfx950) in-tree: paper_2504_11320_amd/libwait_sim.so."""
+"""Build the HIP library (gfx950) in-tree: paper_2504_11320_amd/libwait_sim.so.
+
+Each source is compiled to an object in parallel, then the objects are
+linked into one shared library."""
 from __future__ import annotations
 
 import os
 import subprocess
 import sys
+import tempfile
+import time
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
-SRCS = [os.path.join(CSRC, f) for f in ("wait_sim_host.hip", "sim_known.hip", "sim_nested.hip")]
+SRC_NAMES = ("wait_sim_host.hip", "sim_known_wait.hip", "sim_known_fcfs.hip",
+             "sim_nested.hip")
+SRCS = [os.path.join(CSRC, f) for f in SRC_NAMES]
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libwait_sim.so")
 
 HIPCC_FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # identical IEEE operations on both sides of the parity tests
     "-ffp-contract=off", "-fno-fast-math",
     # no packed-FP32 instructions
@@ -29,13 +37,31 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build(verbose: bool = False) -> str:
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INC, "-I", CSRC, "-o", LIB + ".tmp"] + SRCS
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+def build(verbose: bool = False, defines=(), out: str = LIB) -> str:
+    """Compile every source for gfx950 and link `out` (default: the in-tree
+    library).  `defines` are extra -D options."""
+    dflags = [f"-D{d}" for d in defines]
+    with tempfile.TemporaryDirectory(prefix="wait_sim_build_") as tmp:
+        def compile_one(src: str):
+            obj = os.path.join(tmp, os.path.basename(src) + ".o")
+            cmd = [hipcc()] + HIPCC_FLAGS + dflags + ["-I", INC, "-I", CSRC, "-c", "-o", obj, src]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            t0 = time.perf_counter()
+            subprocess.run(cmd, check=True)
+            if verbose:
+                print(f"  {os.path.basename(src)}: {time.perf_counter() - t0:.1f} s", flush=True)
+            return obj
+
+        workers = max(1, min(len(SRCS), os.cpu_count() or 1))
+        with ThreadPoolExecutor(workers) as ex:
+            objs = list(ex.map(compile_one, SRCS))
+        cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", out + ".tmp"] + objs
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
 
 
 if __name__ == "__main__":

@@ -78,6 +78,7 @@ struct KArgs {
   int64_t horizon;
   int32_t resume;
   int32_t any_trace;   // some job of this launch replays a fixed arrival list
+  int32_t lanes;       // replicas per wavefront (lanes >= this are padding)
 };
 
 __device__ __forceinline__ int64_t slot_i(const KArgs &A, int s, int64_t r) {
@@ -254,7 +255,8 @@ __device__ __forceinline__ void place_if(T (&a)[MT], int j, bool c, T v) {
 }
 
 // Launchers, one per kernel family (defined next to their kernels).
-hipError_t launch_known(int policy, int max_m, const KArgs &A, hipStream_t s);
+hipError_t launch_known_wait(int max_m, const KArgs &A, hipStream_t s);
+hipError_t launch_known_fcfs(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s);
 
 }  // namespace wsim

@@ -1,5 +1,6 @@
-// sim_known.hip -- simulation kernel for WAIT and FCFS with known output
-// lengths (arXiv 2504.11320: Algorithm 1, Section 4.1).
+// sim_known_impl.h -- simulation kernel for WAIT and FCFS with known output
+// lengths (arXiv 2504.11320: Algorithm 1, Section 4.1).  Included by one
+// translation unit per policy (sim_known_wait.hip, sim_known_fcfs.hip).
 //
 // One lane per replica.  A replica's state is a handful of scalars (clock,
 // per-type next arrival, counters, areas) held in registers, plus ring
@@ -25,12 +26,17 @@
 // Arithmetic follows the model contract exactly (same IEEE operations in the
 // same order, no FMA contraction), so integer state is bit-identical to the
 // oracle's and floating sums agree to rounding.
+#pragma once
+
 #include "sim_common.h"
 
 namespace wsim {
 namespace {
 
-template <int MT, int POL, bool TRACE>
+// MT: type slots (>= m); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
+// launch replays an arrival list; LN: replicas per wavefront (lanes LN..63
+// are padding), which sizes the per-lane LDS arrays.
+template <int MT, int POL, bool TRACE, int LN>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 sim_known_kernel(KArgs A) {
   constexpr bool WAIT = POL == WS_WAIT;
@@ -41,13 +47,13 @@ sim_known_kernel(KArgs A) {
   constexpr int GU = GR / 2;            // gaps added per refill
   constexpr uint32_t kLow = GU / 2;     // a lane below this triggers a refill
   __shared__ double s_edges[WS_MAX_HIST_EDGES];
-  __shared__ double s_gap[MT][GR][64];
-  __shared__ uint64_t s_seed[64];
-  __shared__ uint32_t s_rid[64], s_req_lane[64], s_req_k[64];
+  __shared__ double s_gap[MT][GR][LN];
+  __shared__ uint64_t s_seed[LN];
+  __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   // The last WB records pushed on each resident deque are also kept in LDS,
   // so LIFO evictions (which pop the back) rarely read HBM.
   constexpr int WB = MT <= 4 ? 8 : 2;
-  __shared__ DRec s_win[MT][WB][64];
+  __shared__ DRec s_win[MT][WB][LN];
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   // replica of this lane, or -1 for padding (padding only ends a job's last
@@ -72,7 +78,7 @@ sim_known_kernel(KArgs A) {
     __syncthreads();
   }
   const double *edges = s_edges;
-  if (r32 < 0) return;  // padding lane
+  if (r32 < 0 || tx >= LN) return;  // padding lane
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
   const uint32_t rid = ((const uint32_t *)(A.ws + A.off_rid))[r];
   s_seed[tx] = seed;
@@ -595,12 +601,22 @@ sim_known_kernel(KArgs A) {
 
 template <int MT, int POL>
 hipError_t launch_mt(const KArgs &A, hipStream_t s) {
-  const int threads = 64;
-  const int blocks = (A.n_list + threads - 1) / threads;
-  if (A.any_trace)
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, true>), dim3(blocks), dim3(threads), 0, s, A);
-  else
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false>), dim3(blocks), dim3(threads), 0, s, A);
+  const int blocks = (A.n_list + 63) / 64;
+  const dim3 g(blocks), b(64);
+  if (A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
+    if (A.lanes != 64) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64>), g, b, 0, s, A);
+  } else if (A.lanes == 64) {
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64>), g, b, 0, s, A);
+  } else if (A.lanes == 32) {
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 32>), g, b, 0, s, A);
+  } else if (A.lanes == 16) {
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 16>), g, b, 0, s, A);
+  } else if (A.lanes == 8) {
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 8>), g, b, 0, s, A);
+  } else {
+    return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -614,10 +630,4 @@ hipError_t launch_pol(int max_m, const KArgs &A, hipStream_t s) {
 }
 
 }  // namespace
-
-hipError_t launch_known(int policy, int max_m, const KArgs &A, hipStream_t s) {
-  if (policy == WS_WAIT) return launch_pol<WS_WAIT>(max_m, A, s);
-  return launch_pol<WS_FCFS>(max_m, A, s);
-}
-
 }  // namespace wsim

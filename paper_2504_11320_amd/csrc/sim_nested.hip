@@ -36,17 +36,19 @@ struct SlotMeta {
   uint32_t suml;  // sum of their prompt lengths
 };
 
-template <int MT, int LT>
+// MT: type slots (>= m); LT: segment slots (>= L); LN: replicas per
+// wavefront (lanes LN..63 are padding), which sizes the per-lane LDS columns.
+template <int MT, int LT, int LN>
 __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
-  __shared__ double s_tnext[MT][64];
-  __shared__ uint32_t s_k[MT][64];
-  __shared__ int32_t s_Ln[MT][64];
-  __shared__ uint32_t s_svc[LT][64], s_I[LT][64], s_vh[LT][64], s_vt[LT][64];
-  __shared__ int64_t s_M[LT][64], s_B[LT][64];
+  __shared__ double s_tnext[MT][LN];
+  __shared__ uint32_t s_k[MT][LN];
+  __shared__ int32_t s_Ln[MT][LN];
+  __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
+  __shared__ int64_t s_M[LT][LN], s_B[LT][LN];
 
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tx;
-  if (gid >= A.n_list) return;  // lanes use only their own LDS column
+  if (gid >= A.n_list || tx >= LN) return;  // lanes use only their own LDS column
   const int32_t r32 = ((const int32_t *)(A.ws + A.off_list))[gid];
   if (r32 < 0) return;  // padding lane
   const int64_t r = r32;
@@ -593,9 +595,17 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
 template <int MT, int LT>
 hipError_t launch_ml(const KArgs &A, hipStream_t s) {
-  const int threads = 64;
-  const int blocks = (A.n_list + threads - 1) / threads;
-  hipLaunchKernelGGL((sim_nested_kernel<MT, LT>), dim3(blocks), dim3(threads), 0, s, A);
+  const dim3 g((A.n_list + 63) / 64), b(64);
+  if (A.lanes == 64)
+    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 64>), g, b, 0, s, A);
+  else if (A.lanes == 32)
+    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 32>), g, b, 0, s, A);
+  else if (A.lanes == 16)
+    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 16>), g, b, 0, s, A);
+  else if (A.lanes == 8)
+    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 8>), g, b, 0, s, A);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -55,6 +55,16 @@ int fail(int code, const std::string &msg) {
   return code;
 }
 
+// Replicas per 64-lane wavefront.  A replica is a serial chain of events, so
+// a wavefront's time per batch is set by latency, not by how many of its lanes
+// are busy: when a launch has few replicas they are spread over more
+// wavefronts (64, 32, 16 or 8 per wavefront) until the launch has at least
+// kTargetWaves wavefronts or reaches 8 per wavefront.
+#ifndef WS_TARGET_WAVES
+#define WS_TARGET_WAVES 1024
+#endif
+constexpr int64_t kTargetWaves = WS_TARGET_WAVES;
+
 int ceil_log2(uint64_t x) {
   int k = 0;
   while ((1ull << k) < x) ++k;
@@ -77,6 +87,7 @@ struct Layout {
            off_rings = 0, total = 0;
   std::vector<JobHost> jobs;
   int32_t list_count[3] = {0, 0, 0};
+  int32_t lanes[3] = {64, 64, 64};  // replicas per wavefront, per launch
   uint64_t list_off[3] = {0, 0, 0};
   int32_t max_m[3] = {0, 0, 0};
   int32_t max_seg = 0;
@@ -276,10 +287,27 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     R += jobs[i].n;
     hmax = std::max(hmax, jobs[i].cfg->n_hist + 1);
     const int pk = jobs[i].pol->kind;
-    // each job starts a new wavefront: its constants are wavefront-uniform
-    Lo.list_count[pk] += (jobs[i].n + 63) / 64 * 64;
     Lo.max_m[pk] = std::max(Lo.max_m[pk], jobs[i].cfg->m);
     if (pk == WS_NESTED_WAIT) Lo.max_seg = std::max(Lo.max_seg, jobs[i].pol->L);
+  }
+  for (int pk = 0; pk < 3; ++pk) {
+    auto waves = [&](int lanes) {
+      // each job starts a new wavefront: its constants are wavefront-uniform
+      int64_t w = 0;
+      for (int i = 0; i < n_jobs; ++i)
+        if (jobs[i].pol->kind == pk) w += (jobs[i].n + lanes - 1) / lanes;
+      return w;
+    };
+    bool any_trace = false;
+    for (int i = 0; i < n_jobs; ++i)
+      any_trace |= jobs[i].pol->kind == pk && jobs[i].cfg->n_trace > 0;
+    int lanes = 64;
+    if (!any_trace)  // arrival-list replays keep 64 per wavefront
+      while (lanes > 8 && waves(lanes) < kTargetWaves) lanes /= 2;
+    Lo.lanes[pk] = lanes;
+    const int64_t count = waves(lanes) * 64;
+    if (count > INT32_MAX) return fail(WS_EINVAL, "too many replicas");
+    Lo.list_count[pk] = (int32_t)count;
   }
   if (R < 1) return fail(WS_EINVAL, "no replicas");
   if (R > (int64_t(1) << 30)) return fail(WS_EINVAL, "too many replicas");
@@ -410,14 +438,17 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
   std::vector<int32_t> lists[3];
   for (int i = 0; i < n_jobs; ++i) {
     const ws_job &jb = jobs[i];
+    std::vector<int32_t> &list = lists[jb.pol->kind];
     for (int x = 0; x < jb.n; ++x, ++r) {
       std::memcpy(img.data() + Lo.off_seed + 8 * r, &jb.streams[x].seed, 8);
       std::memcpy(img.data() + Lo.off_rid + 4 * r, &jb.streams[x].replica_id, 4);
       const uint32_t ji = (uint32_t)i;
       std::memcpy(img.data() + Lo.off_job_of + 4 * r, &ji, 4);
-      lists[jb.pol->kind].push_back((int32_t)r);
+      list.push_back((int32_t)r);
+      if (list.size() % 64 == (size_t)Lo.lanes[jb.pol->kind])
+        while (list.size() % 64 != 0) list.push_back(-1);
     }
-    while (lists[jb.pol->kind].size() % 64 != 0) lists[jb.pol->kind].push_back(-1);
+    while (list.size() % 64 != 0) list.push_back(-1);
     const ws_config &c = *jb.cfg;
     const JobDev &d = Lo.jobs[i].d;
     if (c.n_hist > 0) std::memcpy(img.data() + d.off_edges, c.hist_edges, 8ull * c.n_hist);
@@ -458,6 +489,7 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     KArgs B = A;
     B.off_list = Lo.list_off[pk];
     B.n_list = Lo.list_count[pk];
+    B.lanes = Lo.lanes[pk];
     B.any_trace = 0;
     for (int i = 0; i < n_jobs; ++i)
       if (jobs[i].pol->kind == pk && jobs[i].cfg->n_trace > 0) B.any_trace = 1;
@@ -465,7 +497,8 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     if (pk == WS_NESTED_WAIT)
       e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, s);
     else
-      e = launch_known(pk, Lo.max_m[pk], B, s);
+      e = pk == WS_WAIT ? launch_known_wait(Lo.max_m[pk], B, s)
+                        : launch_known_fcfs(Lo.max_m[pk], B, s);
     if (e != hipSuccess) return fail(WS_EDEVICE, std::string("launch: ") + hipGetErrorString(e));
   }
   const int tb = 256;
