@@ -15,7 +15,7 @@ against the ALU peak with an explicit operation model (lane-operations the
 method needs per arrival, batch, completion, eviction and idle wait; see the
 design notes), using the event counts the kernel itself returns.  The
 cpu_baseline object times the CPU oracle on a bounded sample of the same
-workload (2 rates x 64 replicas x the full horizon) on the host's cores.
+workload (2 rates x 256 replicas x the full horizon) on the host's cores.
 """
 from __future__ import annotations
 
@@ -39,8 +39,12 @@ CUS, LANES_PER_CU_CLK, CLOCK_HZ = 256, 64, 2.4e9
 ALU_PEAK = CUS * LANES_PER_CU_CLK * CLOCK_HZ          # 3.93e13 lane-ops/s
 HBM_PEAK = 8.0e12                                     # bytes/s
 
-KERNEL_SRC = os.path.join(ROOT, "paper_2504_11320_amd", "csrc", "sim_known.hip")
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_kernel_wait_config2_hbm.md")
+CSRC = os.path.join(ROOT, "paper_2504_11320_amd", "csrc")
+# the sources that define the benchmark's kernel (hashed to tie the committed
+# HBM counter summary to the kernel it was measured on)
+KERNEL_SRCS = [os.path.join(CSRC, f)
+               for f in ("sim_known_impl.h", "sim_known_wait.hip", "sim_common.h")]
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_wait_3type_32x1024x1e5_hbm.md")
 
 
 def op_model(m: int) -> dict:
@@ -75,8 +79,11 @@ def algorithmic_bytes(res: dict) -> float:
 
 
 def source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_from_profile():
@@ -115,7 +122,7 @@ def main() -> int:
     ap.add_argument("--horizon", type=int, default=100000)
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-replicas", type=int, default=64)
+    ap.add_argument("--cpu-replicas", type=int, default=256)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (used to "
                          "scale the HBM byte counters)")
@@ -134,8 +141,8 @@ def main() -> int:
 
     if args.gpus != 1:
         print(f"bench.py: this simulator runs on one GPU; --gpus {args.gpus} is not "
-              f"supported (replicas shard across GPUs with no communication, but this "
-              f"build measures a single MI355X)", file=sys.stderr)
+              f"supported (replicas shard across GPUs with no communication; this "
+              f"benchmark measures a single MI355X)", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -183,7 +190,13 @@ def main() -> int:
                 "traffic": traffic,
                 "algorithmic_ops_per_replica_iteration": ops / rep_its,
                 "algorithmic_bytes_per_launch": algorithmic_bytes(res),
-                "kernel": "sim_known_kernel<4, WAIT>"}
+                # the HBM side of the same launch: algorithmic record bytes and
+                # the measured DRAM bytes (traffic), each per second over the
+                # 8 TB/s peak
+                "hbm_algorithmic_frac": algorithmic_bytes(res) / (ms_step / 1e3) / HBM_PEAK,
+                "hbm_measured_frac": (traffic / (ms_step / 1e3) / HBM_PEAK
+                                      if traffic is not None else None),
+                "kernel": f"sim_known_kernel (WAIT, {m} types)"}
 
     out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
