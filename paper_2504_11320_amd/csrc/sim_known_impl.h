@@ -15,11 +15,15 @@
 // matrix: admissions push at the back, completions pop at the front, LIFO
 // evictions pop at the back, and each step costs O(events), not O(stages).
 //
-// Latency: the hot ends of every ring (queue head, deque front and back) are
-// cached in registers, so a pop needs no load; the refill of the cache is
-// issued at the pop and consumed later.  First tokens are counted per cohort
-// (how many prompts of the newest cohort have not produced one yet), so
-// resident records are never rewritten.  All lanes of a wavefront belong to
+// Latency: the hot ends of every ring are cached in registers.  The queue
+// head and the first two deque records are prefetched one pop ahead with
+// unconditional loads (a slot past the tail reads a stale value that a later
+// push replaces through a separate register and a bit mask), and the loads
+// of one iteration are waited for once, at the start of the next, so a pop
+// consumes a value loaded long before; the deque back is served from a
+// window of the most recent pushes kept in LDS.  First tokens are counted per
+// cohort (how many prompts of the newest cohort have not produced one yet),
+// so resident records are never rewritten.  All lanes of a wavefront belong to
 // one job (the replica lists are padded per job), so the job's constants are
 // wavefront-uniform and live in scalar registers.
 //
@@ -114,12 +118,21 @@ sim_known_kernel(KArgs A) {
   uint32_t gend[MT];  // gaps of arrivals kk+1 .. gend-1 are in the ring
   uint32_t lv[MT];    // deque records lv .. dt-1 are also in the LDS window
   int32_t Mj[MT];  // resident memory per type (< 2C <= 2^31)
-  double qhead[MT];      // WAIT: record at each queue's head
-  QRec qhead0;           // FCFS: record at the shared queue's head
-  // cached deque ends, one array per field (arrays of structs would be
-  // indexed as memory by the compiler)
-  double fa[MT], ba[MT];
-  uint32_t fkb[MT], fkc[MT], bkb[MT], bkc[MT];
+  // Queue heads.  WAIT: the head of queue j is qpu[j] if bit j of qsrc is
+  // set (pushed into an empty queue), else qld[j] (loaded when the previous
+  // head left).  FCFS: the same for the shared queue with q0pu / q0ld.
+  double qld[MT], qpu[MT];
+  uint32_t qsrc = 0;
+  QRec q0ld, q0pu;
+  bool q0src = false;
+  // Deque fronts: the first record (fa = arrival, fadm = admission service
+  // under WAIT, admission batch under FCFS) and the second, which is s1pa /
+  // s1padm if bit j of s1src is set, else s1a / s1adm (prefetched).  The
+  // back record (ba, bkb, bkc) is kept for the LIFO repair.  One array per
+  // field: arrays of structs would be indexed as memory by the compiler.
+  double fa[MT], s1a[MT], s1pa[MT], ba[MT];
+  uint32_t fadm[MT], s1adm[MT], s1padm[MT], bkb[MT], bkc[MT];
+  uint32_t s1src = 0;
 
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
   int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, Mres, tridx;
@@ -183,19 +196,21 @@ sim_known_kernel(KArgs A) {
   for (int j = 0; j < MT; ++j) {
     gend[j] = kk[j] + 1u;
     lv[j] = dt[j];
-    if (WAIT && qt[j] != qh[j]) qhead[j] = qring(j)[qh[j] & qmask];
-    if (dt[j] != dh[j]) {
-      const DRec f = dring(j)[dh[j] & dmask[j]];
-      const DRec b = dring(j)[(dt[j] - 1u) & dmask[j]];
-      fa[j] = f.a_ft;
-      fkb[j] = f.kb;
-      fkc[j] = f.kc;
-      ba[j] = b.a_ft;
-      bkb[j] = b.kb;
-      bkc[j] = b.kc;
-    }
+    // unconditional loads: a slot past the tail holds a stale record that is
+    // never used (the masks keep every index inside its ring)
+    if (WAIT) qld[j] = qring(j)[qh[j] & qmask];
+    const DRec f = dring(j)[dh[j] & dmask[j]];
+    const DRec f2 = dring(j)[(dh[j] + 1u) & dmask[j]];
+    const DRec b = dring(j)[(dt[j] - 1u) & dmask[j]];
+    fa[j] = f.a_ft;
+    fadm[j] = WAIT ? f.kc : f.kb;
+    s1a[j] = f2.a_ft;
+    s1adm[j] = WAIT ? f2.kc : f2.kb;
+    ba[j] = b.a_ft;
+    bkb[j] = b.kb;
+    bkc[j] = b.kc;
   }
-  if (!WAIT && qt[0] != qh[0]) qhead0 = qring0()[qh[0] & qmask];
+  if (!WAIT) q0ld = qring0()[qh[0] & qmask];
 
   // ---- ring operations ------------------------------------------------------
   // Operations with a compile-time type index j (inside unrolled loops).
@@ -207,11 +222,13 @@ sim_known_kernel(KArgs A) {
     dring(j)[dt[j] & dmask[j]] = rec;
     s_win[j][dt[j] % WB][tx] = rec;
     if (dt[j] + 1u > (uint32_t)WB && dt[j] + 1u - WB > lv[j]) lv[j] = dt[j] + 1u - WB;
-    if (dt[j] == dh[j]) {
-      fa[j] = a_ft;
-      fkb[j] = kb;
-      fkc[j] = kc;
-    }
+    const uint32_t adm = WAIT ? kc : kb;
+    const bool empty = dt[j] == dh[j], second = dt[j] == dh[j] + 1u;
+    fa[j] = empty ? a_ft : fa[j];
+    fadm[j] = empty ? adm : fadm[j];
+    s1pa[j] = second ? a_ft : s1pa[j];
+    s1padm[j] = second ? adm : s1padm[j];
+    s1src |= (second ? 1u : 0u) << j;
     ba[j] = a_ft;
     bkb[j] = kb;
     bkc[j] = kc;
@@ -219,44 +236,42 @@ sim_known_kernel(KArgs A) {
   };
   auto dpop_front = [&](int j) __attribute__((always_inline)) {
     dh[j]++;
-    if (dh[j] + 1u == dt[j]) {
-      fa[j] = ba[j];
-      fkb[j] = bkb[j];
-      fkc[j] = bkc[j];
-    } else if (dh[j] != dt[j]) {
-      DRec f;
-      if (dh[j] >= lv[j])
-        f = s_win[j][dh[j] % WB][tx];
-      else
-        f = dring(j)[dh[j] & dmask[j]];
-      fa[j] = f.a_ft;
-      fkb[j] = f.kb;
-      fkc[j] = f.kc;
-    }
+    const bool pushed = (s1src >> j) & 1u;
+    fa[j] = pushed ? s1pa[j] : s1a[j];
+    fadm[j] = pushed ? s1padm[j] : s1adm[j];
+    s1src &= ~(1u << j);
+    const DRec n = dring(j)[(dh[j] + 1u) & dmask[j]];  // next second record
+    s1a[j] = n.a_ft;
+    s1adm[j] = WAIT ? n.kc : n.kb;
   };
   // Operations with a lane-dependent type index: every per-type array is
   // read and written through selects (pick / place).
   auto push_wait_dyn = [&](int j, double a_ft) __attribute__((always_inline)) {
+    // (flag and head updates are branch-free: stores to different variables
+    // in the two arms of a branch get merged into one store through a
+    // selected address, which would move both variables to scratch memory)
     const uint32_t h = pick(qh, j), tq = pick(qt, j);
-    if (tq - h >= rec_cap) {
-      flags |= kFlagCap;  // the replica stops at its next decision
-    } else {
-      ((double *)(blk + pick(qoff, j)))[tq & qmask] = a_ft;
-      place_if(qhead, j, tq == h, a_ft);
-    }
+    const bool full = tq - h >= rec_cap;  // the replica stops at its next decision
+    flags |= full ? kFlagCap : 0u;
+    const bool first = !full && tq == h;
+    place_if(qpu, j, first, a_ft);
+    qsrc |= (first ? 1u : 0u) << j;
+    if (!full) ((double *)(blk + pick(qoff, j)))[tq & qmask] = a_ft;
     place(qt, j, tq + 1u);
   };
   auto push_fcfs = [&](double a_ft, int32_t j, int32_t L) __attribute__((always_inline)) {
-    if (qt[0] - qh[0] >= rec_cap) {
-      flags |= kFlagCap;
-    } else {
-      QRec rec;
-      rec.a_ft = a_ft;
-      rec.j = j;
-      rec.L = L;
-      qring0()[qt[0] & qmask] = rec;
-      if (qt[0] == qh[0]) qhead0 = rec;
-    }
+    const bool full = qt[0] - qh[0] >= rec_cap;
+    flags |= full ? kFlagCap : 0u;
+    const bool first = !full && qt[0] == qh[0];
+    QRec rec;
+    rec.a_ft = a_ft;
+    rec.j = j;
+    rec.L = L;
+    q0pu.a_ft = first ? a_ft : q0pu.a_ft;
+    q0pu.j = first ? j : q0pu.j;
+    q0pu.L = first ? L : q0pu.L;
+    q0src = q0src || first;
+    if (!full) qring0()[qt[0] & qmask] = rec;
     qt[0]++;
   };
   auto dpush_dyn = [&](int j, double a_ft, uint32_t kb, uint32_t kc) __attribute__((always_inline)) {
@@ -269,10 +284,14 @@ sim_known_kernel(KArgs A) {
     s_win[j][tq % WB][tx] = rec;
     const uint32_t lvj = pick(lv, j);
     place_if(lv, j, tq + 1u > (uint32_t)WB && tq + 1u - WB > lvj, tq + 1u - WB);
-    const bool empty = tq == pick(dh, j);
+    const uint32_t h = pick(dh, j);
+    const uint32_t adm = WAIT ? kc : kb;
+    const bool empty = tq == h, second = tq == h + 1u;
     place_if(fa, j, empty, a_ft);
-    place_if(fkb, j, empty, kb);
-    place_if(fkc, j, empty, kc);
+    place_if(fadm, j, empty, adm);
+    place_if(s1pa, j, second, a_ft);
+    place_if(s1padm, j, second, adm);
+    s1src |= (second ? 1u : 0u) << j;
     place(ba, j, a_ft);
     place(bkb, j, kb);
     place(bkc, j, kc);
@@ -281,11 +300,7 @@ sim_known_kernel(KArgs A) {
   auto dpop_back_dyn = [&](int j) __attribute__((always_inline)) {
     const uint32_t tq = pick(dt, j) - 1u, h = pick(dh, j);
     place(dt, j, tq);
-    if (tq - 1u == h) {
-      place(ba, j, pick(fa, j));
-      place(bkb, j, pick(fkb, j));
-      place(bkc, j, pick(fkc, j));
-    } else if (tq != h) {
+    if (tq != h) {
       DRec b;
       if (tq - 1u >= pick(lv, j))
         b = s_win[j][(tq - 1u) % WB][tx];
@@ -385,6 +400,21 @@ sim_known_kernel(KArgs A) {
       }
     }
 
+    // The prefetched ring records become usable here, with one wait for the
+    // loads issued during the previous iteration (their uses below need no
+    // further wait).
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      if (WAIT) qld[j] = opaque(qld[j]);
+      s1a[j] = opaque(s1a[j]);
+      s1adm[j] = opaque(s1adm[j]);
+    }
+    if (!WAIT) {
+      q0ld.a_ft = opaque(q0ld.a_ft);
+      q0ld.j = opaque(q0ld.j);
+      q0ld.L = opaque(q0ld.L);
+    }
+
     // ---- decision: form a batch or wait for the next arrival ------------
     uint32_t elig = 0;
     for (;;) {
@@ -440,9 +470,10 @@ sim_known_kernel(KArgs A) {
         if (!(elig & (1u << j))) continue;
         const uint32_t c = svc[j] + 1u;
         for (int x = 0; x < nth[j]; ++x) {
-          const double a_ft = qhead[j];
+          const double a_ft = ((qsrc >> j) & 1u) ? qpu[j] : qld[j];
+          qsrc &= ~(1u << j);
           qh[j]++;
-          if (qt[j] != qh[j]) qhead[j] = qring(j)[qh[j] & qmask];
+          qld[j] = qring(j)[qh[j] & qmask];  // the next head, used at a later admission
           dpush(j, a_ft, bidx, c);
           pendnew[j] += has_ft(a_ft) ? 0u : 1u;
         }
@@ -454,12 +485,13 @@ sim_known_kernel(KArgs A) {
       tokens = Mres;
       uint32_t p = 0;
       while (qt[0] != qh[0]) {
-        const QRec head = qhead0;
+        const QRec head = q0src ? q0pu : q0ld;
         const int hj = head.j;
         const int64_t hl = pick(l, hj);
         if (Mres + prefill_l + hl > cap_adm) break;
         qh[0]++;
-        if (qt[0] != qh[0]) qhead0 = qring0()[qh[0] & qmask];
+        q0src = false;
+        q0ld = qring0()[qh[0] & qmask];
         dpush_dyn(hj, head.a_ft, bidx, p++);
         place(fresh, hj, pick(fresh, hj) + 1u);
         place(pendnew, hj, pick(pendnew, hj) + (has_ft(head.a_ft) ? 0u : 1u));
@@ -505,8 +537,7 @@ sim_known_kernel(KArgs A) {
       uint32_t done = 0;
       // completions: processed at stage l'_j (fresh records never qualify)
       while (done < before) {
-        const uint32_t admb = WAIT ? fkc[j] : fkb[j];
-        if (admb + (uint32_t)lp[j] != now) break;
+        if (fadm[j] + (uint32_t)lp[j] != now) break;
         const double lat = t_end - arrival_of(fa[j]);
         lat_sum += lat;
         __hip_atomic_fetch_add(&hist[hist_bin(edges, n_hist, lat)], 1u, __ATOMIC_RELAXED,
