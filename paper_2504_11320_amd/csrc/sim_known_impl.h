@@ -139,6 +139,8 @@ sim_known_kernel(KArgs A) {
   int32_t N, U;  // requests in system, and those without a first token
   uint32_t flags;
 
+  uint32_t bidx_cur = 0;  // index of the batch being formed
+
   auto qring = [&](int j) __attribute__((always_inline)) { return (double *)(blk + qoff[j]); };
   auto qring0 = [&]() __attribute__((always_inline)) { return (QRec *)(blk + qoff[0]); };
   auto dring = [&](int j) __attribute__((always_inline)) { return (DRec *)(blk + doff[j]); };
@@ -297,18 +299,45 @@ sim_known_kernel(KArgs A) {
     place(bkc, j, kc);
     place(dt, j, tq + 1u);
   };
-  auto dpop_back_dyn = [&](int j) __attribute__((always_inline)) {
-    const uint32_t tq = pick(dt, j) - 1u, h = pick(dh, j);
-    place(dt, j, tq);
-    if (tq != h) {
+  // LIFO eviction of the back record of deque j (static j): it returns to
+  // the tail of its external queue with its first-token flag.
+  auto evict = [&](int j) __attribute__((always_inline)) {
+    const double ra = ba[j];
+    const uint32_t rkb = bkb[j], rkc = bkc[j];
+    const uint32_t tq = dt[j] - 1u;
+    dt[j] = tq;
+    if (tq != dh[j]) {  // the new back record
       DRec b;
-      if (tq - 1u >= pick(lv, j))
+      if (tq - 1u >= lv[j])
         b = s_win[j][(tq - 1u) % WB][tx];
       else
-        b = ((const DRec *)(blk + pick(doff, j)))[(tq - 1u) & pick(dmask, j)];
-      place(ba, j, b.a_ft);
-      place(bkb, j, b.kb);
-      place(bkc, j, b.kc);
+        b = dring(j)[(tq - 1u) & dmask[j]];
+      ba[j] = b.a_ft;
+      bkb[j] = b.kb;
+      bkc[j] = b.kc;
+    }
+    const uint32_t admb = WAIT ? rkc : rkb;
+    const uint32_t now = WAIT ? svc[j] : bidx_cur;
+    const int32_t stage = (int32_t)(now - admb) + 1;
+    const int32_t ch = l[j] + stage;
+    Mj[j] -= ch;
+    Mres -= ch;
+    evicts++;
+    etok += stage - 1;
+    const bool ft = has_ft(ra);
+    pend[j] -= (stage == 1 && !ft) ? 1u : 0u;
+    const double a_ft = (ft || stage >= 2) ? with_ft(ra) : ra;
+    if (WAIT) {
+      const uint32_t h = qh[j], tq2 = qt[j];
+      const bool full = tq2 - h >= rec_cap;
+      flags |= full ? kFlagCap : 0u;
+      const bool first = !full && tq2 == h;
+      qpu[j] = first ? a_ft : qpu[j];
+      qsrc |= (first ? 1u : 0u) << j;
+      if (!full) qring(j)[tq2 & qmask] = a_ft;
+      qt[j] = tq2 + 1u;
+    } else {
+      push_fcfs(a_ft, j, lp[j]);
     }
   };
 
@@ -461,6 +490,7 @@ sim_known_kernel(KArgs A) {
 
     // ---- launch: admissions and batch tokens --------------------------
     const uint32_t bidx = (uint32_t)batches;
+    bidx_cur = bidx;
     int64_t tokens = 0, prefill_l = 0;
 #pragma unroll
     for (int j = 0; j < MT; ++j) fresh[j] = pendnew[j] = 0;
@@ -571,24 +601,12 @@ sim_known_kernel(KArgs A) {
         }
       }
       if (jb < 0) break;
-      const double ra = pick(ba, jb);
-      const uint32_t rkb = pick(bkb, jb), rkc = pick(bkc, jb);
-      dpop_back_dyn(jb);
-      const uint32_t admb = WAIT ? rkc : rkb;
-      const uint32_t now = WAIT ? pick(svc, jb) : bidx;
-      const int32_t stage = (int32_t)(now - admb) + 1;
-      const int32_t ch = pick(l, jb) + stage;
-      place(Mj, jb, pick(Mj, jb) - ch);
-      Mres -= ch;
-      evicts++;
-      etok += stage - 1;
-      const bool ft = has_ft(ra);
-      if (stage == 1 && !ft) place(pend, jb, pick(pend, jb) - 1u);
-      const double a_ft = (ft || stage >= 2) ? with_ft(ra) : ra;
-      if (WAIT)
-        push_wait_dyn(jb, a_ft);
-      else
-        push_fcfs(a_ft, jb, pick(lp, jb));
+      // one unrolled body per type, each with static register indices; the
+      // lanes of a wavefront mostly evict the same type, so usually one body
+      // runs
+#pragma unroll
+      for (int j = 0; j < MT; ++j)
+        if (jb == j) evict(j);
     }
     batches++;
     btok += tokens;
