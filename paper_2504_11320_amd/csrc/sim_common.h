@@ -189,6 +189,84 @@ __device__ __forceinline__ int hist_bin(const double *edges, int n, double lat) 
   return pos;
 }
 
+// Histogram bin through a bucket index: the non-negative edges are bucketed
+// by the top bits of their IEEE patterns (which order non-negative doubles
+// like their values), so a latency (always >= 0) finds its bin with one table
+// read and a few comparisons instead of a chain of dependent searches.  The
+// result equals hist_bin: the number of edges <= lat.
+constexpr int kHistTab = 512;  // bucket-table entries
+
+struct HistIdx {
+  int32_t shift;  // bucket = (bits >> shift) - kmin, clamped to [0, K)
+  int32_t kmin;
+  int32_t K;
+  int32_t steps;  // most edges in one bucket
+};
+
+__device__ __forceinline__ uint64_t dbits(double x) {
+  return (uint64_t)__double_as_longlong(x);
+}
+
+// Block-cooperative (every thread of the block calls it): E[0..n-1] are the
+// edges staged in LDS with E[n] = +infinity; fills the table T (kHistTab
+// bytes of LDS) and returns the block-uniform index parameters.
+__device__ __forceinline__ HistIdx hist_index_build(const double *E, int n, uint8_t *T,
+                                                    int *s_steps) {
+  int p0 = 0;  // negative edges (a prefix) are below every latency
+  while (p0 < n && __builtin_signbit(E[p0])) ++p0;
+  HistIdx H;
+  if (p0 == n) {
+    H.shift = 63;
+    H.kmin = 0;
+    H.K = 1;
+  } else {
+    const uint64_t b0 = dbits(E[p0]), b1 = dbits(E[n - 1]);
+    int s = 44;
+    while ((b1 >> s) - (b0 >> s) >= (uint64_t)kHistTab) ++s;
+    H.shift = s;
+    H.kmin = (int32_t)(b0 >> s);
+    H.K = (int32_t)((b1 >> s) - (b0 >> s)) + 1;
+  }
+  for (int k = threadIdx.x; k < H.K; k += blockDim.x) {
+    // edges whose bucket is below k: the first edge at or above the
+    // smallest pattern of bucket k
+    const uint64_t lower = (uint64_t)(H.kmin + k) << H.shift;
+    int lo = p0, hi = n;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (dbits(E[mid]) < lower)
+        lo = mid + 1;
+      else
+        hi = mid;
+    }
+    T[k] = (uint8_t)(p0 == n ? n : lo);
+  }
+  if (threadIdx.x == 0) *s_steps = 0;
+  __syncthreads();
+  int mx = 0;
+  for (int k = threadIdx.x; k < H.K; k += blockDim.x) {
+    const int next = k + 1 < H.K ? (int)T[k + 1] : n;
+    mx = max(mx, next - (int)T[k]);
+  }
+  atomicMax(s_steps, mx);
+  __syncthreads();
+  H.steps = *s_steps;
+  H.shift = __builtin_amdgcn_readfirstlane(H.shift);
+  H.kmin = __builtin_amdgcn_readfirstlane(H.kmin);
+  H.K = __builtin_amdgcn_readfirstlane(H.K);
+  H.steps = __builtin_amdgcn_readfirstlane(H.steps);
+  return H;
+}
+
+__device__ __forceinline__ int hist_bin_idx(const double *E, const uint8_t *T, const HistIdx &H,
+                                            double lat) {
+  const int64_t key = (int64_t)(dbits(lat) >> H.shift) - H.kmin;
+  const int kc = key < 0 ? 0 : (key >= H.K ? H.K - 1 : (int)key);
+  int pos = T[kc];
+  for (int s = 0; s < H.steps; ++s) pos += E[pos] <= lat ? 1 : 0;
+  return pos;
+}
+
 // ------------------------------------------------------------- records --
 
 // The first-token flag travels in the sign bit of the arrival time.

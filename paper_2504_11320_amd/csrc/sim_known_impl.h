@@ -50,13 +50,15 @@ sim_known_kernel(KArgs A) {
   constexpr int GR = MT <= 4 ? 16 : 4;  // ring size per (type, lane)
   constexpr int GU = GR / 2;            // gaps added per refill
   constexpr uint32_t kLow = GU / 2;     // a lane below this triggers a refill
-  __shared__ double s_edges[WS_MAX_HIST_EDGES];
+  __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
+  __shared__ uint8_t s_htab[kHistTab];
+  __shared__ int s_hsteps;
   __shared__ double s_gap[MT][GR][LN];
   __shared__ uint64_t s_seed[LN];
   __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   // The last WB records pushed on each resident deque are also kept in LDS,
   // so LIFO evictions (which pop the back) rarely read HBM.
-  constexpr int WB = MT <= 4 ? 8 : 2;
+  constexpr int WB = MT <= 4 ? 16 : 2;
   __shared__ DRec s_win[MT][WB][LN];
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -75,12 +77,15 @@ sim_known_kernel(KArgs A) {
   const int32_t cap_adm = (int32_t)(J->C - J->reserve_tok);
   const int n_hist = J->n_hist;
   // the latency histogram's edges, searched at every completion, staged in
-  // LDS by all lanes of the block (one wavefront, one job)
+  // LDS with their bucket index by all lanes of the block (one wavefront,
+  // one job)
   {
     const double *edges_g = (const double *)(A.ws + J->off_edges);
-    for (int b = threadIdx.x; b < n_hist; b += 64) s_edges[b] = edges_g[b];
+    for (int b = threadIdx.x; b <= n_hist; b += 64)
+      s_edges[b] = b < n_hist ? edges_g[b] : INFINITY;
     __syncthreads();
   }
+  const HistIdx hidx = hist_index_build(s_edges, n_hist, s_htab, &s_hsteps);
   const double *edges = s_edges;
   if (r32 < 0 || tx >= LN) return;  // padding lane
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
@@ -116,7 +121,7 @@ sim_known_kernel(KArgs A) {
   double tnext[MT];
   uint32_t kk[MT], qh[MT], qt[MT], dh[MT], dt[MT], svc[MT], pend[MT];
   uint32_t gend[MT];  // gaps of arrivals kk+1 .. gend-1 are in the ring
-  uint32_t lv[MT];    // deque records lv .. dt-1 are also in the LDS window
+  uint32_t wv[MT];    // deque records dt-wv .. dt-1 are also in the LDS window
   int32_t Mj[MT];  // resident memory per type (< 2C <= 2^31)
   // Queue heads.  WAIT: the head of queue j is qpu[j] if bit j of qsrc is
   // set (pushed into an empty queue), else qld[j] (loaded when the previous
@@ -197,7 +202,7 @@ sim_known_kernel(KArgs A) {
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
     gend[j] = kk[j] + 1u;
-    lv[j] = dt[j];
+    wv[j] = 0;
     // unconditional loads: a slot past the tail holds a stale record that is
     // never used (the masks keep every index inside its ring)
     if (WAIT) qld[j] = qring(j)[qh[j] & qmask];
@@ -223,7 +228,7 @@ sim_known_kernel(KArgs A) {
     rec.kc = kc;
     dring(j)[dt[j] & dmask[j]] = rec;
     s_win[j][dt[j] % WB][tx] = rec;
-    if (dt[j] + 1u > (uint32_t)WB && dt[j] + 1u - WB > lv[j]) lv[j] = dt[j] + 1u - WB;
+    wv[j] = wv[j] < (uint32_t)WB ? wv[j] + 1u : wv[j];
     const uint32_t adm = WAIT ? kc : kb;
     const bool empty = dt[j] == dh[j], second = dt[j] == dh[j] + 1u;
     fa[j] = empty ? a_ft : fa[j];
@@ -284,8 +289,8 @@ sim_known_kernel(KArgs A) {
     rec.kc = kc;
     ((DRec *)(blk + pick(doff, j)))[tq & pick(dmask, j)] = rec;
     s_win[j][tq % WB][tx] = rec;
-    const uint32_t lvj = pick(lv, j);
-    place_if(lv, j, tq + 1u > (uint32_t)WB && tq + 1u - WB > lvj, tq + 1u - WB);
+    const uint32_t wvj = pick(wv, j);
+    place(wv, j, wvj < (uint32_t)WB ? wvj + 1u : wvj);
     const uint32_t h = pick(dh, j);
     const uint32_t adm = WAIT ? kc : kb;
     const bool empty = tq == h, second = tq == h + 1u;
@@ -308,7 +313,7 @@ sim_known_kernel(KArgs A) {
     dt[j] = tq;
     if (tq != dh[j]) {  // the new back record
       DRec b;
-      if (tq - 1u >= lv[j])
+      if (wv[j] >= 2u)
         b = s_win[j][(tq - 1u) % WB][tx];
       else
         b = dring(j)[(tq - 1u) & dmask[j]];
@@ -316,6 +321,7 @@ sim_known_kernel(KArgs A) {
       bkb[j] = b.kb;
       bkc[j] = b.kc;
     }
+    wv[j] = wv[j] > 0u ? wv[j] - 1u : 0u;
     const uint32_t admb = WAIT ? rkc : rkb;
     const uint32_t now = WAIT ? svc[j] : bidx_cur;
     const int32_t stage = (int32_t)(now - admb) + 1;
@@ -570,7 +576,7 @@ sim_known_kernel(KArgs A) {
         if (fadm[j] + (uint32_t)lp[j] != now) break;
         const double lat = t_end - arrival_of(fa[j]);
         lat_sum += lat;
-        __hip_atomic_fetch_add(&hist[hist_bin(edges, n_hist, lat)], 1u, __ATOMIC_RELAXED,
+        __hip_atomic_fetch_add(&hist[hist_bin_idx(edges, s_htab, hidx, lat)], 1u, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
         comps++;
         ctok += lp[j];

@@ -59,7 +59,8 @@ int fail(int code, const std::string &msg) {
 // a wavefront's time per batch is set by latency, not by how many of its lanes
 // are busy: when a launch has few replicas they are spread over more
 // wavefronts (64, 32, 16 or 8 per wavefront) until the launch has at least
-// kTargetWaves wavefronts or reaches 8 per wavefront.
+// kTargetWaves wavefronts or reaches 8 per wavefront.  A wavefront never has
+// more lanes than the largest job has replicas (fewer lanes, less LDS).
 #ifndef WS_TARGET_WAVES
 #define WS_TARGET_WAVES 1024
 #endif
@@ -301,9 +302,14 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     bool any_trace = false;
     for (int i = 0; i < n_jobs; ++i)
       any_trace |= jobs[i].pol->kind == pk && jobs[i].cfg->n_trace > 0;
+    int32_t nmax = 0;  // largest job: no wavefront needs more lanes
+    for (int i = 0; i < n_jobs; ++i)
+      if (jobs[i].pol->kind == pk) nmax = std::max(nmax, jobs[i].n);
     int lanes = 64;
-    if (!any_trace)  // arrival-list replays keep 64 per wavefront
+    if (!any_trace) {  // arrival-list replays keep 64 per wavefront
+      while (lanes > 8 && lanes / 2 >= nmax) lanes /= 2;
       while (lanes > 8 && waves(lanes) < kTargetWaves) lanes /= 2;
+    }
     Lo.lanes[pk] = lanes;
     const int64_t count = waves(lanes) * 64;
     if (count > INT32_MAX) return fail(WS_EINVAL, "too many replicas");

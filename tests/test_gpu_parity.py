@@ -141,6 +141,26 @@ def test_edge_cases(sim):
     _check(sim, [W.Job(wl5, 3, W.ids(33))], 2000, "fcfs reserve 1%")
 
 
+def test_histogram_edge_sets(sim):
+    """Bins through the bucket index equal the oracle's count of edges <= the
+    latency for unusual edge sets: negative and zero edges, a span of
+    hundreds of binades, many edges in one binade, one edge, none."""
+    base = W.config2(replicas=1, rate_index=[12])[0].wl
+    sets = [
+        [-5.0, -1.0, 0.0, 1e-300, 1e-3, 7.5, 1e300],
+        list(np.linspace(14.0, 16.0, 255)),
+        [100.0],
+        [],
+        [-1.0],
+        list(np.geomspace(1e-200, 1e200, 255)),
+    ]
+    jobs = []
+    for i, e in enumerate(sets):
+        wl = W.Workload(**{**base.__dict__, "hist_edges": np.asarray(e, dtype=np.float64)})
+        jobs.append(W.Job(wl, 0, W.ids(40, start=100 * i)))
+    _check(sim, jobs, 2500, "histogram edge sets")
+
+
 @pytest.mark.slow
 def test_config2_full_size_sampled(sim):
     """The benchmark's launch: 32 rates x 1024 replicas x 1e5 batches in one
