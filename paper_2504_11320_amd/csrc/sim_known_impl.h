@@ -218,6 +218,16 @@ sim_known_kernel(KArgs A) {
     bkc[j] = b.kc;
   }
   if (!WAIT) q0ld = qring0()[qh[0] & qmask];
+  // wait for these loads here: otherwise the first use inside the loop would
+  // carry a wait that runs on every iteration
+#pragma unroll
+  for (int j = 0; j < MT; ++j) {
+    fa[j] = opaque(fa[j]);
+    fadm[j] = opaque(fadm[j]);
+    ba[j] = opaque(ba[j]);
+    bkb[j] = opaque(bkb[j]);
+    bkc[j] = opaque(bkc[j]);
+  }
 
   // ---- ring operations ------------------------------------------------------
   // Operations with a compile-time type index j (inside unrolled loops).
@@ -311,12 +321,15 @@ sim_known_kernel(KArgs A) {
     const uint32_t rkb = bkb[j], rkc = bkc[j];
     const uint32_t tq = dt[j] - 1u;
     dt[j] = tq;
-    if (tq != dh[j]) {  // the new back record
-      DRec b;
-      if (wv[j] >= 2u)
-        b = s_win[j][(tq - 1u) % WB][tx];
-      else
-        b = dring(j)[(tq - 1u) & dmask[j]];
+    if (tq != dh[j]) {  // the new back record, read from the window
+      if (wv[j] < 2u) {
+        // rare: not in the window; copy it in from HBM.  The load is consumed
+        // inside this branch, so no wait for memory operations (such as the
+        // prefetches of this iteration) follows the branch.
+        s_win[j][(tq - 1u) % WB][tx] = dring(j)[(tq - 1u) & dmask[j]];
+        wv[j] = 2u;  // after the pop below: the new back is valid
+      }
+      const DRec b = s_win[j][(tq - 1u) % WB][tx];
       ba[j] = b.a_ft;
       bkb[j] = b.kb;
       bkc[j] = b.kc;
