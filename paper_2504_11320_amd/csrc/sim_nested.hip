@@ -40,29 +40,61 @@ struct SlotMeta {
 // wavefront (lanes LN..63 are padding), which sizes the per-lane LDS columns.
 template <int MT, int LT, int LN>
 __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
+  // Inter-arrival gaps and output lengths are drawn ahead of use by the
+  // whole wavefront at once into a ring of GR draws per type and lane; a
+  // lane whose ring runs dry draws for itself.
+  constexpr int GR = MT <= 4 ? 16 : 4;
+  constexpr int GU = GR / 2;         // draws added per refill
+  constexpr uint32_t kLow = GU / 2;  // a lane below this triggers a refill
   __shared__ double s_tnext[MT][LN];
-  __shared__ uint32_t s_k[MT][LN];
+  __shared__ uint32_t s_k[MT][LN], s_gend[MT][LN];
   __shared__ int32_t s_Ln[MT][LN];
+  __shared__ double s_gap[MT][GR][LN];
+  __shared__ int32_t s_glen[MT][GR][LN];
+  __shared__ uint64_t s_seed[LN];
+  __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
   __shared__ int64_t s_M[LT][LN], s_B[LT][LN];
+  __shared__ int32_t s_l[MT], s_lp[MT];
+  __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
+  __shared__ uint8_t s_htab[kHistTab];
+  __shared__ int s_hsteps;
 
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tx;
-  if (gid >= A.n_list || tx >= LN) return;  // lanes use only their own LDS column
-  const int32_t r32 = ((const int32_t *)(A.ws + A.off_list))[gid];
-  if (r32 < 0) return;  // padding lane
-  const int64_t r = r32;
-  const uint32_t jix = ((const uint32_t *)(A.ws + A.off_job_of))[r];
+  // replica of this lane, or -1 for padding (padding only ends a job's
+  // wavefront, so lane 0 of every wavefront holds a replica)
+  const int32_t r32 = gid < A.n_list ? ((const int32_t *)(A.ws + A.off_list))[gid] : -1;
+  const int64_t r = r32 < 0 ? 0 : r32;
+  // every lane of a wavefront belongs to the same job: its constants are
+  // wavefront-uniform
+  const uint32_t jix =
+      __builtin_amdgcn_readfirstlane(((const uint32_t *)(A.ws + A.off_job_of))[r]);
   const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
+  const int m = J.m;
+  const int n_hist = J.n_hist;
+  // per-type prompt lengths (indexed by a lane's request type) and the
+  // histogram edges with their bucket index, staged in LDS by the block
+  {
+    const double *edges_g = (const double *)(A.ws + J.off_edges);
+    for (int b = tx; b <= n_hist; b += 64) s_edges[b] = b < n_hist ? edges_g[b] : INFINITY;
+    for (int j = tx; j < MT; j += 64) {
+      s_l[j] = j < m ? J.l[j] : 0;
+      s_lp[j] = j < m ? J.lp[j] : 1;
+    }
+    __syncthreads();
+  }
+  const HistIdx hidx = hist_index_build(s_edges, n_hist, s_htab, &s_hsteps);
+  const double *edges = s_edges;
+  if (r32 < 0 || tx >= LN) return;  // padding lane: uses only its own LDS columns
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
   const uint32_t rid = ((const uint32_t *)(A.ws + A.off_rid))[r];
+  s_seed[tx] = seed;
+  s_rid[tx] = rid;
 
-  const int m = J.m;
   const int L = J.nseg;
   const double d0 = J.d0, d1 = J.d1;
   const int64_t C = J.C;
-  const int n_hist = J.n_hist;
-  const double *edges = (const double *)(A.ws + J.off_edges);
   const bool trace = J.n_trace > 0;
   const bool known = J.known != 0;
   const int32_t cap = J.out_cap;
@@ -161,6 +193,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
   }
 
+  for (int j = 0; j < MT; ++j) s_gend[j][tx] = s_k[j][tx] + 1u;  // gap rings start empty
+
   // ---- arrivals ------------------------------------------------------------
   auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
     if (trace) {
@@ -199,16 +233,23 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   auto take = [&](int jn, double a) __attribute__((always_inline)) {
     int32_t Lr;
     if (trace) {
-      Lr = known ? J.lp[jn] : tr_len[tridx];
+      Lr = known ? s_lp[jn] : tr_len[tridx];
       tridx++;
     } else {
       Lr = s_Ln[jn][tx];
       const uint32_t k = s_k[jn][tx] + 1u;
       s_k[jn][tx] = k;
       int32_t Lj = 1;
-      const double g = draw_gap(seed, rid, (uint32_t)jn, k, J.lambda[jn], row_of(jn), cap, &Lj);
+      double g;
+      if (k < s_gend[jn][tx]) {
+        g = s_gap[jn][k % GR][tx];
+        Lj = s_glen[jn][k % GR][tx];
+      } else {
+        g = draw_gap(seed, rid, (uint32_t)jn, k, J.lambda[jn], row_of(jn), cap, &Lj);
+        s_gend[jn][tx] = k + 1u;
+      }
       s_tnext[jn][tx] = s_tnext[jn][tx] + g;
-      s_Ln[jn][tx] = known ? J.lp[jn] : (cap <= 1 ? 1 : Lj);
+      s_Ln[jn][tx] = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
     }
     arrivals++;
     N++;
@@ -224,7 +265,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const NRec rec = v[vt & vmask(h)];
     s_vt[h][tx] = vt;
     const int32_t rprev = J.seg_end[h - 1];
-    const int64_t ch = (int64_t)J.l[rec.j] + rprev;
+    const int64_t ch = (int64_t)s_l[rec.j] + rprev;
     s_B[h][tx] -= ch;
     Mres -= ch;
     evicts++;
@@ -265,12 +306,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const int32_t delta = J.seg_delta[k];
     const int32_t nk = J.seg_n[k];
     const int64_t stage = (int64_t)J.seg_entry[k] + (int64_t)(s_svc[k][tx] - rec.c) + 1;
-    const int64_t ch = (int64_t)J.l[rec.j] + stage;
+    const int64_t ch = (int64_t)s_l[rec.j] + stage;
     const uint32_t slot = idx / (uint32_t)nk;
     (void)delta;
     SlotMeta *mt = metas(k);
     mt[slot].live -= 1u;
-    mt[slot].suml -= (uint32_t)J.l[rec.j];
+    mt[slot].suml -= (uint32_t)s_l[rec.j];
     const int32_t Lr = rec.L;
     rec.L = 0;  // leaves a hole; the calendar skips it
     rc[idx] = rec;
@@ -323,6 +364,44 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
+    // ---- refill the draw rings, all active lanes together -----------------
+    if (!trace) {
+      const uint64_t act = __ballot(1);
+      const int nact = __popcll(act);
+      const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)act, 0u));
+      for (int j = 0; j < m; ++j) {
+        const uint32_t ge = s_gend[j][tx];
+        const uint32_t avail = ge - s_k[j][tx] - 1u;
+        if (__ballot(avail < kLow) == 0) continue;
+        const bool room = avail <= (uint32_t)(GR - GU);
+        const uint64_t need = __ballot(room);
+        const int p = __popcll(need);
+        if (room) {
+          const int rk = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(need >> 32),
+                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
+          s_req_lane[rk] = (uint32_t)tx;
+          s_req_k[rk] = ge;
+        }
+        __syncthreads();
+        const int total = p * GU;
+        const double lamj = J.lambda[j];
+        const uint32_t *row = row_of(j);
+        for (int base = 0; base < total; base += nact) {
+          const int w = base + wrank;
+          if (w < total) {
+            const int ln = (int)s_req_lane[w / GU];
+            const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
+            int32_t Lj = 1;
+            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lamj, row, cap, &Lj);
+            s_glen[j][k % GR][ln] = Lj;
+          }
+        }
+        __syncthreads();
+        if (room) s_gend[j][tx] = ge + GU;
+      }
+    }
+
     // ---- decision: largest prefix of segments meeting their thresholds -----
     int kmax = 0;
     for (;;) {
@@ -383,12 +462,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           e.L = qr.L;
           e.kb = bidx;
           e.kp = (uint32_t)i;
-          tokens += J.l[qr.j];
-          prefill_l += J.l[qr.j];
+          tokens += s_l[qr.j];
+          prefill_l += s_l[qr.j];
           if (!has_ft(qr.a_ft)) pend_new++;
         } else {
           e = vring(k)[(s_vh[k][tx] + (uint32_t)i) & vmask(k)];
-          tokens += (int64_t)J.l[e.j] + J.seg_end[k - 1] + 1;
+          tokens += (int64_t)s_l[e.j] + J.seg_end[k - 1] + 1;
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
@@ -397,7 +476,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         e.next = bk[b];
         bk[b] = idx;
         rc[idx] = e;
-        suml += (uint32_t)J.l[e.j];
+        suml += (uint32_t)s_l[e.j];
       }
       SlotMeta sm;
       sm.live = (uint32_t)nk;
@@ -484,7 +563,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       // entering prompts: leave the entry queue, stay unless they exit now
       for (int32_t i = 0; i < nk; ++i) {
         const NRec e = rc[slot * (uint32_t)nk + (uint32_t)i];
-        const int64_t le = J.l[e.j];
+        const int64_t le = s_l[e.j];
         if (k > 0) {
           s_B[k][tx] -= le + J.seg_end[k - 1];
           Mres -= le + J.seg_end[k - 1];
@@ -504,7 +583,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         const NRec rec = rc[idx];
         const uint32_t nxt = rec.next;
         if (rec.L != 0) {  // holes left by evictions are skipped
-          const int64_t le = J.l[rec.j];
+          const int64_t le = s_l[rec.j];
           const int32_t p = rec.L < rk ? rec.L : rk;
           if (rec.c != x) {  // an interior prompt: it had advanced to p + 1
             Mk -= le + p + 1;
@@ -516,7 +595,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           if (rec.L == p) {  // completion at its own output length
             const double lat = t_end - arrival_of(rec.a_ft);
             lat_sum += lat;
-            __hip_atomic_fetch_add(&hist[hist_bin(edges, n_hist, lat)], 1u,
+            __hip_atomic_fetch_add(&hist[hist_bin_idx(edges, s_htab, hidx, lat)], 1u,
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             comps++;
             ctok += rec.L;
