@@ -47,16 +47,19 @@ KERNEL_SRCS = [os.path.join(CSRC, f)
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_wait_3type_32x1024x1e5_hbm.md")
 
 
-def op_model(m: int) -> dict:
+def op_model(m: int, cdf_cap: int = 0) -> dict:
     """Algorithmic lane-operations per event (full-rate VALU instruction
-    equivalents; a 32x32->64-bit multiply counts 4)."""
+    equivalents; a 32x32->64-bit multiply counts 4).  cdf_cap > 1: output
+    lengths are drawn from a CDF table of that many entries (a search of
+    2 ops per halving step)."""
     philox = 10 * (2 * 4 + 4 + 2)     # 2 wide multiplies, 4 xor, 2 key adds per round
     uniform = 10                      # 52-bit assembly, int->fp64, scale
     ln = 50                           # reduction, one fp64 division, 12-term Horner, e*ln2
     gap = 14                          # fp64 division by lambda, add to the clock
     book = 12                         # queue push, counters, area terms
+    cdf = 2 * max(0, int(cdf_cap - 1).bit_length()) if cdf_cap > 1 else 0
     return {
-        "arrival": philox + uniform + ln + gap + book + 2 * m,
+        "arrival": philox + uniform + ln + gap + book + 2 * m + cdf,
         "batch": 24 + 6 * m,          # eligibility, tokens, tau, clock, areas, peak
         "completion": 35,             # latency, sum, histogram search and update
         "eviction": 14 + 3 * m,       # LIFO choice, stage, memory, re-queue
@@ -64,8 +67,8 @@ def op_model(m: int) -> dict:
     }
 
 
-def algorithmic_ops(res: dict, m: int) -> float:
-    c = op_model(m)
+def algorithmic_ops(res: dict, m: int, cdf_cap: int = 0) -> float:
+    c = op_model(m, cdf_cap)
     return float(c["batch"] * res["batches"].sum() + c["arrival"] * res["arrivals"].sum()
                  + c["completion"] * res["completions"].sum()
                  + c["eviction"] * res["evictions"].sum() + c["idle"] * res["idle_waits"].sum())
@@ -99,18 +102,46 @@ def traffic_from_profile():
     return float(b.group(1))
 
 
-def cpu_baseline(horizon: int, replicas: int, threads: int) -> dict:
-    from oracle import oracle as O
+# Workloads this script can time (the first is the benchmark's).  Each entry:
+# (description, job builder, horizon, policy, jobs sampled by the CPU baseline)
+def _workloads():
     import workloads as W
-    jobs = W.config2(replicas=replicas, rate_index=[0, 31])
+    return {
+        "wait-llama": ("WAIT, Llama-2-7B-shaped 3-type synthetic mix, 32 rates "
+                       "0.5-1.2x fluid boundary, 1024 replicas each",
+                       lambda reps: W.config2(replicas=reps), 100000, "wait", [0, 31]),
+        "nested-geometric": ("Nested WAIT, 3 types, geometric outputs capped at 2048, "
+                             "segments (64,256,1024,2048), 32 rates x 1024 replicas",
+                             lambda reps: W.config3(replicas=reps), 100000, "nested", [0, 31]),
+        "wait-sweep": ("WAIT threshold grid 16x16 x 16 rates x 16 replicas plus FCFS "
+                       "on the same streams",
+                       lambda reps: W.config4(), 100000, "wait+fcfs", [0, 4096]),
+        "nested-heavytail": ("Nested WAIT, 10 lognormal-decile prompt types, lognormal "
+                             "outputs capped at 4096, 6 segments, 8192 replicas",
+                             lambda reps: W.config5(), 1000000, "nested", [0]),
+        "wait-small": ("WAIT, 2 types (16/8, 32/16), C = 2048, 64 replicas",
+                       lambda reps: W.config1(), 10000, "wait", [0]),
+    }
+
+
+def cpu_baseline(jobs, pick, horizon: int, replicas: int, threads: int) -> dict:
+    """The oracle on a bounded sample: `replicas` replicas of each picked job,
+    the full horizon (at most 1e5 batches)."""
+    from oracle import oracle as O
+    import numpy as np
+    import workloads as W
+    horizon = min(horizon, 100000)
     t0 = time.perf_counter()
     total = 0
-    for job in jobs:
-        r = O.run_job(job, horizon, threads=threads)
+    for i in pick:
+        job = jobs[i]
+        sub = W.Job(job.wl, job.seed, np.asarray(job.replica_ids[:replicas], dtype=np.uint32))
+        r = O.run_job(sub, horizon, threads=threads)
         total += int(r["batches"].sum())
     dt = time.perf_counter() - t0
+    n = min(replicas, min(jobs[i].n for i in pick))
     return {"value": total / dt, "unit": UNIT, "cores": threads, "kind": "oracle",
-            "sample": f"rates 0 and 31 of 32 x {replicas} replicas x {horizon} batches "
+            "sample": f"jobs {pick} of {len(jobs)} x {n} replicas x {horizon} batches "
                       f"({total} replica-iterations, {dt:.1f} s)"}
 
 
@@ -119,7 +150,10 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--horizon", type=int, default=100000)
+    ap.add_argument("--workload", default="wait-llama",
+                    help="wait-llama (the benchmark), nested-geometric, wait-sweep, "
+                         "nested-heavytail, wait-small")
+    ap.add_argument("--horizon", type=int, default=0, help="batches (0: the workload's)")
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-replicas", type=int, default=256)
@@ -155,8 +189,15 @@ def main() -> int:
         return 1
     B.lib()  # fails loudly if the HIP library is missing
 
-    jobs = W.config2(replicas=args.replicas)
-    m = jobs[0].wl.m
+    table = _workloads()
+    if args.workload not in table:
+        print(f"bench.py: unknown workload {args.workload}", file=sys.stderr)
+        return 2
+    desc, build, horizon0, policy, pick = table[args.workload]
+    args.horizon = args.horizon or horizon0
+    jobs = build(args.replicas)
+    m = max(j.wl.m for j in jobs)
+    cdf_cap = max((j.wl.out_cap for j in jobs if j.wl.out_cdf is not None), default=0)
     sim = B.Simulation(jobs)
     sim.prepare()
     stream = torch.cuda.current_stream()
@@ -178,13 +219,13 @@ def main() -> int:
 
     res = sim.results()
     rep_its = int(res["batches"].sum())
-    if rep_its != len(res["batches"]) * args.horizon or np.any(res["flags"]):
+    if rep_its != len(res["batches"]) * args.horizon or np.any(res["flags"] & 3):
         print("bench.py: some replicas stopped early (flags set)", file=sys.stderr)
     value = rep_its / (ms_step / 1e3)
 
-    ops = algorithmic_ops(res, m)
+    ops = algorithmic_ops(res, m, cdf_cap)
     achieved = ops / (ms_step / 1e3)
-    traffic = traffic_from_profile()
+    traffic = traffic_from_profile() if args.workload == "wait-llama" else None
     roofline = {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK,
                 "unit": "lane-ops/s", "frac": achieved / ALU_PEAK,
                 "traffic": traffic,
@@ -196,23 +237,23 @@ def main() -> int:
                 "hbm_algorithmic_frac": algorithmic_bytes(res) / (ms_step / 1e3) / HBM_PEAK,
                 "hbm_measured_frac": (traffic / (ms_step / 1e3) / HBM_PEAK
                                       if traffic is not None else None),
-                "kernel": f"sim_known_kernel (WAIT, {m} types)"}
+                "kernel": (f"sim_nested_kernel ({m} types)" if policy == "nested"
+                           else f"sim_known_kernel ({policy}, {m} types)")}
 
     out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "f64", "data": "synthetic",
-           "config": {"workload": "WAIT, Llama-2-7B-shaped 3-type synthetic mix, "
-                                  "32 rates 0.5-1.2x fluid boundary",
-                      "replicas": len(res["batches"]), "rates": len(jobs),
-                      "replicas_per_rate": args.replicas, "horizon_batches": args.horizon,
-                      "replica_iterations_per_step": rep_its, "policy": "wait",
-                      "kv_budget_tokens": 131072},
+           "config": {"workload": desc, "name": args.workload,
+                      "replicas": len(res["batches"]), "jobs": len(jobs),
+                      "horizon_batches": args.horizon,
+                      "replica_iterations_per_step": rep_its, "policy": policy,
+                      "kv_budget_tokens": int(max(j.wl.C for j in jobs))},
            "roofline": roofline,
            "wall_s_timed": wall}
     if not args.no_cpu_baseline:
         threads = max(1, min(os.cpu_count() or 1, 16))
-        out["cpu_baseline"] = cpu_baseline(args.horizon, args.cpu_replicas, threads)
+        out["cpu_baseline"] = cpu_baseline(jobs, pick, args.horizon, args.cpu_replicas, threads)
     print(json.dumps(out), flush=True)
     return 0
 
