@@ -63,7 +63,7 @@ typedef enum {
   WS_ENOMEM = -2,      /* host allocation failed                          */
   WS_EDEVICE = -3,     /* HIP runtime error                               */
   WS_EWORKSPACE = -4,  /* workspace or result buffer too small            */
-  WS_EUNSUPPORTED = -5 /* valid model, but outside this build's limits    */
+  WS_EUNSUPPORTED = -5 /* valid model, but outside the library's limits  */
 } ws_status;
 
 typedef enum { WS_WAIT = 0, WS_NESTED_WAIT = 1, WS_FCFS = 2 } ws_policy_kind;
@@ -75,7 +75,7 @@ typedef enum { WS_WAIT = 0, WS_NESTED_WAIT = 1, WS_FCFS = 2 } ws_policy_kind;
 #define WS_FLAG_OVERFLOW 4u /* Nested WAIT launched with a projected state
                                above C after every allowed eviction          */
 
-/* Limits of this build. */
+/* Limits of the library. */
 #define WS_MAX_TYPES 16
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255

@@ -172,7 +172,7 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     for (int j = 0; j < c.m; ++j)
       if (c.prompt_len[j] > c.C - reserve_tok)
         return fail(WS_EINVAL, at + "a prompt does not fit below the FCFS reserve");
-    if (!known) return fail(WS_EUNSUPPORTED, at + "FCFS with unknown lengths is not in this build");
+    if (!known) return fail(WS_EUNSUPPORTED, at + "FCFS with unknown lengths is not supported");
   } else if (p.kind == WS_NESTED_WAIT) {
     if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail(WS_EINVAL, at + "L out of range");
     if (!p.n || !p.seg_end) return fail(WS_EINVAL, at + "thresholds and seg_end required");
