@@ -43,7 +43,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // Inter-arrival gaps and output lengths are drawn ahead of use by the
   // whole wavefront at once into a ring of GR draws per type and lane; a
   // lane whose ring runs dry draws for itself.
-  constexpr int GR = MT <= 4 ? 16 : 4;
+  constexpr int GR = MT <= 4 ? 8 : 4;
   constexpr int GU = GR / 2;         // draws added per refill
   constexpr uint32_t kLow = GU / 2;  // a lane below this triggers a refill
   __shared__ double s_tnext[MT][LN];
@@ -56,6 +56,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
   __shared__ int64_t s_M[LT][LN], s_B[LT][LN];
   __shared__ int32_t s_l[MT], s_lp[MT];
+  // Per lane: the back record of each boundary queue, and the youngest live
+  // interior record of each segment with its index (kNil: not known; found by
+  // a scan when next needed).  LIFO selections then read no HBM.
+  __shared__ NRec s_vb[LT][LN], s_yi[LT][LN];
+  __shared__ uint32_t s_yidx[LT][LN];
   __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
   __shared__ uint8_t s_htab[kHistTab];
   __shared__ int s_hsteps;
@@ -194,6 +199,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   }
 
   for (int j = 0; j < MT; ++j) s_gend[j][tx] = s_k[j][tx] + 1u;  // gap rings start empty
+  for (int k = 0; k < LT; ++k) {
+    s_yidx[k][tx] = kNil;
+    if (k >= 1 && k < L && s_vt[k][tx] != s_vh[k][tx])
+      s_vb[k][tx] = vring(k)[(s_vt[k][tx] - 1u) & vmask(k)];
+  }
 
   // ---- arrivals ------------------------------------------------------------
   auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
@@ -260,10 +270,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // ---- evictions -------------------------------------------------------------
   // Evict the back (most recently admitted) prompt of boundary queue h >= 1.
   auto evict_boundary = [&](int h) __attribute__((always_inline)) -> int64_t {
-    NRec *v = vring(h);
     const uint32_t vt = s_vt[h][tx] - 1u;
-    const NRec rec = v[vt & vmask(h)];
+    const NRec rec = s_vb[h][tx];
     s_vt[h][tx] = vt;
+    if (vt != s_vh[h][tx]) s_vb[h][tx] = vring(h)[(vt - 1u) & vmask(h)];  // the new back
     const int32_t rprev = J.seg_end[h - 1];
     const int64_t ch = (int64_t)s_l[rec.j] + rprev;
     s_B[h][tx] -= ch;
@@ -279,6 +289,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // or kNil.
   auto youngest_interior = [&](int k, uint32_t &kb, uint32_t &kp) __attribute__((always_inline)) -> uint32_t {
     if (s_I[k][tx] == 0) return kNil;
+    const uint32_t y = s_yidx[k][tx];
+    if (y != kNil) {
+      kb = s_yi[k][tx].kb;
+      kp = s_yi[k][tx].kp;
+      return y;
+    }
     const int32_t delta = J.seg_delta[k];
     const int32_t nk = J.seg_n[k];
     const uint32_t svc = s_svc[k][tx];
@@ -293,6 +309,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         if (rec.L != 0) {
           kb = rec.kb;
           kp = rec.kp;
+          s_yi[k][tx] = rec;
+          s_yidx[k][tx] = idx;
           return idx;
         }
       }
@@ -302,7 +320,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
   auto evict_interior = [&](int k, uint32_t idx) __attribute__((always_inline)) -> int64_t {
     NRec *rc = recs(k);
-    NRec rec = rc[idx];
+    NRec rec = s_yi[k][tx];  // idx is the segment's youngest live interior record
+    s_yidx[k][tx] = kNil;
     const int32_t delta = J.seg_delta[k];
     const int32_t nk = J.seg_n[k];
     const int64_t stage = (int64_t)J.seg_entry[k] + (int64_t)(s_svc[k][tx] - rec.c) + 1;
@@ -335,11 +354,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     uint32_t bkb = 0, bkp = 0;
     for (int h = 1; h < L; ++h) {
       if (s_vt[h][tx] == s_vh[h][tx]) continue;
-      const NRec rec = vring(h)[(s_vt[h][tx] - 1u) & vmask(h)];
-      if (hb < 0 || rec.kb > bkb || (rec.kb == bkb && rec.kp > bkp)) {
+      const uint32_t rkb = s_vb[h][tx].kb, rkp = s_vb[h][tx].kp;
+      if (hb < 0 || rkb > bkb || (rkb == bkb && rkp > bkp)) {
         hb = h;
-        bkb = rec.kb;
-        bkp = rec.kp;
+        bkb = rkb;
+        bkp = rkp;
       }
     }
     if (hb >= 0) return evict_boundary(hb);
@@ -476,6 +495,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         e.next = bk[b];
         bk[b] = idx;
         rc[idx] = e;
+        if (i == nk - 1) {  // the cohort's last record is the segment's youngest
+          s_yi[k][tx] = e;
+          s_yidx[k][tx] = idx;
+        }
         suml += (uint32_t)s_l[e.j];
       }
       SlotMeta sm;
@@ -583,6 +606,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         const NRec rec = rc[idx];
         const uint32_t nxt = rec.next;
         if (rec.L != 0) {  // holes left by evictions are skipped
+          if (idx == s_yidx[k][tx]) s_yidx[k][tx] = kNil;  // the youngest leaves
           const int64_t le = s_l[rec.j];
           const int32_t p = rec.L < rk ? rec.L : rk;
           if (rec.c != x) {  // an interior prompt: it had advanced to p + 1
@@ -608,6 +632,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             if (vt - s_vh[h][tx] <= vmask(h)) {
               vring(h)[vt & vmask(h)] = v;
               s_vt[h][tx] = vt + 1u;
+              s_vb[h][tx] = v;
             } else {
               flags |= kFlagCap;  // bounded by construction; guards the ring
             }
@@ -675,9 +700,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 template <int MT, int LT>
 hipError_t launch_ml(const KArgs &A, hipStream_t s) {
   const dim3 g((A.n_list + 63) / 64), b(64);
-  if (A.lanes == 64)
-    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 64>), g, b, 0, s, A);
-  else if (A.lanes == 32)
+  if (A.lanes == 32)
     hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 32>), g, b, 0, s, A);
   else if (A.lanes == 16)
     hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 16>), g, b, 0, s, A);

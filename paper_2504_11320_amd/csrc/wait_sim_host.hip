@@ -305,8 +305,9 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     int32_t nmax = 0;  // largest job: no wavefront needs more lanes
     for (int i = 0; i < n_jobs; ++i)
       if (jobs[i].pol->kind == pk) nmax = std::max(nmax, jobs[i].n);
-    int lanes = 64;
-    if (!any_trace) {  // arrival-list replays keep 64 per wavefront
+    // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32
+    int lanes = pk == WS_NESTED_WAIT ? 32 : 64;
+    if (!any_trace || pk == WS_NESTED_WAIT) {  // known-length replays keep 64
       while (lanes > 8 && lanes / 2 >= nmax) lanes /= 2;
       while (lanes > 8 && waves(lanes) < kTargetWaves) lanes /= 2;
     }
