@@ -41,7 +41,6 @@ struct JobDev {
   uint64_t off_d[kMaxTypes];    // resident deques inside a replica block
   uint64_t off_rec[kMaxSeg];    // Nested: interior records [delta][n]
   uint64_t off_bkt[kMaxSeg];    // Nested: calendar bucket heads [delta]
-  uint64_t off_meta[kMaxSeg];   // Nested: cohort-slot live count and sum of l
   uint64_t off_v[kMaxSeg];      // Nested: boundary-queue rings (k >= 1)
 };
 

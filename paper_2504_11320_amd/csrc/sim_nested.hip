@@ -24,17 +24,13 @@
 // of survivors joining the next boundary queue.
 //
 // The projected state Q+ of the pre-launch repair (apply the selected moves
-// with no early completion) is computed from per-segment counts and the live
-// count and prompt-length sum of the terminal cohort slot.
+// with no early completion) is computed from per-segment counts and the
+// prompts still live in the terminal cohort slot (a record with L = 0 has left
+// its segment).
 #include "sim_common.h"
 
 namespace wsim {
 namespace {
-
-struct SlotMeta {
-  uint32_t live;  // prompts of the cohort still in the segment
-  uint32_t suml;  // sum of their prompt lengths
-};
 
 // MT: type slots (>= m); LT: segment slots (>= L); LN: replicas per
 // wavefront (lanes LN..63 are padding), which sizes the per-lane LDS columns.
@@ -61,6 +57,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // a scan when next needed).  LIFO selections then read no HBM.
   __shared__ NRec s_vb[LT][LN], s_yi[LT][LN];
   __shared__ uint32_t s_yidx[LT][LN];
+  // per lane and segment: the entering cohort's accounting, formed at launch
+  __shared__ int32_t s_eB[LT][LN], s_eM[LT][LN];
+  __shared__ uint32_t s_eI[LT][LN];
   __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
   __shared__ uint8_t s_htab[kHistTab];
   __shared__ int s_hsteps;
@@ -115,7 +114,6 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
   auto recs = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + J.off_rec[k]); };
   auto bkts = [&](int k) __attribute__((always_inline)) { return (uint32_t *)(blk + J.off_bkt[k]); };
-  auto metas = [&](int k) __attribute__((always_inline)) { return (SlotMeta *)(blk + J.off_meta[k]); };
   auto vring = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + J.off_v[k]); };
   auto vmask = [&](int k) __attribute__((always_inline)) { return (1u << J.vcap_log2[k]) - 1u; };
   auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
@@ -149,12 +147,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       s_M[k][tx] = s_B[k][tx] = 0;
       if (k < L) {
         uint32_t *bk = bkts(k);
-        SlotMeta *mt = metas(k);
-        for (int x = 0; x < J.seg_delta[k]; ++x) {
-          bk[x] = kNil;
-          mt[x].live = 0;
-          mt[x].suml = 0;
-        }
+        for (int x = 0; x < J.seg_delta[k]; ++x) bk[x] = kNil;
       }
     }
     for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
@@ -298,11 +291,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const int32_t delta = J.seg_delta[k];
     const int32_t nk = J.seg_n[k];
     const uint32_t svc = s_svc[k][tx];
-    const SlotMeta *mt = metas(k);
     const NRec *rc = recs(k);
     for (int32_t back = 0; back < delta && (int64_t)svc - back >= 1; ++back) {
       const uint32_t slot = (svc - (uint32_t)back) % (uint32_t)delta;
-      if (mt[slot].live == 0) continue;
+      // a record with L = 0 has left the segment (exit or eviction)
       for (int32_t i = nk - 1; i >= 0; --i) {
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
         const NRec rec = rc[idx];
@@ -326,11 +318,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const int32_t nk = J.seg_n[k];
     const int64_t stage = (int64_t)J.seg_entry[k] + (int64_t)(s_svc[k][tx] - rec.c) + 1;
     const int64_t ch = (int64_t)s_l[rec.j] + stage;
-    const uint32_t slot = idx / (uint32_t)nk;
     (void)delta;
-    SlotMeta *mt = metas(k);
-    mt[slot].live -= 1u;
-    mt[slot].suml -= (uint32_t)s_l[rec.j];
+    (void)nk;
     const int32_t Lr = rec.L;
     rec.L = 0;  // leaves a hole; the calendar skips it
     rc[idx] = rec;
@@ -471,6 +460,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       uint32_t *bk = bkts(k);
       tokens += s_M[k][tx];
       uint32_t suml = 0;
+      int32_t eB = 0, eM = 0;
+      uint32_t eI = 0;
       // link in reverse selection order: traversal is then in key order
       for (int32_t i = nk - 1; i >= 0; --i) {
         NRec e;
@@ -500,11 +491,17 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           s_yidx[k][tx] = idx;
         }
         suml += (uint32_t)s_l[e.j];
+        // what the completion step does with the entering prompts
+        const int32_t le = s_l[e.j];
+        if (k > 0) eB += le + J.seg_end[k - 1];
+        if (pexit > ent) {
+          eI += 1u;
+          eM += le + ent + 1;
+        }
       }
-      SlotMeta sm;
-      sm.live = (uint32_t)nk;
-      sm.suml = suml;
-      metas(k)[slot] = sm;
+      s_eB[k][tx] = eB;
+      s_eI[k][tx] = eI;
+      s_eM[k][tx] = eM;
       if (k == 0)
         qh += (uint32_t)nk;
       else
@@ -513,9 +510,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       if (delta >= 2) {
         uint32_t T = 0, Tl = 0;
         if ((int64_t)x - (delta - 1) >= 1) {
-          const SlotMeta tm = metas(k)[(x - (uint32_t)(delta - 1)) % (uint32_t)delta];
-          T = tm.live;
-          Tl = tm.suml;
+          // the terminal cohort slot: its prompts still in the segment
+          const uint32_t ts = (x - (uint32_t)(delta - 1)) % (uint32_t)delta;
+          for (int32_t i = 0; i < nk; ++i) {
+            const NRec tr = rc[ts * (uint32_t)nk + (uint32_t)i];
+            const bool live = tr.L != 0;
+            T += live ? 1u : 0u;
+            Tl += live ? (uint32_t)s_l[tr.j] : 0u;
+          }
         }
         mplus += (int64_t)s_I[k][tx] - T;
         if (k == L - 1) mplus -= (int64_t)Tl + (int64_t)T * rk;
@@ -569,14 +571,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     // ---- completion transition, segment by segment ---------------------------
     for (int k = 0; k < kmax; ++k) {
       const int32_t delta = J.seg_delta[k];
-      const int32_t nk = J.seg_n[k];
       const int32_t rk = J.seg_end[k];
-      const int32_t ent = J.seg_entry[k];
       const uint32_t x = s_svc[k][tx] + 1u;
       s_svc[k][tx] = x;
-      const uint32_t slot = x % (uint32_t)delta;
       NRec *rc = recs(k);
-      SlotMeta *mt = metas(k);
       if (k == 0) {  // the stage-1 cohort produces its first tokens
         U -= pendft;
         pendft = pend_new;
@@ -584,19 +582,13 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       int64_t Mk = s_M[k][tx] + (int64_t)s_I[k][tx];  // every interior prompt advances
       uint32_t Ik = s_I[k][tx];
       // entering prompts: leave the entry queue, stay unless they exit now
-      for (int32_t i = 0; i < nk; ++i) {
-        const NRec e = rc[slot * (uint32_t)nk + (uint32_t)i];
-        const int64_t le = s_l[e.j];
-        if (k > 0) {
-          s_B[k][tx] -= le + J.seg_end[k - 1];
-          Mres -= le + J.seg_end[k - 1];
-        }
-        const int32_t pexit = e.L < rk ? e.L : rk;
-        if (pexit > ent) {
-          Ik += 1u;
-          Mk += le + ent + 1;
-        }
+      // (their sums were formed at launch)
+      if (k > 0) {
+        s_B[k][tx] -= s_eB[k][tx];
+        Mres -= s_eB[k][tx];
       }
+      Ik += s_eI[k][tx];
+      Mk += s_eM[k][tx];
       // prompts whose exit is at this service
       uint32_t *bk = bkts(k);
       const uint32_t b = x % (uint32_t)delta;
@@ -613,9 +605,6 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             Mk -= le + p + 1;
             Ik -= 1u;
           }
-          SlotMeta &sm = mt[idx / (uint32_t)nk];
-          sm.live -= 1u;
-          sm.suml -= (uint32_t)le;
           if (rec.L == p) {  // completion at its own output length
             const double lat = t_end - arrival_of(rec.a_ft);
             lat_sum += lat;

@@ -258,8 +258,6 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
       off += align_up(sizeof(NRec) * slots * (uint64_t)p.n[k], 256);
       d.off_bkt[k] = off;
       off += align_up(4ull * slots, 256);
-      d.off_meta[k] = off;
-      off += align_up(8ull * slots, 256);
       if (k > 0) {
         d.off_v[k] = off;
         off += align_up(sizeof(NRec) << d.vcap_log2[k], 256);
