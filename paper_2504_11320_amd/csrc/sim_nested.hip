@@ -32,6 +32,20 @@
 namespace wsim {
 namespace {
 
+// Per-segment constants, staged in LDS: a segment index is often
+// lane-dependent (it starts at a lane's own prefix length), and LDS serves
+// such reads without a round trip to the job table in memory.
+struct SegConst {
+  int32_t end;      // r_k
+  int32_t n;        // n_k
+  int32_t delta;    // processing stages (cohort slots)
+  int32_t entry;    // processing stage of an entering prompt
+  uint32_t vmask;   // boundary-queue ring mask (k >= 1)
+  uint32_t off_rec; // ring offsets inside a replica block
+  uint32_t off_bkt;
+  uint32_t off_v;
+};
+
 // MT: type slots (>= m); LT: segment slots (>= L); LN: replicas per
 // wavefront (lanes LN..63 are padding), which sizes the per-lane LDS columns.
 template <int MT, int LT, int LN>
@@ -52,6 +66,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
   __shared__ int64_t s_M[LT][LN], s_B[LT][LN];
   __shared__ int32_t s_l[MT], s_lp[MT];
+  __shared__ SegConst s_seg[LT];
   // Per lane: the back record of each boundary queue, and the youngest live
   // interior record of each segment with its index (kNil: not known; found by
   // a scan when next needed).  LIFO selections then read no HBM.
@@ -86,6 +101,19 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       s_l[j] = j < m ? J.l[j] : 0;
       s_lp[j] = j < m ? J.lp[j] : 1;
     }
+    for (int k = tx; k < LT; k += 64) {
+      SegConst c;
+      const bool on = k < J.nseg;
+      c.end = on ? J.seg_end[k] : 0;
+      c.n = on ? J.seg_n[k] : 0;
+      c.delta = on ? J.seg_delta[k] : 1;
+      c.entry = on ? J.seg_entry[k] : 0;
+      c.vmask = on && k >= 1 ? (1u << J.vcap_log2[k]) - 1u : 0u;
+      c.off_rec = on ? (uint32_t)J.off_rec[k] : 0u;
+      c.off_bkt = on ? (uint32_t)J.off_bkt[k] : 0u;
+      c.off_v = on && k >= 1 ? (uint32_t)J.off_v[k] : 0u;
+      s_seg[k] = c;
+    }
     __syncthreads();
   }
   const HistIdx hidx = hist_index_build(s_edges, n_hist, s_htab, &s_hsteps);
@@ -112,10 +140,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   QRec *q10 = (QRec *)(blk + J.off_q[0]);
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
 
-  auto recs = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + J.off_rec[k]); };
-  auto bkts = [&](int k) __attribute__((always_inline)) { return (uint32_t *)(blk + J.off_bkt[k]); };
-  auto vring = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + J.off_v[k]); };
-  auto vmask = [&](int k) __attribute__((always_inline)) { return (1u << J.vcap_log2[k]) - 1u; };
+  auto recs = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + s_seg[k].off_rec); };
+  auto bkts = [&](int k) __attribute__((always_inline)) { return (uint32_t *)(blk + s_seg[k].off_bkt); };
+  auto vring = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + s_seg[k].off_v); };
+  auto vmask = [&](int k) __attribute__((always_inline)) { return s_seg[k].vmask; };
   auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
     return (known || cap <= 1) ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
   };
@@ -147,7 +175,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       s_M[k][tx] = s_B[k][tx] = 0;
       if (k < L) {
         uint32_t *bk = bkts(k);
-        for (int x = 0; x < J.seg_delta[k]; ++x) bk[x] = kNil;
+        for (int x = 0; x < s_seg[k].delta; ++x) bk[x] = kNil;
       }
     }
     for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
@@ -267,7 +295,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const NRec rec = s_vb[h][tx];
     s_vt[h][tx] = vt;
     if (vt != s_vh[h][tx]) s_vb[h][tx] = vring(h)[(vt - 1u) & vmask(h)];  // the new back
-    const int32_t rprev = J.seg_end[h - 1];
+    const int32_t rprev = s_seg[h - 1].end;
     const int64_t ch = (int64_t)s_l[rec.j] + rprev;
     s_B[h][tx] -= ch;
     Mres -= ch;
@@ -288,8 +316,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       kp = s_yi[k][tx].kp;
       return y;
     }
-    const int32_t delta = J.seg_delta[k];
-    const int32_t nk = J.seg_n[k];
+    const int32_t delta = s_seg[k].delta;
+    const int32_t nk = s_seg[k].n;
     const uint32_t svc = s_svc[k][tx];
     const NRec *rc = recs(k);
     for (int32_t back = 0; back < delta && (int64_t)svc - back >= 1; ++back) {
@@ -314,9 +342,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     NRec *rc = recs(k);
     NRec rec = s_yi[k][tx];  // idx is the segment's youngest live interior record
     s_yidx[k][tx] = kNil;
-    const int32_t delta = J.seg_delta[k];
-    const int32_t nk = J.seg_n[k];
-    const int64_t stage = (int64_t)J.seg_entry[k] + (int64_t)(s_svc[k][tx] - rec.c) + 1;
+    const int32_t delta = s_seg[k].delta;
+    const int32_t nk = s_seg[k].n;
+    const int64_t stage = (int64_t)s_seg[k].entry + (int64_t)(s_svc[k][tx] - rec.c) + 1;
     const int64_t ch = (int64_t)s_l[rec.j] + stage;
     (void)delta;
     (void)nk;
@@ -417,9 +445,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         stopped = true;
         break;
       }
-      if ((int64_t)(qt - qh) >= J.seg_n[0]) {
+      if ((int64_t)(qt - qh) >= s_seg[0].n) {
         kmax = 1;
-        while (kmax < L && (int64_t)(s_vt[kmax][tx] - s_vh[kmax][tx]) >= J.seg_n[kmax]) kmax++;
+        while (kmax < L && (int64_t)(s_vt[kmax][tx] - s_vh[kmax][tx]) >= s_seg[kmax].n) kmax++;
         break;
       }
       int jn;
@@ -450,10 +478,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     int64_t tokens = 0, prefill_l = 0, mplus = Mres;
     int64_t pend_new = 0;
     for (int k = 0; k < kmax; ++k) {
-      const int32_t delta = J.seg_delta[k];
-      const int32_t nk = J.seg_n[k];
-      const int32_t rk = J.seg_end[k];
-      const int32_t ent = J.seg_entry[k];
+      const int32_t delta = s_seg[k].delta;
+      const int32_t nk = s_seg[k].n;
+      const int32_t rk = s_seg[k].end;
+      const int32_t ent = s_seg[k].entry;
       const uint32_t x = s_svc[k][tx] + 1u;
       const uint32_t slot = x % (uint32_t)delta;
       NRec *rc = recs(k);
@@ -477,7 +505,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           if (!has_ft(qr.a_ft)) pend_new++;
         } else {
           e = vring(k)[(s_vh[k][tx] + (uint32_t)i) & vmask(k)];
-          tokens += (int64_t)s_l[e.j] + J.seg_end[k - 1] + 1;
+          tokens += (int64_t)s_l[e.j] + s_seg[k - 1].end + 1;
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
@@ -493,7 +521,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         suml += (uint32_t)s_l[e.j];
         // what the completion step does with the entering prompts
         const int32_t le = s_l[e.j];
-        if (k > 0) eB += le + J.seg_end[k - 1];
+        if (k > 0) eB += le + s_seg[k - 1].end;
         if (pexit > ent) {
           eI += 1u;
           eM += le + ent + 1;
@@ -529,7 +557,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         if (k < L - 1)
           mplus += nk;                  // l + r_{k-1} -> l + r_k
         else
-          mplus -= (int64_t)suml + (int64_t)nk * J.seg_end[k - 1];
+          mplus -= (int64_t)suml + (int64_t)nk * s_seg[k - 1].end;
       }
     }
 
@@ -570,8 +598,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
     // ---- completion transition, segment by segment ---------------------------
     for (int k = 0; k < kmax; ++k) {
-      const int32_t delta = J.seg_delta[k];
-      const int32_t rk = J.seg_end[k];
+      const int32_t delta = s_seg[k].delta;
+      const int32_t rk = s_seg[k].end;
       const uint32_t x = s_svc[k][tx] + 1u;
       s_svc[k][tx] = x;
       NRec *rc = recs(k);

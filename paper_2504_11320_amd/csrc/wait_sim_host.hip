@@ -270,6 +270,8 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
   }
   d.ring_stride = off;
+  // ring offsets inside a replica block are kept as 32-bit values on the device
+  if (off >= (1ull << 32)) return fail(WS_EUNSUPPORTED, at + "record rings exceed 4 GiB per replica");
   return WS_OK;
 }
 
