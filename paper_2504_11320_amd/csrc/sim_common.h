@@ -295,6 +295,17 @@ struct NRec {   // Nested WAIT boundary / interior record, 32 bytes
   uint32_t next;// calendar-bucket link
 };
 
+// Orders LDS accesses between the lanes of one wavefront.  The simulation
+// kernels run one wavefront per workgroup, and a wavefront's LDS operations
+// complete in issue order, so a compiler barrier with wavefront-scope fences
+// suffices; a workgroup barrier would also wait for every outstanding global
+// store of the wavefront.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Opaque copy: stops the compiler from turning a chain of selects over the
 // elements of a register array back into a dynamically indexed access (which
 // would move the array to scratch memory).

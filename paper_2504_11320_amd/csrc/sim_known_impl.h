@@ -432,7 +432,7 @@ sim_known_kernel(KArgs A) {
           s_req_lane[rk] = (uint32_t)tx;
           s_req_k[rk] = gend[j];
         }
-        __syncthreads();
+        wave_lds_sync();
         const int total = p * GU;
         for (int base = 0; base < total; base += nact) {
           const int w = base + wrank;
@@ -443,7 +443,7 @@ sim_known_kernel(KArgs A) {
                 draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lam[j], nullptr, 0, nullptr);
           }
         }
-        __syncthreads();
+        wave_lds_sync();
         if (room) gend[j] += GU;
       }
     }

@@ -419,7 +419,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           s_req_lane[rk] = (uint32_t)tx;
           s_req_k[rk] = ge;
         }
-        __syncthreads();
+        wave_lds_sync();
         const int total = p * GU;
         const double lamj = J.lambda[j];
         const uint32_t *row = row_of(j);
@@ -433,7 +433,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             s_glen[j][k % GR][ln] = Lj;
           }
         }
-        __syncthreads();
+        wave_lds_sync();
         if (room) s_gend[j][tx] = ge + GU;
       }
     }
