@@ -273,7 +273,7 @@ sim_known_kernel(KArgs A) {
     const bool first = !full && tq == h;
     place_if(qpu, j, first, a_ft);
     qsrc |= (first ? 1u : 0u) << j;
-    if (!full) ((double *)(blk + pick(qoff, j)))[tq & qmask] = a_ft;
+    ((double *)(blk + pick(qoff, j)))[tq & qmask] = a_ft;  // see evict
     place(qt, j, tq + 1u);
   };
   auto push_fcfs = [&](double a_ft, int32_t j, int32_t L) __attribute__((always_inline)) {
@@ -353,7 +353,9 @@ sim_known_kernel(KArgs A) {
       const bool first = !full && tq2 == h;
       qpu[j] = first ? a_ft : qpu[j];
       qsrc |= (first ? 1u : 0u) << j;
-      if (!full) qring(j)[tq2 & qmask] = a_ft;
+      // unconditional (no branch): a full queue ends the replica at its next
+      // decision and its ring is not read again
+      qring(j)[tq2 & qmask] = a_ft;
       qt[j] = tq2 + 1u;
     } else {
       push_fcfs(a_ft, j, lp[j]);
