@@ -77,6 +77,7 @@ typedef enum { WS_WAIT = 0, WS_NESTED_WAIT = 1, WS_FCFS = 2 } ws_policy_kind;
 
 /* Limits of the library. */
 #define WS_MAX_TYPES 16
+#define WS_MAX_TYPES_KNOWN 8  /* WAIT and FCFS: more types give WS_EUNSUPPORTED */
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255
 

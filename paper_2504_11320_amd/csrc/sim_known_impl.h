@@ -37,7 +37,7 @@
 namespace wsim {
 namespace {
 
-// MT: type slots (>= m); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
+// MT: type slots (>= m, at most 8); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
 // launch replays an arrival list; LN: replicas per wavefront (lanes LN..63
 // are padding), which sizes the per-lane LDS arrays.
 template <int MT, int POL, bool TRACE, int LN>
@@ -696,7 +696,7 @@ hipError_t launch_pol(int max_m, const KArgs &A, hipStream_t s) {
   if (max_m <= 3) return launch_mt<3, POL>(A, s);
   if (max_m <= 4) return launch_mt<4, POL>(A, s);
   if (max_m <= 8) return launch_mt<8, POL>(A, s);
-  return launch_mt<16, POL>(A, s);
+  return hipErrorInvalidValue;  // the host admits at most WS_MAX_TYPES_KNOWN types
 }
 
 }  // namespace

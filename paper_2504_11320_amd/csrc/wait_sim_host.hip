@@ -160,6 +160,9 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
   }
   int64_t reserve_tok = 0;
+  if (p.kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
+    return fail(WS_EUNSUPPORTED, at + "WAIT and FCFS take at most " +
+                                     std::to_string(WS_MAX_TYPES_KNOWN) + " request types");
   if (p.kind == WS_WAIT) {
     if (!known) return fail(WS_EINVAL, at + "WAIT needs known output lengths");
     if (!p.n) return fail(WS_EINVAL, at + "thresholds required");

@@ -69,3 +69,26 @@ def test_fcfs_reserve_validation():
     fc = [j for j in jobs if j.wl.policy == "fcfs"][:1]
     fc[0].wl.reserve = 1.0
     assert _err(fc).code == B.WS_EINVAL
+
+
+def test_type_limits():
+    """WAIT and FCFS take at most 8 request types (more: WS_EUNSUPPORTED);
+    Nested WAIT takes up to 16; more than 16 is invalid everywhere."""
+    from paper_2504_11320_amd import binding as B
+
+    def model(m, policy):
+        kw = dict(prompt_len=[16] * m, lam=[0.01] * m, d0=5.0, d1=0.01, C=4096,
+                  policy=policy, hist_edges=W.default_edges(5.0, 50))
+        if policy == "nested":
+            cap = 32
+            kw.update(n=[1, 1], out_cap=cap, seg_end=[8, cap],
+                      out_cdf=np.stack([W.geometric_cdf_table(8.0, cap)] * m))
+        else:
+            kw.update(out_len=[8] * m, n=[1] * m if policy == "wait" else [])
+        return [W.Job(W.Workload(**kw), 0, W.ids(2))]
+
+    for policy in ("wait", "fcfs"):
+        assert B.workspace_bytes(B.JobArray(model(8, policy))) > 0
+        assert _err(model(9, policy)).code == B.WS_EUNSUPPORTED
+    assert B.workspace_bytes(B.JobArray(model(16, "nested"))) > 0
+    assert _err(model(17, "nested")).code == B.WS_EINVAL

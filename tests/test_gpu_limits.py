@@ -1,0 +1,83 @@
+"""GPU parity at the library's size limits and across wavefront layouts.
+
+* Maximum model sizes against the oracle: 8 request types for WAIT and FCFS,
+  16 types and 16 segments for Nested WAIT, 255 histogram edges.
+* Launches large enough that the host packs 16, 32 or 64 replicas per
+  wavefront: a replica's outputs depend only on (model, policy, seed,
+  replica id, horizon), so the same replicas run alone (8 per wavefront) must
+  give bit-identical results.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from tests.gpu_util import check, sim_module
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B():
+    return sim_module()
+
+
+def _types(rng, m):
+    l = [int(x) for x in rng.integers(4, 200, m)]
+    lam = [float(x) for x in rng.uniform(0.002, 0.02, m)]
+    return l, lam
+
+
+def test_eight_types_wait_and_fcfs(B):
+    rng = np.random.default_rng(16)
+    l, lam = _types(rng, 8)
+    lp = [int(x) for x in rng.integers(1, 64, 8)]
+    C = 4 * max(a + b for a, b in zip(l, lp)) * 4
+    edges = W.default_edges(5.0, 255)
+    wait = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="wait",
+                      n=[int(x) for x in rng.integers(1, 4, 8)], out_len=lp,
+                      hist_edges=edges, record_capacity=1 << 12)
+    fcfs = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="fcfs", n=[],
+                      out_len=lp, reserve=0.01, hist_edges=edges, record_capacity=1 << 12)
+    jobs = [W.Job(wait, 11, W.ids(37)), W.Job(fcfs, 12, W.ids(29, start=500))]
+    check(B, jobs, 1200, "8 types, WAIT and FCFS, 255 edges")
+
+
+def test_sixteen_segments_nested(B):
+    rng = np.random.default_rng(1616)
+    l, lam = _types(rng, 16)
+    cap = 64
+    seg_end = list(range(4, 65, 4))            # 16 segments
+    cdf = np.stack([W.geometric_cdf_table(float(rng.uniform(3.0, 40.0)), cap)
+                    for _ in range(16)])
+    n = [int(x) for x in rng.integers(1, 3, 16)]
+    wl = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=8000, policy="nested", n=n,
+                    out_cap=cap, out_cdf=cdf, seg_end=seg_end,
+                    hist_edges=W.default_edges(5.0, 255), record_capacity=1 << 12)
+    check(B, [W.Job(wl, 5, W.ids(41))], 1000, "nested, 16 types x 16 segments")
+
+
+def _subset_equal(B, jobs, horizon, picks, ctx):
+    big = B.run_batch(jobs, horizon)
+    starts = np.cumsum([0] + [j.n for j in jobs])
+    small_jobs = [W.Job(jobs[ji].wl, jobs[ji].seed,
+                        np.asarray(jobs[ji].replica_ids[a:b], dtype=np.uint32))
+                  for ji, a, b in picks]
+    small = B.run_batch(small_jobs, horizon)
+    idx = np.concatenate([np.arange(starts[ji] + a, starts[ji] + b) for ji, a, b in picks])
+    for k in big:
+        assert np.array_equal(big[k][idx], small[k]), (ctx, k)
+    print(f"[gpu] {ctx}: {len(idx)} replicas identical to a separate launch", flush=True)
+
+
+@pytest.mark.parametrize("reps", [512, 1024, 2048])   # 16, 32, 64 per wavefront
+def test_wait_layouts_agree(B, reps):
+    jobs = W.config2(replicas=reps)
+    _subset_equal(B, jobs, 400, [(0, 0, 33), (17, reps - 40, reps), (31, 5, 9)],
+                  f"WAIT, {32 * reps} replicas")
+
+
+@pytest.mark.parametrize("reps", [512, 1024])         # 16, 32 per wavefront
+def test_nested_layouts_agree(B, reps):
+    jobs = W.config3(replicas=reps)
+    _subset_equal(B, jobs, 300, [(0, 0, 33), (20, reps - 40, reps)],
+                  f"Nested WAIT, {32 * reps} replicas")
