@@ -139,6 +139,15 @@ def test_edge_cases(sim):
     wl5 = [j for j in W.config4(replicas=1, grid=1, n_rates=4) if j.wl.policy == "fcfs"][2].wl
     wl5.reserve = 0.01
     _check(sim, [W.Job(wl5, 3, W.ids(33))], 2000, "fcfs reserve 1%")
+    # a job with no replicas between two others; one replica per job
+    base = W.config2(replicas=1, rate_index=[7])[0].wl
+    empty = W.Job(base, 0, W.ids(0))
+    res, _ = _check(sim, [W.Job(base, 0, W.ids(1)), empty, W.Job(wl5, 3, W.ids(1, start=9))],
+                    1500, "empty job, single replicas")
+    assert len(res["batches"]) == 2
+    # no replicas at all is invalid
+    with pytest.raises(sim.WaitSimError):
+        sim.run_batch([empty], 10)
 
 
 def test_histogram_edge_sets(sim):
