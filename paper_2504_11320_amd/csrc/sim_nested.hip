@@ -46,6 +46,57 @@ struct SegConst {
   uint32_t off_v;
 };
 
+__device__ __forceinline__ NRec nrec_of(uint4 a, uint4 b) {
+  NRec r;
+  r.a_ft = __longlong_as_double((long long)(((uint64_t)a.y << 32) | a.x));
+  r.kb = a.z;
+  r.kp = a.w;
+  r.j = (int32_t)b.x;
+  r.L = (int32_t)b.y;
+  r.c = b.z;
+  r.next = b.w;
+  return r;
+}
+__device__ __forceinline__ uint4 nrec_lo(const NRec &r) {
+  const uint64_t u = (uint64_t)__double_as_longlong(r.a_ft);
+  return make_uint4((uint32_t)u, (uint32_t)(u >> 32), r.kb, r.kp);
+}
+__device__ __forceinline__ uint4 nrec_hi(const NRec &r) {
+  return make_uint4((uint32_t)r.j, (uint32_t)r.L, r.c, r.next);
+}
+__device__ __forceinline__ QRec qrec_of(uint4 a) {
+  QRec q;
+  q.a_ft = __longlong_as_double((long long)(((uint64_t)a.y << 32) | a.x));
+  q.j = (int32_t)a.z;
+  q.L = (int32_t)a.w;
+  return q;
+}
+__device__ __forceinline__ uint4 qrec_u4(const QRec &q) {
+  const uint64_t u = (uint64_t)__double_as_longlong(q.a_ft);
+  return make_uint4((uint32_t)u, (uint32_t)(u >> 32), (uint32_t)q.j, (uint32_t)q.L);
+}
+// Asynchronous copy of 4 or 16 bytes per lane from HBM into LDS: lane t
+// writes lds_base + t * size, so lds_base is the start of a per-lane array
+// (and must be the same for all lanes).
+__device__ __forceinline__ void copy4_to_lds(const void *src, void *lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 4, 0,
+                                   0);
+}
+__device__ __forceinline__ void copy16_to_lds(const void *src, void *lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 16, 0,
+                                   0);
+}
+__device__ __forceinline__ uint4 opaque4(uint4 v) {
+  v.x = opaque(v.x);
+  v.y = opaque(v.y);
+  v.z = opaque(v.z);
+  v.w = opaque(v.w);
+  return v;
+}
+// Wait for every outstanding memory operation of the wavefront (including the
+// asynchronous copies); also a compiler barrier for memory accesses.
+__device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // MT: type slots (>= m); LT: segment slots (>= L); LN: replicas per
 // wavefront (lanes LN..63 are padding), which sizes the per-lane LDS columns.
 template <int MT, int LT, int LN>
@@ -53,7 +104,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // Inter-arrival gaps and output lengths are drawn ahead of use by the
   // whole wavefront at once into a ring of GR draws per type and lane; a
   // lane whose ring runs dry draws for itself.
-  constexpr int GR = MT <= 4 ? 8 : 4;
+  constexpr int GR = 4;
   constexpr int GU = GR / 2;         // draws added per refill
   constexpr uint32_t kLow = GU / 2;  // a lane below this triggers a refill
   __shared__ double s_tnext[MT][LN];
@@ -72,6 +123,16 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // a scan when next needed).  LIFO selections then read no HBM.
   __shared__ NRec s_vb[LT][LN], s_yi[LT][LN];
   __shared__ uint32_t s_yidx[LT][LN];
+  // Prefetch landing slots, one per lane, filled by asynchronous copies from
+  // HBM (global_load_lds) issued at the end of an iteration and waited for at
+  // the start of the next: the head of Q_{1,0}; per segment that can launch
+  // next, the front of its boundary queue, the first record of the next
+  // launch's terminal cohort slot and the head of the calendar bucket served
+  // next.  32-byte records land as two 16-byte halves.
+  __shared__ uint4 s_q0[LN];
+  __shared__ uint4 s_vfa[LT][LN], s_vfb[LT][LN];
+  __shared__ uint4 s_tra[LT][LN], s_trb[LT][LN];
+  __shared__ uint32_t s_bh[LT][LN];
   // per lane and segment: the entering cohort's accounting, formed at launch
   __shared__ int32_t s_eB[LT][LN], s_eM[LT][LN];
   __shared__ uint32_t s_eI[LT][LN];
@@ -257,6 +318,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       rec.j = j;
       rec.L = Lr;
       q10[qt & qmask] = rec;
+      if (qt == qh) s_q0[tx] = qrec_u4(rec);  // the new head
     }
     qt++;
   };
@@ -397,7 +459,37 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return evict_interior(kbest, ibest);
   };
 
+  // Stage A of the prefetch (end of an iteration): everything the next
+  // launch and completion read first.  Slot indices are masked into their
+  // rings, so a slot past a queue's tail reads a stale record that is never
+  // used (a push into the empty queue writes the landing slot instead).
+  // A segment k >= 1 can be in the next launch only if its boundary queue
+  // already holds n_k prompts (boundary queues change only in the completion
+  // step); only those segments are prefetched.
+  auto may_launch = [&](int k) __attribute__((always_inline)) {
+    return k == 0 || (int32_t)(s_vt[k][tx] - s_vh[k][tx]) >= s_seg[k].n;
+  };
+  auto prefetch_a = [&]() __attribute__((always_inline)) {
+    copy16_to_lds(q10 + (qh & qmask), &s_q0[0]);
+    for (int k = 0; k < L; ++k) {
+      if (!may_launch(k)) continue;
+      const int32_t delta = s_seg[k].delta;
+      const uint32_t x = s_svc[k][tx] + 1u;  // the segment's next service
+      copy4_to_lds(bkts(k) + x % (uint32_t)delta, &s_bh[k][0]);
+      if (k >= 1) {
+        const NRec *f = vring(k) + (s_vh[k][tx] & vmask(k));
+        copy16_to_lds(f, &s_vfa[k][0]);
+        copy16_to_lds((const uint8_t *)f + 16, &s_vfb[k][0]);
+      }
+      if (s_seg[k].n == 1) {
+        const NRec *tr = recs(k) + (x - (uint32_t)(delta - 1)) % (uint32_t)delta;
+        copy16_to_lds(tr, &s_tra[k][0]);
+        copy16_to_lds((const uint8_t *)tr + 16, &s_trb[k][0]);
+      }
+    }
+  };
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
+  if (!stopped) prefetch_a();
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- refill the draw rings, all active lanes together -----------------
@@ -438,6 +530,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       }
     }
 
+    wait_memory();  // stage A has landed
+
     // ---- decision: largest prefix of segments meeting their thresholds -----
     int kmax = 0;
     for (;;) {
@@ -473,6 +567,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
     if (stopped) break;
 
+
     // ---- launch: entering cohorts, calendar links, batch tokens -----------
     const uint32_t bidx = (uint32_t)batches;
     int64_t tokens = 0, prefill_l = 0, mplus = Mres;
@@ -494,7 +589,15 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       for (int32_t i = nk - 1; i >= 0; --i) {
         NRec e;
         if (k == 0) {
-          const QRec qr = q10[(qh + (uint32_t)i) & qmask];
+          QRec qr;
+          if (i == 0) {
+            qr = qrec_of(s_q0[tx]);  // the head, prefetched
+          } else {
+            qr = q10[(qh + (uint32_t)i) & qmask];
+            qr.a_ft = opaque(qr.a_ft);  // waited for inside this branch
+            qr.j = opaque(qr.j);
+            qr.L = opaque(qr.L);
+          }
           e.a_ft = qr.a_ft;
           e.j = qr.j;
           e.L = qr.L;
@@ -504,14 +607,25 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           prefill_l += s_l[qr.j];
           if (!has_ft(qr.a_ft)) pend_new++;
         } else {
-          e = vring(k)[(s_vh[k][tx] + (uint32_t)i) & vmask(k)];
+          if (i == 0) {
+            e = nrec_of(s_vfa[k][tx], s_vfb[k][tx]);  // the front, prefetched
+          } else {
+            const NRec *src = vring(k) + ((s_vh[k][tx] + (uint32_t)i) & vmask(k));
+            const uint4 lo = opaque4(*(const uint4 *)src), hi = opaque4(((const uint4 *)src)[1]);
+            e = nrec_of(lo, hi);
+          }
           tokens += (int64_t)s_l[e.j] + s_seg[k - 1].end + 1;
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
         const uint32_t b = (x + (uint32_t)(pexit - ent)) % (uint32_t)delta;
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
-        e.next = bk[b];
+        if (b == slot) {  // exits at this very service: heads the bucket served now
+          e.next = s_bh[k][tx];
+          s_bh[k][tx] = idx;
+        } else {
+          e.next = bk[b];
+        }
         bk[b] = idx;
         rc[idx] = e;
         if (i == nk - 1) {  // the cohort's last record is the segment's youngest
@@ -540,11 +654,17 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         if ((int64_t)x - (delta - 1) >= 1) {
           // the terminal cohort slot: its prompts still in the segment
           const uint32_t ts = (x - (uint32_t)(delta - 1)) % (uint32_t)delta;
-          for (int32_t i = 0; i < nk; ++i) {
-            const NRec tr = rc[ts * (uint32_t)nk + (uint32_t)i];
-            const bool live = tr.L != 0;
-            T += live ? 1u : 0u;
-            Tl += live ? (uint32_t)s_l[tr.j] : 0u;
+          if (nk == 1) {  // prefetched
+            const int32_t trL = (int32_t)s_trb[k][tx].y, trj = (int32_t)s_trb[k][tx].x;
+            T = trL != 0 ? 1u : 0u;
+            Tl = trL != 0 ? (uint32_t)s_l[trj] : 0u;
+          } else {
+            for (int32_t i = 0; i < nk; ++i) {
+              const NRec tr = rc[ts * (uint32_t)nk + (uint32_t)i];
+              const bool live = tr.L != 0;
+              T += live ? 1u : 0u;
+              Tl += live ? (uint32_t)s_l[tr.j] : 0u;
+            }
           }
         }
         mplus += (int64_t)s_I[k][tx] - T;
@@ -617,10 +737,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       }
       Ik += s_eI[k][tx];
       Mk += s_eM[k][tx];
-      // prompts whose exit is at this service
+      // prompts whose exit is at this service: the bucket's head was
+      // prefetched, the list's records are read on demand
       uint32_t *bk = bkts(k);
       const uint32_t b = x % (uint32_t)delta;
-      uint32_t idx = bk[b];
+      uint32_t idx = s_bh[k][tx];
       bk[b] = kNil;
       while (idx != kNil) {
         const NRec rec = rc[idx];
@@ -648,6 +769,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             const uint32_t vt = s_vt[h][tx];
             if (vt - s_vh[h][tx] <= vmask(h)) {
               vring(h)[vt & vmask(h)] = v;
+              if (vt == s_vh[h][tx]) {  // pushed into an empty queue: its front
+                s_vfa[h][tx] = nrec_lo(v);
+                s_vfb[h][tx] = nrec_hi(v);
+              }
               s_vt[h][tx] = vt + 1u;
               s_vb[h][tx] = v;
             } else {
@@ -672,7 +797,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
     batches++;
     btok += tokens;
+    prefetch_a();
   }
+  // no asynchronous copy may still target this workgroup's LDS when it ends
+  wait_memory();
 
   // ---- save state ------------------------------------------------------------
   put_f(A, S_T, r, t);
