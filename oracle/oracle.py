@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "wait_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
-POLICY = {"wait": 0, "nested": 1, "fcfs": 2}
+POLICY = {"wait": 0, "nested": 1, "fcfs": 2, "wait-nowait": 3}
 FLAG_CAPACITY, FLAG_STALL, FLAG_OVERFLOW = 1, 2, 4
 
 INT_FIELDS = ["batches", "arrivals", "completions", "completed_tokens",

@@ -13,7 +13,11 @@
  *     tau = d0 + d1 * sum_{i in batch}(l_i + s_i), memory constraint
  *     eq. (memory_constraint) over GPU-resident prompts, LIFO eviction with
  *     restart from prefill, censored latency / TTFT metrics (Section 2.4);
- *   - WAIT: Algorithm 1 (Section 4.2);
+ *   - WAIT: Algorithm 1 (Section 4.2), and its threshold-only variant
+ *     WAIT-no-wait (appendix, threshold without waiting): a type is served
+ *     whenever it has a waiting or resident prompt, admitting at most n_j
+ *     waiting prompts, so the per-stage upper bound n_j is kept but service
+ *     never waits for a full cohort;
  *   - Nested WAIT: Algorithm 2 (Section 5.1) in the event-driven form of
  *     Algorithm 4 (Appendix B.1), with coarse segments (Appendix A, segment
  *     design);
@@ -48,6 +52,10 @@
 #include <pthread.h>
 #include <stdlib.h>
 #include <string.h>
+
+static int is_wait(const or_config *c) {
+  return c->policy == OR_WAIT || c->policy == OR_WAIT_NOWAIT;
+}
 
 /* ------------------------------------------------------------------ RNG -- */
 
@@ -320,7 +328,7 @@ static double peek_arrival(const sim_t *S, int32_t *jout) {
 
 static void push_queue(sim_t *S, int64_t r) {
   const or_config *c = S->cfg;
-  int32_t qi = (c->policy == OR_WAIT) ? S->R[r].j : 0;
+  int32_t qi = is_wait(c) ? S->R[r].j : 0;
   if (S->q[qi].len >= c->record_capacity) S->out->flags |= OR_FLAG_CAPACITY;
   S->R[r].loc = LOC_QUEUE;
   dq_push(&S->q[qi], r);
@@ -397,14 +405,24 @@ static void select_by_stage(sim_t *S, int64_t lo, int64_t hi, int32_t cap,
  * every stage s select min(n_j, n_js).  Returns 1 if a batch was formed. */
 static int decide_wait(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   const or_config *c = S->cfg;
+  const int nowait = c->policy == OR_WAIT_NOWAIT;
+  /* residents per type (WAIT-no-wait also serves a type that has residents
+   * and nothing waiting) */
+  int64_t nres[c->m];
+  int elig[c->m];
+  for (int32_t j = 0; j < c->m; j++) nres[j] = 0;
+  for (int64_t i = 0; i < S->res.len; i++) nres[S->R[S->res.v[i]].j]++;
   int any = 0;
-  for (int32_t j = 0; j < c->m; j++)
-    if (S->q[j].len >= c->n[j]) any = 1;
+  for (int32_t j = 0; j < c->m; j++) {
+    elig[j] = nowait ? (S->q[j].len > 0 || nres[j] > 0) : (S->q[j].len >= c->n[j]);
+    if (elig[j]) any = 1;
+  }
   if (!any) return 0;
   int64_t p = 0;
   for (int32_t j = 0; j < c->m; j++) {
-    if (S->q[j].len < c->n[j]) continue;
-    for (int32_t i = 0; i < c->n[j]; i++) {
+    if (!elig[j]) continue;
+    const int64_t admit = nowait ? (S->q[j].len < c->n[j] ? S->q[j].len : c->n[j]) : c->n[j];
+    for (int64_t i = 0; i < admit; i++) {
       int64_t r = dq_pop_front(&S->q[j]);
       S->R[r].kb = S->b;
       S->R[r].kp = p++;
@@ -725,7 +743,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
   S.out = out;
   S.hist = hist;
   S.rlog = rlog;
-  S.nq = (c->policy == OR_WAIT) ? c->m : 1;
+  S.nq = is_wait(c) ? c->m : 1;
   S.q = (dq_t *)calloc((size_t)S.nq, sizeof(dq_t));
   S.bnd = (dq_t *)calloc((size_t)(c->policy == OR_NESTED ? c->nseg + 2 : 1),
                          sizeof(dq_t));
@@ -753,7 +771,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
       tokens = 0;
       prefill_l = 0;
       int got;
-      if (c->policy == OR_WAIT)
+      if (is_wait(c))
         got = decide_wait(&S, &tokens, &prefill_l);
       else if (c->policy == OR_FCFS)
         got = decide_fcfs(&S, &tokens, &prefill_l);

@@ -25,6 +25,7 @@ extern "C" {
 #define OR_WAIT 0
 #define OR_NESTED 1
 #define OR_FCFS 2
+#define OR_WAIT_NOWAIT 3 /* WAIT's thresholds without waiting (appendix) */
 
 #define OR_FLAG_CAPACITY 1u
 #define OR_FLAG_STALL 2u
@@ -46,7 +47,7 @@ typedef struct {
   const int32_t *tr_type;   /* trace mode: types [n_trace]                     */
   const int32_t *tr_L;      /* trace mode: output lengths [n_trace] or NULL    */
   int64_t n_trace;
-  int32_t policy;           /* OR_WAIT / OR_NESTED / OR_FCFS                   */
+  int32_t policy;           /* OR_WAIT / OR_NESTED / OR_FCFS / OR_WAIT_NOWAIT  */
   const int32_t *n;         /* thresholds: WAIT [m], NESTED [nseg]             */
   int32_t nseg;             /* NESTED: number of segments                      */
   const int32_t *seg_end;   /* NESTED: r_1 < ... < r_nseg                      */

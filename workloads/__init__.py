@@ -32,7 +32,7 @@ class Workload:
     d0: float                        # ms per iteration
     d1: float                        # ms per cached token
     C: int                           # KV budget, tokens
-    policy: str                      # "wait" | "nested" | "fcfs"
+    policy: str                      # "wait" | "wait-nowait" | "nested" | "fcfs"
     n: List[int]                     # thresholds (WAIT: per type, Nested: per segment)
     out_len: Optional[List[int]] = None     # known output lengths, or None
     out_cap: int = 0                         # distribution mode: cap
