@@ -119,9 +119,19 @@ def _workloads():
         "nested-heavytail": ("Nested WAIT, 10 lognormal-decile prompt types, lognormal "
                              "outputs capped at 4096, 6 segments, 8192 replicas",
                              lambda reps: W.config5(), 1000000, "nested", [0]),
+        "nowait-llama": ("WAIT-no-wait (thresholds 1, 1, 1) on the Llama-2-7B-shaped "
+                         "3-type mix, 32 rates 0.5-1.2x fluid boundary, 1024 replicas each",
+                         lambda reps: _nowait(W.config2(replicas=reps)), 100000,
+                         "wait-nowait", [0, 31]),
         "wait-small": ("WAIT, 2 types (16/8, 32/16), C = 2048, 64 replicas",
                        lambda reps: W.config1(), 10000, "wait", [0]),
     }
+
+
+def _nowait(jobs):
+    for j in jobs:
+        j.wl.policy = "wait-nowait"
+    return jobs
 
 
 def cpu_baseline(jobs, pick, horizon: int, replicas: int, threads: int) -> dict:
@@ -152,7 +162,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="wait-llama",
                     help="wait-llama (the benchmark), nested-geometric, wait-sweep, "
-                         "nested-heavytail, wait-small")
+                         "nested-heavytail, nowait-llama, wait-small")
     ap.add_argument("--horizon", type=int, default=0, help="batches (0: the workload's)")
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")

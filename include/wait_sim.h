@@ -66,7 +66,14 @@ typedef enum {
   WS_EUNSUPPORTED = -5 /* valid model, but outside the library's limits  */
 } ws_status;
 
-typedef enum { WS_WAIT = 0, WS_NESTED_WAIT = 1, WS_FCFS = 2 } ws_policy_kind;
+typedef enum {
+  WS_WAIT = 0,         /* Algorithm 1                                          */
+  WS_NESTED_WAIT = 1,  /* Algorithm 2 / Algorithm 4                            */
+  WS_FCFS = 2,         /* greedy FCFS, LIFO eviction on overflow (Section 4.1) */
+  WS_WAIT_NOWAIT = 3   /* WAIT's thresholds without waiting (appendix): a type
+                          is served whenever it has a waiting or resident
+                          prompt, admitting at most n_j waiting prompts      */
+} ws_policy_kind;
 
 /* Per-replica flags (result field "flags"). */
 #define WS_FLAG_CAPACITY 1u /* an external queue exceeded record_capacity;

@@ -17,10 +17,11 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libwait_sim.so")
 
 WS_OK, WS_EINVAL, WS_ENOMEM, WS_EDEVICE, WS_EWORKSPACE, WS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
-WS_WAIT, WS_NESTED_WAIT, WS_FCFS = 0, 1, 2
+WS_WAIT, WS_NESTED_WAIT, WS_FCFS, WS_WAIT_NOWAIT = 0, 1, 2, 3
 WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW = 1, 2, 4
 WS_NI64, WS_NF64 = 12, 6
-POLICY = {"wait": WS_WAIT, "nested": WS_NESTED_WAIT, "fcfs": WS_FCFS}
+POLICY = {"wait": WS_WAIT, "nested": WS_NESTED_WAIT, "fcfs": WS_FCFS,
+          "wait-nowait": WS_WAIT_NOWAIT}
 
 I64_FIELDS = ["batches", "arrivals", "completions", "completed_tokens",
               "evictions", "evicted_tokens", "fallback_evictions",

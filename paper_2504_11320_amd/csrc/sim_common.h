@@ -22,6 +22,7 @@ constexpr uint32_t kNil = 0xFFFFFFFFu;
 struct JobDev {
   int32_t m, policy, n_hist, out_cap;
   int32_t nseg, known, qcap_log2, rec_cap;
+  int32_t nowait, pad_;  // WAIT: serve without waiting for a full cohort
   double d0, d1;
   int64_t C, reserve_tok;
   int64_t n_trace;

@@ -93,6 +93,9 @@ sim_known_kernel(KArgs A) {
   s_seed[tx] = seed;
   s_rid[tx] = rid;
   const bool trace = TRACE && J->n_trace > 0;  // compiled out of the common kernel
+  // WAIT-no-wait: a type is served whenever it has a waiting or resident
+  // prompt and admits at most n_j waiting ones (job-uniform)
+  const bool nowait = WAIT && J->nowait != 0;
   const int64_t n_trace = J->n_trace;
   const double *tr_time = (const double *)(A.ws + J->off_tr_time);
   const int32_t *tr_type = (const int32_t *)(A.ws + J->off_tr_type);
@@ -476,7 +479,9 @@ sim_known_kernel(KArgs A) {
       if (WAIT) {
 #pragma unroll
         for (int j = 0; j < MT; ++j)
-          if (j < m && (qt[j] - qh[j]) >= (uint32_t)nth[j]) elig |= 1u << j;
+          if (j < m && (nowait ? (qt[j] != qh[j] || dt[j] != dh[j])
+                               : (qt[j] - qh[j]) >= (uint32_t)nth[j]))
+            elig |= 1u << j;
       } else {
         uint32_t resident = 0;
 #pragma unroll
@@ -520,7 +525,10 @@ sim_known_kernel(KArgs A) {
       for (int j = 0; j < MT; ++j) {
         if (!(elig & (1u << j))) continue;
         const uint32_t c = svc[j] + 1u;
-        for (int x = 0; x < nth[j]; ++x) {
+        // admissions: n_j (WAIT), at most n_j of those waiting (no-wait)
+        const uint32_t waiting = qt[j] - qh[j];
+        const int32_t na = nowait && waiting < (uint32_t)nth[j] ? (int32_t)waiting : nth[j];
+        for (int x = 0; x < na; ++x) {
           const double a_ft = ((qsrc >> j) & 1u) ? qpu[j] : qld[j];
           qsrc &= ~(1u << j);
           qh[j]++;
@@ -528,9 +536,9 @@ sim_known_kernel(KArgs A) {
           dpush(j, a_ft, bidx, c);
           pendnew[j] += has_ft(a_ft) ? 0u : 1u;
         }
-        fresh[j] = (uint32_t)nth[j];
-        tokens += (int64_t)nth[j] * l[j] + Mj[j];
-        prefill_l += (int64_t)nth[j] * l[j];
+        fresh[j] = (uint32_t)na;
+        tokens += (int64_t)na * l[j] + Mj[j];
+        prefill_l += (int64_t)na * l[j];
       }
     } else {
       tokens = Mres;

@@ -94,6 +94,11 @@ struct Layout {
   int32_t max_seg = 0;
 };
 
+// The launch (kernel family and replica list) a policy runs in.
+int launch_kind(const ws_policy *p) {
+  return p->kind == WS_WAIT_NOWAIT ? (int)WS_WAIT : (int)p->kind;
+}
+
 int validate_job(const ws_job &jb, int idx, JobHost &H) {
   const std::string at = "job " + std::to_string(idx) + ": ";
   if (!jb.cfg || !jb.pol) return fail(WS_EINVAL, at + "cfg and pol must be non-NULL");
@@ -101,6 +106,8 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   if (jb.n > 0 && !jb.streams) return fail(WS_EINVAL, at + "streams must be non-NULL");
   const ws_config &c = *jb.cfg;
   const ws_policy &p = *jb.pol;
+  // WAIT-no-wait runs on the WAIT kernel with a flag
+  const int kind = p.kind == WS_WAIT_NOWAIT ? (int)WS_WAIT : (int)p.kind;
   if (c.m < 1 || c.m > WS_MAX_TYPES)
     return fail(WS_EINVAL, at + "m must be in 1.." + std::to_string(WS_MAX_TYPES));
   if (!c.prompt_len || !c.lambda) return fail(WS_EINVAL, at + "prompt_len and lambda required");
@@ -160,15 +167,15 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
   }
   int64_t reserve_tok = 0;
-  if (p.kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
+  if (kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
     return fail(WS_EUNSUPPORTED, at + "WAIT and FCFS take at most " +
                                      std::to_string(WS_MAX_TYPES_KNOWN) + " request types");
-  if (p.kind == WS_WAIT) {
+  if (kind == WS_WAIT) {
     if (!known) return fail(WS_EINVAL, at + "WAIT needs known output lengths");
     if (!p.n) return fail(WS_EINVAL, at + "thresholds required");
     for (int j = 0; j < c.m; ++j)
       if (p.n[j] < 1) return fail(WS_EINVAL, at + "thresholds must be >= 1");
-  } else if (p.kind == WS_FCFS) {
+  } else if (kind == WS_FCFS) {
     if (!(p.fcfs_reserve >= 0.0 && p.fcfs_reserve < 1.0))
       return fail(WS_EINVAL, at + "fcfs_reserve must be in [0,1)");
     reserve_tok = (int64_t)std::ceil(p.fcfs_reserve * (double)c.C);
@@ -176,7 +183,7 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
       if (c.prompt_len[j] > c.C - reserve_tok)
         return fail(WS_EINVAL, at + "a prompt does not fit below the FCFS reserve");
     if (!known) return fail(WS_EUNSUPPORTED, at + "FCFS with unknown lengths is not supported");
-  } else if (p.kind == WS_NESTED_WAIT) {
+  } else if (kind == WS_NESTED_WAIT) {
     if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail(WS_EINVAL, at + "L out of range");
     if (!p.n || !p.seg_end) return fail(WS_EINVAL, at + "thresholds and seg_end required");
     for (int k = 0; k < p.L; ++k) {
@@ -198,10 +205,11 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   JobDev &d = H.d;
   std::memset(&d, 0, sizeof(d));
   d.m = c.m;
-  d.policy = p.kind;
+  d.policy = kind;
+  d.nowait = p.kind == WS_WAIT_NOWAIT ? 1 : 0;
   d.n_hist = c.n_hist;
   d.out_cap = c.out_cap;
-  d.nseg = p.kind == WS_NESTED_WAIT ? p.L : 0;
+  d.nseg = kind == WS_NESTED_WAIT ? p.L : 0;
   d.known = known ? 1 : 0;
   d.qcap_log2 = ceil_log2((uint64_t)c.record_capacity);
   d.rec_cap = c.record_capacity;
@@ -214,16 +222,16 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     d.l[j] = c.prompt_len[j];
     d.lp[j] = known ? c.out_len[j] : c.out_cap;
     d.lambda[j] = c.lambda[j];
-    d.n[j] = (p.kind == WS_WAIT) ? p.n[j] : 0;
+    d.n[j] = (kind == WS_WAIT) ? p.n[j] : 0;
     uint64_t dcap;
-    if (p.kind == WS_WAIT)  // launch holds <= (l'_j + 1) n_j records
+    if (kind == WS_WAIT)  // launch holds <= (l'_j + 1) n_j records
       dcap = (uint64_t)(c.out_len[j] + 1) * (uint64_t)p.n[j];
     else                    // residents of type j charge >= l_j each
       dcap = (uint64_t)(c.C / c.prompt_len[j]) + 2;
-    if (p.kind == WS_NESTED_WAIT) dcap = 2;
+    if (kind == WS_NESTED_WAIT) dcap = 2;
     d.dcap_log2[j] = ceil_log2(std::max<uint64_t>(dcap, 2));
   }
-  if (p.kind == WS_NESTED_WAIT) {
+  if (kind == WS_NESTED_WAIT) {
     int32_t lmin = c.prompt_len[0];
     for (int j = 1; j < c.m; ++j) lmin = std::min(lmin, c.prompt_len[j]);
     for (int k = 0; k < p.L; ++k) {
@@ -248,13 +256,13 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   H.trace_bytes = c.n_trace > 0 ? align_up(16ull * (uint64_t)c.n_trace, 256) : 0;
   // ring block of one replica
   uint64_t off = 0;
-  const uint64_t qrec = (p.kind == WS_WAIT) ? 8 : 16;
-  const int nq = (p.kind == WS_WAIT) ? c.m : 1;
+  const uint64_t qrec = (kind == WS_WAIT) ? 8 : 16;
+  const int nq = (kind == WS_WAIT) ? c.m : 1;
   for (int j = 0; j < nq; ++j) {
     d.off_q[j] = off;
     off += align_up(qrec << d.qcap_log2, 256);
   }
-  if (p.kind == WS_NESTED_WAIT) {
+  if (kind == WS_NESTED_WAIT) {
     for (int k = 0; k < p.L; ++k) {
       const uint64_t slots = (uint64_t)d.seg_delta[k];
       d.off_rec[k] = off;
@@ -290,7 +298,7 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     Lo.jobs[i].d.replica_begin = R;
     R += jobs[i].n;
     hmax = std::max(hmax, jobs[i].cfg->n_hist + 1);
-    const int pk = jobs[i].pol->kind;
+    const int pk = launch_kind(jobs[i].pol);
     Lo.max_m[pk] = std::max(Lo.max_m[pk], jobs[i].cfg->m);
     if (pk == WS_NESTED_WAIT) Lo.max_seg = std::max(Lo.max_seg, jobs[i].pol->L);
   }
@@ -299,15 +307,15 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
       // each job starts a new wavefront: its constants are wavefront-uniform
       int64_t w = 0;
       for (int i = 0; i < n_jobs; ++i)
-        if (jobs[i].pol->kind == pk) w += (jobs[i].n + lanes - 1) / lanes;
+        if (launch_kind(jobs[i].pol) == pk) w += (jobs[i].n + lanes - 1) / lanes;
       return w;
     };
     bool any_trace = false;
     for (int i = 0; i < n_jobs; ++i)
-      any_trace |= jobs[i].pol->kind == pk && jobs[i].cfg->n_trace > 0;
+      any_trace |= launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_trace > 0;
     int32_t nmax = 0;  // largest job: no wavefront needs more lanes
     for (int i = 0; i < n_jobs; ++i)
-      if (jobs[i].pol->kind == pk) nmax = std::max(nmax, jobs[i].n);
+      if (launch_kind(jobs[i].pol) == pk) nmax = std::max(nmax, jobs[i].n);
     // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32
     int lanes = pk == WS_NESTED_WAIT ? 32 : 64;
     if (!any_trace || pk == WS_NESTED_WAIT) {  // known-length replays keep 64
@@ -448,14 +456,14 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
   std::vector<int32_t> lists[3];
   for (int i = 0; i < n_jobs; ++i) {
     const ws_job &jb = jobs[i];
-    std::vector<int32_t> &list = lists[jb.pol->kind];
+    std::vector<int32_t> &list = lists[launch_kind(jb.pol)];
     for (int x = 0; x < jb.n; ++x, ++r) {
       std::memcpy(img.data() + Lo.off_seed + 8 * r, &jb.streams[x].seed, 8);
       std::memcpy(img.data() + Lo.off_rid + 4 * r, &jb.streams[x].replica_id, 4);
       const uint32_t ji = (uint32_t)i;
       std::memcpy(img.data() + Lo.off_job_of + 4 * r, &ji, 4);
       list.push_back((int32_t)r);
-      if (list.size() % 64 == (size_t)Lo.lanes[jb.pol->kind])
+      if (list.size() % 64 == (size_t)Lo.lanes[launch_kind(jb.pol)])
         while (list.size() % 64 != 0) list.push_back(-1);
     }
     while (list.size() % 64 != 0) list.push_back(-1);
@@ -502,7 +510,7 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     B.lanes = Lo.lanes[pk];
     B.any_trace = 0;
     for (int i = 0; i < n_jobs; ++i)
-      if (jobs[i].pol->kind == pk && jobs[i].cfg->n_trace > 0) B.any_trace = 1;
+      if (launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_trace > 0) B.any_trace = 1;
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)
       e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, s);
