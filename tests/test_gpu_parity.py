@@ -190,3 +190,20 @@ def test_config2_full_size_sampled(sim):
     gsub = {k: v[idx] for k, v in g.items()}
     st = compare(gsub, o, "config2 full-size sample")
     print(f"[gpu] config2 full size sample ok, bit-exact fp64 {st}", flush=True)
+
+
+def test_rate_sweep_stability_point(sim):
+    """The Llama-shaped WAIT sweep read with the analysis helpers: completion
+    rates follow the arrival rates at low load and fall behind past the
+    stability point, which lies inside the swept span (0.5-1.2 Lambda*)."""
+    from paper_2504_11320_amd import analysis as A
+    jobs = W.config2(replicas=64, n_rates=8)
+    res = sim.run_batch(jobs, 20000)
+    s = A.summarize(res)
+    means = A.job_means(s["completion_rate"], [j.n for j in jobs])
+    rates = [sum(j.wl.lam) for j in jobs]
+    comp = [m for m, _ in means]
+    lam_hat = A.lambda_hat(rates, comp, tol=0.05)
+    print(f"[gpu] sweep: lambda_hat / Lambda* = {lam_hat / W.LAM_STAR_C2:.3f}", flush=True)
+    assert rates[0] <= lam_hat < rates[-1]
+    assert comp[0] >= 0.95 * rates[0] and comp[-1] < 0.95 * rates[-1]
