@@ -18,7 +18,7 @@ SRC = os.path.join(HERE, "wait_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 POLICY = {"wait": 0, "nested": 1, "fcfs": 2, "wait-nowait": 3}
-FLAG_CAPACITY, FLAG_STALL, FLAG_OVERFLOW = 1, 2, 4
+FLAG_CAPACITY, FLAG_STALL, FLAG_OVERFLOW, FLAG_THIN_LIMIT = 1, 2, 4, 8
 
 INT_FIELDS = ["batches", "arrivals", "completions", "completed_tokens",
               "evictions", "evicted_tokens", "fallback_evictions",
@@ -38,6 +38,7 @@ class _Config(C.Structure):
         ("tr_type", C.c_void_p), ("tr_L", C.c_void_p), ("n_trace", C.c_int64),
         ("policy", C.c_int32), ("n", C.c_void_p), ("nseg", C.c_int32),
         ("seg_end", C.c_void_p), ("reserve", C.c_double),
+        ("n_rate_pts", C.c_int32), ("rate_t", C.c_void_p), ("rate_f", C.c_void_p),
     ]
 
 
@@ -90,6 +91,10 @@ def lib():
         L.oracle_uniform.restype = C.c_double
         L.oracle_ln.argtypes = [C.c_double]
         L.oracle_ln.restype = C.c_double
+        L.oracle_arrival_times.argtypes = [C.POINTER(_Config), C.c_uint64,
+                                           C.c_uint32, C.c_int32, C.c_int64,
+                                           C.c_void_p, C.c_void_p, C.c_void_p]
+        L.oracle_arrival_times.restype = C.c_int
         L.oracle_draw.argtypes = [C.c_uint64, C.c_uint32, C.c_int32, C.c_uint32,
                                   C.c_double, C.c_void_p, C.c_int32,
                                   C.POINTER(C.c_double), C.POINTER(C.c_int32)]
@@ -143,6 +148,13 @@ class _Pinned:
         else:
             c.seg_end, c.nseg = None, 0
         c.reserve = float(wl.reserve)
+        if getattr(wl, "rate_t", None) is not None:
+            rt = arr(wl.rate_t, np.float64)
+            rf = arr(np.asarray(wl.rate_f, dtype=np.float64).reshape(wl.m, len(rt)),
+                     np.float64)
+            c.n_rate_pts, c.rate_t, c.rate_f = len(rt), _ptr(rt), _ptr(rf)
+        else:
+            c.n_rate_pts, c.rate_t, c.rate_f = 0, None, None
         self.cfg = c
 
 
@@ -239,3 +251,16 @@ def draw(seed: int, replica_id: int, j: int, k: int, lam: float,
     L.oracle_draw(C.c_uint64(seed), replica_id, j, k, lam, _ptr(row), out_cap,
                   C.byref(g), C.byref(Lout))
     return g.value, Lout.value
+
+
+def arrival_times(wl, seed: int, replica_id: int, j: int, n: int):
+    """First n arrival times of type j (inf once it has stopped), their output
+    lengths and Philox counters, and the result flags."""
+    L = lib()
+    pin = _Pinned(wl)
+    t = np.zeros(n, dtype=np.float64)
+    Ls = np.zeros(n, dtype=np.int32)
+    k = np.zeros(n, dtype=np.uint32)
+    fl = L.oracle_arrival_times(C.byref(pin.cfg), C.c_uint64(seed), replica_id, j, n,
+                                t.ctypes.data, Ls.ctypes.data, k.ctypes.data)
+    return t, Ls, k, fl

@@ -38,6 +38,17 @@
  *   horizon counts batches; arrivals at t <= t_end are handled before the
  *   decision at t_end.
  *
+ * Time-varying arrivals (appendix, time-varying rates: independent
+ * nonhomogeneous Poisson processes with continuous bounded intensities):
+ * intensity lambda_j f_j(t), f_j piecewise linear through the profile points
+ * and constant outside them, sampled by thinning (Lewis and Shedler, 1979):
+ * candidates of the Poisson process at rate lambda_j max f_j drawn as above
+ * (counter k = candidate index), candidate k kept when w3 max f_j < f_j(t_k)
+ * 2^32 (w3 the candidate's fourth Philox word), its output length from its
+ * w2.  A candidate inside a stretch where f_j is zero moves the clock to the
+ * stretch's end; a type whose intensity is zero from the last point on, or
+ * that rejects 2^20 candidates in a row (flagged), has no further arrivals.
+ *
  * Randomness: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11) keyed by the
  * 64-bit seed, counter (k, type, replica, 0) for the k-th arrival of a type.
  * Uniform u = (2x+1) 2^-53 from 52 bits of (w0, w1); gap = -ln(u)/lambda with
@@ -123,6 +134,23 @@ double oracle_ln(double u) {
   double lnf = (z + z) * p;
   double de = (double)e;
   return de * OR_LN2_HI + (de * OR_LN2_LO + lnf);
+}
+
+void oracle_draw_w3(uint64_t seed, uint32_t replica_id, int32_t type, uint32_t k,
+                    double lambda, const uint32_t *cdf_row, int32_t out_cap,
+                    double *gap, int32_t *L, uint32_t *w3) {
+  uint32_t ctr[4] = {k, (uint32_t)type, replica_id, 0u};
+  uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  uint32_t w[4];
+  oracle_philox4x32_10(ctr, key, w);
+  double u = oracle_uniform(w[0], w[1]);
+  *gap = -oracle_ln(u) / lambda;
+  if (cdf_row != NULL && L != NULL) {
+    int32_t s = 1;
+    while (s < out_cap && !(w[2] < cdf_row[s - 1])) s++;
+    *L = s;
+  }
+  *w3 = w[3];
 }
 
 void oracle_draw(uint64_t seed, uint32_t replica_id, int32_t type, uint32_t k,
@@ -296,16 +324,111 @@ static int64_t charge(const sim_t *S, const req_t *r) {
 
 /* -------------------------------------------------------- arrivals ---- */
 
+/* Rate profile of type j (time-varying rates): factors f_j at the points
+ * rate_t[0..P-1], row j of rate_f.  seg_of gives -1 before the first point,
+ * P-1 from the last point on, else the i with rate_t[i] <= t < rate_t[i+1]. */
+static int32_t seg_of(const or_config *c, double t) {
+  const int32_t P = c->n_rate_pts;
+  if (t < c->rate_t[0]) return -1;
+  if (!(t < c->rate_t[P - 1])) return P - 1;
+  int32_t i = 0;
+  while (!(t < c->rate_t[i + 1])) i++;
+  return i;
+}
+
+/* f_j(t): constant outside the points, linear between them. */
+static double rate_factor(const or_config *c, int32_t j, int32_t i, double t) {
+  const int32_t P = c->n_rate_pts;
+  const double *f = c->rate_f + (size_t)j * (size_t)P;
+  if (i < 0) return f[0];
+  if (i == P - 1) return f[P - 1];
+  const double frac = (t - c->rate_t[i]) / (c->rate_t[i + 1] - c->rate_t[i]);
+  return f[i] + (f[i + 1] - f[i]) * frac;
+}
+
 static void draw_next(sim_t *S, int32_t j) {
   const or_config *c = S->cfg;
   double gap = 0.0;
   int32_t L = 0;
   const uint32_t *row =
       (c->lp == NULL) ? c->cdf + (size_t)j * (size_t)(c->out_cap - 1) : NULL;
-  oracle_draw(S->seed, S->rid, j, S->k_next[j], c->lambda[j], row, c->out_cap,
-              &gap, &L);
-  S->t_next[j] = S->t_next[j] + gap;
+  if (c->n_rate_pts == 0) {
+    oracle_draw(S->seed, S->rid, j, S->k_next[j], c->lambda[j], row, c->out_cap,
+                &gap, &L);
+    S->t_next[j] = S->t_next[j] + gap;
+    S->L_next[j] = (c->lp != NULL) ? c->lp[j] : L;
+    return;
+  }
+  /* Thinning: candidates of a Poisson process at the bound lambda_j f_max,
+   * candidate k kept with probability f_j(t_k) / f_max.  A candidate inside a
+   * stretch where f_j is zero moves the clock to the end of that stretch. */
+  const int32_t P = c->n_rate_pts;
+  const double *f = c->rate_f + (size_t)j * (size_t)P;
+  double fmax = f[0];
+  for (int32_t i = 1; i < P; i++)
+    if (f[i] > fmax) fmax = f[i];
+  if (!(fmax > 0.0)) {
+    S->t_next[j] = INFINITY;
+    return;
+  }
+  const double lam_c = c->lambda[j] * fmax;
+  for (uint32_t tries = 0;; tries++) {
+    uint32_t w3 = 0;
+    oracle_draw_w3(S->seed, S->rid, j, S->k_next[j], lam_c, row, c->out_cap, &gap,
+                   &L, &w3);
+    const double tc = S->t_next[j] + gap;
+    const int32_t i = seg_of(c, tc);
+    if ((double)w3 * fmax < rate_factor(c, j, i, tc) * 4294967296.0) {
+      S->t_next[j] = tc; /* accepted */
+      break;
+    }
+    if (tries + 1 >= OR_THIN_MAX) {
+      S->out->flags |= OR_FLAG_THIN_LIMIT;
+      S->t_next[j] = INFINITY;
+      return;
+    }
+    if (i == P - 1 && f[P - 1] == 0.0) {
+      S->t_next[j] = INFINITY; /* zero intensity from here on */
+      return;
+    }
+    if (i < 0 && f[0] == 0.0)
+      S->t_next[j] = c->rate_t[0];
+    else if (i >= 0 && f[i] == 0.0 && f[i + 1] == 0.0)
+      S->t_next[j] = c->rate_t[i + 1];
+    else
+      S->t_next[j] = tc;
+    S->k_next[j]++;
+  }
   S->L_next[j] = (c->lp != NULL) ? c->lp[j] : L;
+}
+
+int oracle_arrival_times(const or_config *cfg, uint64_t seed, uint32_t replica_id,
+                         int32_t type, int64_t n, double *t, int32_t *L,
+                         uint32_t *k) {
+  sim_t S;
+  or_result out;
+  memset(&S, 0, sizeof(S));
+  memset(&out, 0, sizeof(out));
+  S.cfg = cfg;
+  S.seed = seed;
+  S.rid = replica_id;
+  S.out = &out;
+  S.t_next = (double *)calloc((size_t)cfg->m, sizeof(double));
+  S.L_next = (int32_t *)calloc((size_t)cfg->m, sizeof(int32_t));
+  S.k_next = (uint32_t *)calloc((size_t)cfg->m, sizeof(uint32_t));
+  draw_next(&S, type);
+  for (int64_t a = 0; a < n; a++) {
+    t[a] = S.t_next[type];
+    if (L) L[a] = S.L_next[type];
+    if (k) k[a] = S.k_next[type];
+    if (!(S.t_next[type] < INFINITY)) continue;
+    S.k_next[type]++;
+    draw_next(&S, type);
+  }
+  free(S.t_next);
+  free(S.L_next);
+  free(S.k_next);
+  return (int)out.flags;
 }
 
 /* Time and type of the next exogenous arrival (ties: lowest type). */

@@ -30,6 +30,8 @@ extern "C" {
 #define OR_FLAG_CAPACITY 1u
 #define OR_FLAG_STALL 2u
 #define OR_FLAG_OVERFLOW 4u
+#define OR_FLAG_THIN_LIMIT 8u /* 2^20 thinning rejections in a row */
+#define OR_THIN_MAX (1u << 20)
 
 typedef struct {
   int32_t m;                /* request types                                   */
@@ -52,6 +54,13 @@ typedef struct {
   int32_t nseg;             /* NESTED: number of segments                      */
   const int32_t *seg_end;   /* NESTED: r_1 < ... < r_nseg                      */
   double reserve;           /* FCFS: admission reserve fraction of C           */
+  /* time-varying arrivals (appendix, time-varying rates): intensity of type j
+   * is lambda_j f_j(t), f_j piecewise linear through (rate_t[i],
+   * rate_f[j * n_rate_pts + i]) and constant outside; n_rate_pts = 0 for
+   * constant rates */
+  int32_t n_rate_pts;
+  const double *rate_t;
+  const double *rate_f;
 } or_config;
 
 typedef struct {
@@ -92,6 +101,14 @@ void oracle_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
                           uint32_t out[4]);
 double oracle_uniform(uint32_t w0, uint32_t w1);
 double oracle_ln(double u);
+/* First n arrival times (INFINITY once the type has stopped), output lengths
+ * and Philox counters of one type's arrival process; returns result flags. */
+int oracle_arrival_times(const or_config *cfg, uint64_t seed, uint32_t replica_id,
+                         int32_t type, int64_t n, double *t, int32_t *L,
+                         uint32_t *k);
+void oracle_draw_w3(uint64_t seed, uint32_t replica_id, int32_t type, uint32_t k,
+                    double lambda, const uint32_t *cdf_row, int32_t out_cap,
+                    double *gap, int32_t *L, uint32_t *w3);
 void oracle_draw(uint64_t seed, uint32_t replica_id, int32_t type,
                  uint32_t k, double lambda, const uint32_t *cdf_row,
                  int32_t out_cap, double *gap, int32_t *L);

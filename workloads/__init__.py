@@ -42,6 +42,10 @@ class Workload:
     hist_edges: Optional[np.ndarray] = None  # latency histogram edges (ms)
     record_capacity: int = 1 << 15           # external-queue capacity
     trace: Optional[tuple] = None            # (times f64, types i32, lengths i32)
+    # time-varying rates: type j arrives at lam[j] * f_j(t), f_j piecewise
+    # linear through (rate_t[i], rate_f[j][i]) and constant outside
+    rate_t: Optional[np.ndarray] = None      # f64 [P], strictly increasing
+    rate_f: Optional[np.ndarray] = None      # f64 [m, P], >= 0
 
     @property
     def m(self) -> int:
