@@ -47,19 +47,26 @@ KERNEL_SRCS = [os.path.join(CSRC, f)
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_wait_3type_32x1024x1e5_hbm.md")
 
 
-def op_model(m: int, cdf_cap: int = 0) -> dict:
+def op_model(m: int, cdf_cap: int = 0, rate_pts: int = 0, cand_per_arrival: float = 1.0) -> dict:
     """Algorithmic lane-operations per event (full-rate VALU instruction
     equivalents; a 32x32->64-bit multiply counts 4).  cdf_cap > 1: output
     lengths are drawn from a CDF table of that many entries (a search of
-    2 ops per halving step)."""
+    2 ops per halving step).  rate_pts > 0: time-varying rates sampled by
+    thinning, cand_per_arrival candidates drawn per arrival, each tested
+    against the profile (a search over its points, one interpolation)."""
     philox = 10 * (2 * 4 + 4 + 2)     # 2 wide multiplies, 4 xor, 2 key adds per round
     uniform = 10                      # 52-bit assembly, int->fp64, scale
     ln = 50                           # reduction, one fp64 division, 12-term Horner, e*ln2
     gap = 14                          # fp64 division by lambda, add to the clock
     book = 12                         # queue push, counters, area terms
     cdf = 2 * max(0, int(cdf_cap - 1).bit_length()) if cdf_cap > 1 else 0
+    cand = philox + uniform + ln + gap + cdf
+    if rate_pts > 0:
+        # search (compare, select per halving step), fp64 division and
+        # interpolation, w3 * fmax and the comparison, zero-stretch tests
+        cand += 3 * max(1, int(rate_pts - 1).bit_length()) + 14 + 4 + 6
     return {
-        "arrival": philox + uniform + ln + gap + book + 2 * m + cdf,
+        "arrival": cand_per_arrival * cand + book + 2 * m,
         "batch": 24 + 6 * m,          # eligibility, tokens, tau, clock, areas, peak
         "completion": 35,             # latency, sum, histogram search and update
         "eviction": 14 + 3 * m,       # LIFO choice, stage, memory, re-queue
@@ -67,8 +74,30 @@ def op_model(m: int, cdf_cap: int = 0) -> dict:
     }
 
 
-def algorithmic_ops(res: dict, m: int, cdf_cap: int = 0) -> float:
-    c = op_model(m, cdf_cap)
+def candidates_per_arrival(jobs) -> float:
+    """Thinning draws lam_j max f_j candidates per unit time for lam_j f_j
+    arrivals: the ratio of the bound to the profile's mean over its span,
+    weighted by the rates (1 for constant rates)."""
+    import numpy as np
+    bound = mean = 0.0
+    for j in jobs:
+        wl = j.wl
+        for k in range(wl.m):
+            if wl.rate_t is None or len(wl.rate_t) < 2:
+                bound += wl.lam[k] * j.n
+                mean += wl.lam[k] * j.n
+                continue
+            f = np.asarray(wl.rate_f, dtype=np.float64).reshape(wl.m, -1)[k]
+            t = np.asarray(wl.rate_t, dtype=np.float64)
+            fbar = float(np.sum(np.diff(t) * (f[1:] + f[:-1]) / 2.0) / (t[-1] - t[0]))
+            bound += wl.lam[k] * f.max() * j.n
+            mean += wl.lam[k] * fbar * j.n
+    return bound / mean if mean > 0 else 1.0
+
+
+def algorithmic_ops(res: dict, m: int, cdf_cap: int = 0, rate_pts: int = 0,
+                    cand_per_arrival: float = 1.0) -> float:
+    c = op_model(m, cdf_cap, rate_pts, cand_per_arrival)
     return float(c["batch"] * res["batches"].sum() + c["arrival"] * res["arrivals"].sum()
                  + c["completion"] * res["completions"].sum()
                  + c["eviction"] * res["evictions"].sum() + c["idle"] * res["idle_waits"].sum())
@@ -123,6 +152,10 @@ def _workloads():
                          "3-type mix, 32 rates 0.5-1.2x fluid boundary, 1024 replicas each",
                          lambda reps: _nowait(W.config2(replicas=reps)), 100000,
                          "wait-nowait", [0, 31]),
+        "wait-cyclic": ("WAIT on the Llama-2-7B-shaped 3-type mix with cyclic "
+                        "time-varying rates lam_j (1 + 0.5 sin(4 pi t / 8e8 ms + 2 pi j / 3)), "
+                        "32 rates 0.5-1.2x fluid boundary, 1024 replicas each",
+                        lambda reps: W.config_cyclic(replicas=reps), 100000, "wait", [0, 31]),
         "wait-small": ("WAIT, 2 types (16/8, 32/16), C = 2048, 64 replicas",
                        lambda reps: W.config1(), 10000, "wait", [0]),
     }
@@ -162,7 +195,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="wait-llama",
                     help="wait-llama (the benchmark), nested-geometric, wait-sweep, "
-                         "nested-heavytail, nowait-llama, wait-small")
+                         "nested-heavytail, nowait-llama, wait-cyclic, wait-small")
     ap.add_argument("--horizon", type=int, default=0, help="batches (0: the workload's)")
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -208,6 +241,8 @@ def main() -> int:
     jobs = build(args.replicas)
     m = max(j.wl.m for j in jobs)
     cdf_cap = max((j.wl.out_cap for j in jobs if j.wl.out_cdf is not None), default=0)
+    rate_pts = max((len(j.wl.rate_t) for j in jobs if j.wl.rate_t is not None), default=0)
+    cpa = candidates_per_arrival(jobs)
     sim = B.Simulation(jobs)
     sim.prepare()
     stream = torch.cuda.current_stream()
@@ -233,7 +268,7 @@ def main() -> int:
         print("bench.py: some replicas stopped early (flags set)", file=sys.stderr)
     value = rep_its / (ms_step / 1e3)
 
-    ops = algorithmic_ops(res, m, cdf_cap)
+    ops = algorithmic_ops(res, m, cdf_cap, rate_pts, cpa)
     achieved = ops / (ms_step / 1e3)
     traffic = traffic_from_profile() if args.workload == "wait-llama" else None
     roofline = {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK,
@@ -248,7 +283,9 @@ def main() -> int:
                 "hbm_measured_frac": (traffic / (ms_step / 1e3) / HBM_PEAK
                                       if traffic is not None else None),
                 "kernel": (f"sim_nested_kernel ({m} types)" if policy == "nested"
-                           else f"sim_known_kernel ({policy}, {m} types)")}
+                           else f"sim_known_kernel ({policy}, {m} types)")
+                          + (f", time-varying rates ({rate_pts} points, "
+                             f"{cpa:.3f} candidates per arrival)" if rate_pts else "")}
 
     out = {"metric": METRIC, "value": value, "unit": UNIT, "n_gpus": 1,
            "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,

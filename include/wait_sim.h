@@ -6,9 +6,10 @@
  * Online Scheduling with Memory Constraints" (arXiv 2504.11320):
  *
  *   - m request types; type j arrives as a Poisson process of rate lambda_j
- *     (Section 2.1), has prompt length l_j and output length l'_j (known), or
- *     an output length drawn per request from a CDF table (unknown lengths,
- *     Section 5.1);
+ *     (Section 2.1), or of time-varying intensity lambda_j f_j(t) (appendix,
+ *     time-varying arrival rates), has prompt length l_j and output length
+ *     l'_j (known), or an output length drawn per request from a CDF table
+ *     (unknown lengths, Section 5.1);
  *   - a batch B takes tau(B) = d0 + d1 * sum_{i in B} (l_i + s_i) where s_i is
  *     the stage being processed, 0 for prefill (eq. time_consump, Section 2.2);
  *   - GPU-resident prompts hold KV cache l_i + s_i and the sum must stay
@@ -30,7 +31,16 @@
  * u = (2x+1) 2^-53 from x = (w0 << 20) | (w1 >> 12); inter-arrival gap
  * -ln(u)/lambda_j; unknown output length = smallest s in 1..cap-1 with
  * w2 < T_j[s], else cap.  A replica's arrival path therefore depends only on
- * (seed, replica_id, lambda), identical across policies and thresholds.
+ * (seed, replica_id, lambda, rate profile), identical across policies and
+ * thresholds.
+ *
+ * Time-varying intensities (ws_config.n_rate_pts > 0) are sampled by thinning
+ * (Lewis and Shedler, 1979): the draws above at the bound rate
+ * lambda_j * max f_j give candidate times; candidate k (counter k) is kept
+ * when w3 * max f_j < f_j(t_k) * 2^32 (w3 its fourth Philox word, the product
+ * in double), and its w2 gives the output length.  A candidate inside a
+ * stretch where f_j is zero moves the clock to the end of that stretch; a
+ * type whose f_j is zero from the last point on has no further arrivals.
  *
  * Memory ownership: every pointer in the config structs is HOST memory read
  * during the call only.  d_workspace and d_results are DEVICE memory owned by
@@ -55,7 +65,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 1
+#define WS_ABI_VERSION 2
 
 typedef enum {
   WS_OK = 0,
@@ -81,12 +91,15 @@ typedef enum {
 #define WS_FLAG_STALL 2u    /* nothing eligible and no further arrival       */
 #define WS_FLAG_OVERFLOW 4u /* Nested WAIT launched with a projected state
                                above C after every allowed eviction          */
+#define WS_FLAG_THIN_LIMIT 8u /* a time-varying type rejected 2^20 candidates
+                                 in a row; it has no further arrivals       */
 
 /* Limits of the library. */
 #define WS_MAX_TYPES 16
 #define WS_MAX_TYPES_KNOWN 8  /* WAIT and FCFS: more types give WS_EUNSUPPORTED */
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255
+#define WS_MAX_RATE_PTS 32
 
 /* The model (Section 2). */
 typedef struct {
@@ -112,6 +125,14 @@ typedef struct {
   const int32_t *trace_type;    /* type of each arrival            [n_trace] */
   const int32_t *trace_out_len; /* output length (distribution mode)        */
   int64_t n_trace;
+  /* Time-varying arrival rates (appendix, time-varying arrival rates): type
+     j arrives at intensity lambda_j * f_j(t), f_j linear between the points
+     (rate_t[i], rate_f[j * n_rate_pts + i]) and constant outside them.
+     n_rate_pts = 0: constant rates (rate_t, rate_f unused); otherwise
+     1..WS_MAX_RATE_PTS, no trace, lambda_j * max f_j finite.               */
+  int32_t n_rate_pts;
+  const double *rate_t;         /* strictly increasing, finite  [n_rate_pts] */
+  const double *rate_f;         /* finite, >= 0            [m][n_rate_pts]   */
 } ws_config;
 
 /* The scheduling policy. */

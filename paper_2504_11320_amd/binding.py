@@ -18,7 +18,8 @@ LIB_PATH = os.path.join(PKG, "libwait_sim.so")
 
 WS_OK, WS_EINVAL, WS_ENOMEM, WS_EDEVICE, WS_EWORKSPACE, WS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 WS_WAIT, WS_NESTED_WAIT, WS_FCFS, WS_WAIT_NOWAIT = 0, 1, 2, 3
-WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW = 1, 2, 4
+WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW, WS_FLAG_THIN_LIMIT = 1, 2, 4, 8
+WS_ABI_VERSION = 2
 WS_NI64, WS_NF64 = 12, 6
 POLICY = {"wait": WS_WAIT, "nested": WS_NESTED_WAIT, "fcfs": WS_FCFS,
           "wait-nowait": WS_WAIT_NOWAIT}
@@ -39,7 +40,8 @@ class WsConfig(C.Structure):
         ("C", C.c_int64), ("hist_edges", C.c_void_p), ("n_hist", C.c_int32),
         ("record_capacity", C.c_int32), ("trace_time", C.c_void_p),
         ("trace_type", C.c_void_p), ("trace_out_len", C.c_void_p),
-        ("n_trace", C.c_int64),
+        ("n_trace", C.c_int64), ("n_rate_pts", C.c_int32),
+        ("rate_t", C.c_void_p), ("rate_f", C.c_void_p),
     ]
 
 
@@ -89,6 +91,9 @@ def lib():
                                          C.c_size_t, C.c_void_p, C.c_size_t, C.c_void_p]
         L.wait_sim_last_error.restype = C.c_char_p
         L.wait_sim_abi_version.restype = C.c_int
+        if L.wait_sim_abi_version() != WS_ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {L.wait_sim_abi_version()}, "
+                               f"this binding needs {WS_ABI_VERSION}: rebuild it")
         _lib = L
     return _lib
 
@@ -133,6 +138,14 @@ class JobArray:
             else:
                 cfg.trace_time = cfg.trace_type = cfg.trace_out_len = None
                 cfg.n_trace = 0
+            if getattr(wl, "rate_t", None) is not None:
+                P = len(wl.rate_t)
+                cfg.n_rate_pts = P
+                cfg.rate_t = self._a(wl.rate_t, np.float64)
+                cfg.rate_f = self._a(np.asarray(wl.rate_f, dtype=np.float64).reshape(wl.m, P),
+                                     np.float64)
+            else:
+                cfg.n_rate_pts, cfg.rate_t, cfg.rate_f = 0, None, None
             pol = WsPolicy()
             pol.kind = POLICY[wl.policy]
             pol.n = self._a(wl.n if len(wl.n) else [0], np.int32)

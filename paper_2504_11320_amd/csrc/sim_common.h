@@ -16,20 +16,25 @@ constexpr int kMaxSeg = WS_MAX_SEGMENTS;
 constexpr uint32_t kFlagCap = WS_FLAG_CAPACITY;
 constexpr uint32_t kFlagStall = WS_FLAG_STALL;
 constexpr uint32_t kFlagOverflow = WS_FLAG_OVERFLOW;
+constexpr uint32_t kFlagThin = WS_FLAG_THIN_LIMIT;
+constexpr int kMaxRatePts = WS_MAX_RATE_PTS;
+constexpr uint32_t kThinMax = 1u << 20;  // thinning rejections in a row
 constexpr uint32_t kNil = 0xFFFFFFFFu;
 
 // One job (a model + policy shared by a group of replicas), in device memory.
 struct JobDev {
   int32_t m, policy, n_hist, out_cap;
   int32_t nseg, known, qcap_log2, rec_cap;
-  int32_t nowait, pad_;  // WAIT: serve without waiting for a full cohort
+  int32_t nowait;  // WAIT: serve without waiting for a full cohort
+  int32_t n_rate;  // rate-profile points (0: constant rates)
   double d0, d1;
   int64_t C, reserve_tok;
   int64_t n_trace;
   int64_t replica_begin;
   int32_t l[kMaxTypes], lp[kMaxTypes], n[kMaxTypes];
   int32_t dcap_log2[kMaxTypes];
-  double lambda[kMaxTypes];
+  double lambda[kMaxTypes];     // draw rate (the thinning bound with a profile)
+  double rate_fmax[kMaxTypes];  // max f_j of the rate profile
   // Nested WAIT segments (index k = 0..nseg-1 is the paper's segment k+1)
   int32_t seg_end[kMaxSeg];    // r_k
   int32_t seg_n[kMaxSeg];      // n_k
@@ -37,6 +42,7 @@ struct JobDev {
   int32_t seg_delta[kMaxSeg];  // number of processing stages (cohort slots)
   int32_t vcap_log2[kMaxSeg];  // boundary-queue ring size (k >= 1)
   uint64_t off_edges, off_cdf, off_tr_time, off_tr_type, off_tr_len;
+  uint64_t off_rate;  // rate profile: t [n_rate], then f [m][n_rate]
   uint64_t off_ring, ring_stride;
   uint64_t off_q[kMaxTypes];    // queue rings inside a replica block
   uint64_t off_d[kMaxTypes];    // resident deques inside a replica block
@@ -78,6 +84,7 @@ struct KArgs {
   int64_t horizon;
   int32_t resume;
   int32_t any_trace;   // some job of this launch replays a fixed arrival list
+  int32_t any_tv;      // some job of this launch has time-varying rates
   int32_t lanes;       // replicas per wavefront (lanes >= this are padding)
 };
 
@@ -156,9 +163,10 @@ __device__ __forceinline__ double ln_unit(double u) {
 __device__ __forceinline__ double draw_gap(uint64_t seed, uint32_t rid,
                                            uint32_t j, uint32_t k, double lam,
                                            const uint32_t *row, int32_t cap,
-                                           int32_t *L) {
+                                           int32_t *L, uint32_t *w3 = nullptr) {
   uint32_t w[4];
   philox10(k, j, rid, 0u, (uint32_t)seed, (uint32_t)(seed >> 32), w);
+  if (w3 != nullptr) *w3 = w[3];
   const uint64_t x = ((uint64_t)w[0] << 20) | (uint64_t)(w[1] >> 12);
   const double u = (double)(2 * x + 1) * 0x1p-53;
   if (row != nullptr) {
@@ -173,6 +181,79 @@ __device__ __forceinline__ double draw_gap(uint64_t seed, uint32_t rid,
     *L = lo;
   }
   return -ln_unit(u) / lam;
+}
+
+// ------------------------------------------------ time-varying rates --
+// A type with a rate profile arrives at intensity lambda_j f_j(t), f_j linear
+// between the points rt[0..P-1] and constant outside them.
+
+// The profile of one job as the kernels stage it in LDS: points, f_j at the
+// points (rows past m are zero) and max f_j.
+template <int MT, int NP>
+struct RateProfLds {
+  double t[NP];
+  double f[MT][NP];
+  double fmax[MT];
+};
+
+// -1 before the first point, P-1 from the last point on, else the i with
+// rt[i] <= t < rt[i+1] (rt strictly increasing).
+__device__ __forceinline__ int rate_seg(const double *rt, int P, double t) {
+  if (t < rt[0]) return -1;
+  if (!(t < rt[P - 1])) return P - 1;
+  int lo = 0, hi = P - 1;  // rt[lo] <= t < rt[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (t < rt[mid])
+      hi = mid;
+    else
+      lo = mid;
+  }
+  return lo;
+}
+
+// f(t) for t in piece i of rate_seg.
+__device__ __forceinline__ double rate_fac(const double *rt, const double *f, int P, int i,
+                                           double t) {
+  if (i < 0) return f[0];
+  if (i == P - 1) return f[P - 1];
+  const double frac = (t - rt[i]) / (rt[i + 1] - rt[i]);
+  return f[i] + (f[i + 1] - f[i]) * frac;
+}
+
+// Next arrival of a type with a rate profile, by thinning: starting from
+// candidate k (the clock at the previous candidate or arrival is t), draw
+// candidates of the Poisson process at the bound lam_c = lambda_j fmax and keep
+// the first with w3 fmax < f(t_k) 2^32.  Returns its time and leaves k at its
+// counter (and *L at its output length when a CDF row is given).  A candidate
+// inside a stretch where f is zero moves the clock to the stretch's end; a
+// zero intensity from the last point on, or kThinMax rejections in a row
+// (flagged), end the type's arrivals (time +inf).
+__device__ __forceinline__ double draw_thinned(uint64_t seed, uint32_t rid, uint32_t j,
+                                               uint32_t &k, double t, double lam_c,
+                                               double fmax, const double *rt,
+                                               const double *f, int P,
+                                               const uint32_t *row, int32_t cap,
+                                               int32_t *L, uint32_t &flags) {
+  if (!(fmax > 0.0)) return INFINITY;
+  for (uint32_t tries = 0;; ++tries) {
+    uint32_t w3;
+    const double tc = t + draw_gap(seed, rid, j, k, lam_c, row, cap, L, &w3);
+    const int i = rate_seg(rt, P, tc);
+    if ((double)w3 * fmax < rate_fac(rt, f, P, i, tc) * 4294967296.0) return tc;
+    if (tries + 1u >= kThinMax) {
+      flags |= kFlagThin;
+      return INFINITY;
+    }
+    if (i == P - 1 && f[P - 1] == 0.0) return INFINITY;
+    if (i < 0 && f[0] == 0.0)
+      t = rt[0];
+    else if (i >= 0 && i < P - 1 && f[i] == 0.0 && f[i + 1] == 0.0)
+      t = rt[i + 1];
+    else
+      t = tc;
+    ++k;
+  }
 }
 
 // Histogram bin of a latency: number of edges <= lat (edges strictly
@@ -347,5 +428,9 @@ __device__ __forceinline__ void place_if(T (&a)[MT], int j, bool c, T v) {
 hipError_t launch_known_wait(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_known_fcfs(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s);
+// the kernels for launches with time-varying rates or an arrival list
+hipError_t launch_known_wait_tv(int max_m, const KArgs &A, hipStream_t s);
+hipError_t launch_known_fcfs_tv(int max_m, const KArgs &A, hipStream_t s);
+hipError_t launch_nested_tv(int max_m, int max_seg, const KArgs &A, hipStream_t s);
 
 }  // namespace wsim

@@ -39,8 +39,9 @@ namespace {
 
 // MT: type slots (>= m, at most 8); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
 // launch replays an arrival list; LN: replicas per wavefront (lanes LN..63
-// are padding), which sizes the per-lane LDS arrays.
-template <int MT, int POL, bool TRACE, int LN>
+// are padding), which sizes the per-lane LDS arrays; TV: jobs with
+// time-varying rates are supported (compiled out of the common kernels).
+template <int MT, int POL, bool TRACE, int LN, bool TV>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 sim_known_kernel(KArgs A) {
   constexpr bool WAIT = POL == WS_WAIT;
@@ -53,7 +54,17 @@ sim_known_kernel(KArgs A) {
   __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
   __shared__ uint8_t s_htab[kHistTab];
   __shared__ int s_hsteps;
-  __shared__ double s_gap[MT][GR][LN];
+  // The gap rings, or for a job with time-varying intensities (whose lanes
+  // draw their own candidates) the rate profile in the same LDS.
+  __shared__ union {
+    double gap[MT][GR][LN];
+    RateProfLds<MT, TV ? kMaxRatePts : 1> prof;
+  } s_u;
+  double(&s_gap)[MT][GR][LN] = s_u.gap;
+  constexpr int NP = TV ? kMaxRatePts : 1;
+  double(&s_rt)[NP] = s_u.prof.t;
+  double(&s_rf)[MT][NP] = s_u.prof.f;
+  double(&s_fmax)[MT] = s_u.prof.fmax;
   __shared__ uint64_t s_seed[LN];
   __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   // The last WB records pushed on each resident deque are also kept in LDS,
@@ -76,13 +87,24 @@ sim_known_kernel(KArgs A) {
   const int32_t C = (int32_t)J->C;  // <= 2^30
   const int32_t cap_adm = (int32_t)(J->C - J->reserve_tok);
   const int n_hist = J->n_hist;
-  // the latency histogram's edges, searched at every completion, staged in
-  // LDS with their bucket index by all lanes of the block (one wavefront,
-  // one job)
+  const int P = TV ? J->n_rate : 0;  // rate-profile points, 0 for constant rates
+  const bool tv = TV && P > 0;
+  // the latency histogram's edges, searched at every completion, and the
+  // rate profile, staged in LDS (the edges with their bucket index) by all
+  // lanes of the block (one wavefront, one job)
   {
     const double *edges_g = (const double *)(A.ws + J->off_edges);
     for (int b = threadIdx.x; b <= n_hist; b += 64)
       s_edges[b] = b < n_hist ? edges_g[b] : INFINITY;
+    if (tv) {
+      const double *rg = (const double *)(A.ws + J->off_rate);
+      for (int i = threadIdx.x; i < P; i += 64) s_rt[i] = rg[i];
+      for (int x = threadIdx.x; x < MT * NP; x += 64) {
+        const int j = x / NP, i = x % NP;
+        s_rf[j][i] = j < m && i < P ? rg[P + j * P + i] : 0.0;
+      }
+      for (int j = threadIdx.x; j < MT; j += 64) s_fmax[j] = j < m ? J->rate_fmax[j] : 0.0;
+    }
     __syncthreads();
   }
   const HistIdx hidx = hist_index_build(s_edges, n_hist, s_htab, &s_hsteps);
@@ -163,8 +185,14 @@ sim_known_kernel(KArgs A) {
       kk[j] = qh[j] = qt[j] = dh[j] = dt[j] = svc[j] = pend[j] = 0;
       Mj[j] = 0;
       tnext[j] = INFINITY;
-      if (j < m && !trace)
+      if (j < m && !trace && tv) {
+        uint32_t k0 = 0;
+        tnext[j] = draw_thinned(seed, rid, (uint32_t)j, k0, 0.0, lam[j], s_fmax[j], s_rt, s_rf[j],
+                                P, nullptr, 0, nullptr, flags);
+        kk[j] = k0;
+      } else if (j < m && !trace) {
         tnext[j] = 0.0 + draw_gap(seed, rid, (uint32_t)j, 0u, lam[j], nullptr, 0, nullptr);
+      }
     }
     for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
   } else {
@@ -392,6 +420,12 @@ sim_known_kernel(KArgs A) {
   auto take = [&](int jn, double a) __attribute__((always_inline)) {
     if (trace) {
       tridx++;
+    } else if (tv) {  // thinning, drawn by the lane itself
+      uint32_t k = pick(kk, jn) + 1u;
+      const double tn = draw_thinned(seed, rid, (uint32_t)jn, k, pick(tnext, jn), pick(lam, jn),
+                                     s_fmax[jn], s_rt, s_rf[jn], P, nullptr, 0, nullptr, flags);
+      place(kk, jn, k);
+      place(tnext, jn, tn);
     } else {
       const uint32_t k = pick(kk, jn) + 1u;
       place(kk, jn, k);
@@ -418,7 +452,7 @@ sim_known_kernel(KArgs A) {
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- refill the gap rings, all active lanes together ----------------
-    if (!TRACE) {
+    if (!TRACE && !tv) {
       const uint64_t act = __ballot(1);
       const int nact = __popcll(act);
       const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
@@ -677,33 +711,35 @@ sim_known_kernel(KArgs A) {
   }
 }
 
-template <int MT, int POL>
+template <int MT, int POL, bool TV>
 hipError_t launch_mt(const KArgs &A, hipStream_t s) {
   const int blocks = (A.n_list + 63) / 64;
   const dim3 g(blocks), b(64);
-  if (A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
+  if (TV && A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
     if (A.lanes != 64) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64, TV>), g, b, 0, s, A);
+  } else if (A.any_trace) {
+    return hipErrorInvalidValue;  // replays run on the TV kernels
   } else if (A.lanes == 64) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64, TV>), g, b, 0, s, A);
   } else if (A.lanes == 32) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 32>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 32, TV>), g, b, 0, s, A);
   } else if (A.lanes == 16) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 16>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 16, TV>), g, b, 0, s, A);
   } else if (A.lanes == 8) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 8>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 8, TV>), g, b, 0, s, A);
   } else {
     return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int POL>
+template <int POL, bool TV>
 hipError_t launch_pol(int max_m, const KArgs &A, hipStream_t s) {
-  if (max_m <= 2) return launch_mt<2, POL>(A, s);
-  if (max_m <= 3) return launch_mt<3, POL>(A, s);
-  if (max_m <= 4) return launch_mt<4, POL>(A, s);
-  if (max_m <= 8) return launch_mt<8, POL>(A, s);
+  if (max_m <= 2) return launch_mt<2, POL, TV>(A, s);
+  if (max_m <= 3) return launch_mt<3, POL, TV>(A, s);
+  if (max_m <= 4) return launch_mt<4, POL, TV>(A, s);
+  if (max_m <= 8) return launch_mt<8, POL, TV>(A, s);
   return hipErrorInvalidValue;  // the host admits at most WS_MAX_TYPES_KNOWN types
 }
 

@@ -77,7 +77,7 @@ uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 struct JobHost {
   JobDev d;
   int64_t reserve_tok;
-  uint64_t edges_bytes, cdf_bytes, trace_bytes;
+  uint64_t edges_bytes, cdf_bytes, trace_bytes, rate_bytes;
 };
 
 struct Layout {
@@ -166,6 +166,29 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
         return fail(WS_EINVAL, at + "trace output length out of range");
     }
   }
+  double fmax[WS_MAX_TYPES] = {};
+  if (c.n_rate_pts != 0) {
+    if (c.n_rate_pts < 0 || c.n_rate_pts > WS_MAX_RATE_PTS)
+      return fail(WS_EINVAL, at + "n_rate_pts must be in 0.." + std::to_string(WS_MAX_RATE_PTS));
+    if (c.n_trace > 0) return fail(WS_EINVAL, at + "a rate profile and a trace are exclusive");
+    if (!c.rate_t || !c.rate_f) return fail(WS_EINVAL, at + "rate_t and rate_f required");
+    const int P = c.n_rate_pts;
+    for (int i = 0; i < P; ++i) {
+      if (!std::isfinite(c.rate_t[i])) return fail(WS_EINVAL, at + "rate_t must be finite");
+      if (i > 0 && !(c.rate_t[i] > c.rate_t[i - 1]))
+        return fail(WS_EINVAL, at + "rate_t must be strictly increasing");
+    }
+    for (int j = 0; j < c.m; ++j) {
+      for (int i = 0; i < P; ++i) {
+        const double f = c.rate_f[(size_t)j * P + i];
+        if (!(f >= 0.0) || !std::isfinite(f))
+          return fail(WS_EINVAL, at + "rate_f must be finite and >= 0");
+        fmax[j] = std::max(fmax[j], f);
+      }
+      if (!std::isfinite(c.lambda[j] * fmax[j]))
+        return fail(WS_EINVAL, at + "lambda_j * max f_j must be finite");
+    }
+  }
   int64_t reserve_tok = 0;
   if (kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
     return fail(WS_EUNSUPPORTED, at + "WAIT and FCFS take at most " +
@@ -218,10 +241,13 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   d.C = c.C;
   d.reserve_tok = reserve_tok;
   d.n_trace = c.n_trace;
+  d.n_rate = c.n_rate_pts;
   for (int j = 0; j < c.m; ++j) {
     d.l[j] = c.prompt_len[j];
     d.lp[j] = known ? c.out_len[j] : c.out_cap;
-    d.lambda[j] = c.lambda[j];
+    // with a rate profile the draws run at the thinning bound lambda_j max f_j
+    d.lambda[j] = c.n_rate_pts > 0 ? c.lambda[j] * fmax[j] : c.lambda[j];
+    d.rate_fmax[j] = fmax[j];
     d.n[j] = (kind == WS_WAIT) ? p.n[j] : 0;
     uint64_t dcap;
     if (kind == WS_WAIT)  // launch holds <= (l'_j + 1) n_j records
@@ -254,6 +280,7 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
                     ? align_up(4ull * (uint64_t)c.m * (uint64_t)(c.out_cap - 1), 256)
                     : 0;
   H.trace_bytes = c.n_trace > 0 ? align_up(16ull * (uint64_t)c.n_trace, 256) : 0;
+  H.rate_bytes = align_up(8ull * (uint64_t)c.n_rate_pts * (uint64_t)(c.m + 1), 256);
   // ring block of one replica
   uint64_t off = 0;
   const uint64_t qrec = (kind == WS_WAIT) ? 8 : 16;
@@ -356,6 +383,8 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     H.d.off_tr_type = off + 8ull * (uint64_t)jobs[i].cfg->n_trace;
     H.d.off_tr_len = off + 12ull * (uint64_t)jobs[i].cfg->n_trace;
     off += H.trace_bytes;
+    H.d.off_rate = off;
+    off += H.rate_bytes;
   }
   off = align_up(off, 256);
   Lo.off_state = off;
@@ -478,6 +507,11 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
       if (c.trace_out_len)
         std::memcpy(img.data() + d.off_tr_len, c.trace_out_len, 4ull * c.n_trace);
     }
+    if (c.n_rate_pts > 0) {  // rate_t [P], then rate_f [m][P]
+      std::memcpy(img.data() + d.off_rate, c.rate_t, 8ull * c.n_rate_pts);
+      std::memcpy(img.data() + d.off_rate + 8ull * c.n_rate_pts, c.rate_f,
+                  8ull * c.n_rate_pts * c.m);
+    }
   }
   for (int pk = 0; pk < 3; ++pk)
     if (!lists[pk].empty())
@@ -508,9 +542,12 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     B.off_list = Lo.list_off[pk];
     B.n_list = Lo.list_count[pk];
     B.lanes = Lo.lanes[pk];
-    B.any_trace = 0;
-    for (int i = 0; i < n_jobs; ++i)
-      if (launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_trace > 0) B.any_trace = 1;
+    B.any_trace = B.any_tv = 0;
+    for (int i = 0; i < n_jobs; ++i) {
+      if (launch_kind(jobs[i].pol) != pk) continue;
+      if (jobs[i].cfg->n_trace > 0) B.any_trace = 1;
+      if (jobs[i].cfg->n_rate_pts > 0) B.any_tv = 1;
+    }
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)
       e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, s);

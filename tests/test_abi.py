@@ -25,7 +25,7 @@ def test_library_exports_header_symbols():
     assert "wait_sim_run" in names and "wait_sim_advance" in names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.wait_sim_abi_version() == 1
+    assert lib.wait_sim_abi_version() == B.WS_ABI_VERSION == 2
 
 
 def _err(jobs):
@@ -92,3 +92,29 @@ def test_type_limits():
         assert _err(model(9, policy)).code == B.WS_EUNSUPPORTED
     assert B.workspace_bytes(B.JobArray(model(16, "nested"))) > 0
     assert _err(model(17, "nested")).code == B.WS_EINVAL
+
+
+def test_rate_profile_validation():
+    """Time-varying rates: points strictly increasing and finite, factors
+    finite and >= 0, at most WS_MAX_RATE_PTS points, no arrival list beside
+    them; a valid profile sizes without error."""
+    from paper_2504_11320_amd import binding as B
+    m = 3
+
+    def prof(t, f, **kw):
+        return _job(rate_t=np.asarray(t, float), rate_f=np.asarray(f, float), **kw)
+
+    ok = prof([0.0, 1000.0], [[1.0, 2.0]] * m)
+    assert B.workspace_bytes(B.JobArray(ok)) > 0
+    assert _err(prof([0.0, 0.0], [[1.0, 2.0]] * m)).code == B.WS_EINVAL
+    assert _err(prof([1.0, 0.0], [[1.0, 2.0]] * m)).code == B.WS_EINVAL
+    assert _err(prof([0.0, np.inf], [[1.0, 2.0]] * m)).code == B.WS_EINVAL
+    assert _err(prof([0.0, 1.0], [[1.0, -2.0]] * m)).code == B.WS_EINVAL
+    assert _err(prof([0.0, 1.0], [[1.0, np.nan]] * m)).code == B.WS_EINVAL
+    assert _err(prof([0.0, 1.0], [[1.0, 1e308]] * m, lam=[10.0, 0.1, 0.1])).code == B.WS_EINVAL
+    P = 33
+    assert _err(prof(np.arange(P), np.ones((m, P)))).code == B.WS_EINVAL
+    assert B.workspace_bytes(B.JobArray(prof(np.arange(32), np.ones((m, 32))))) > 0
+    tr = W.trace_workload("wait", [16], [4], 5.0, 0.01, 1000, [1], [0.0], [0])
+    tr.rate_t, tr.rate_f = np.array([0.0]), np.array([[1.0]])
+    assert _err([W.Job(tr, 0, W.ids(1))]).code == B.WS_EINVAL

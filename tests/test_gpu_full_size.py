@@ -1,5 +1,5 @@
-"""Full-size launches of the Nested WAIT, policy-sweep and heavy-tailed
-workloads, exactly as configured (every replica, the full horizon, one
+"""Full-size launches of the Nested WAIT, policy-sweep, heavy-tailed and
+cyclic time-varying workloads, exactly as configured (every replica, the full horizon, one
 launch): properties that hold for every replica are checked on all of them,
 and sampled replicas are recomputed one by one by the oracle and compared
 field by field (integers exact, fp64 within 1e-12 relative)."""
@@ -96,3 +96,14 @@ def test_config5_full_size(B):
     g = _run(B, jobs, 1000000, "config5 full size")
     _invariants(g, 1000000, "config5")
     _sampled(g, jobs, 1000000, [(0, 0), (0, 4095), (0, 8191)], "config5 full size")
+
+
+def test_cyclic_full_size(B):
+    """Llama-shaped WAIT sweep with cyclic time-varying rates (two cycles of
+    lam_j (1 + 0.5 sin(.)) over 8e8 ms, phases 2 pi j / 3): 32 rates x 1024
+    replicas x 1e5 batches, the benchmark's launch."""
+    jobs = W.config_cyclic()
+    g = _run(B, jobs, 100000, "cyclic full size")
+    _invariants(g, 100000, "cyclic")
+    picks = [(0, 0), (0, 1023), (15, 511), (31, 7), (31, 1000)]
+    _sampled(g, jobs, 100000, picks, "cyclic full size")

@@ -217,6 +217,43 @@ def config5(replicas: int = 8192, record_capacity: int = 1 << 18) -> List[Job]:
     return [Job(wl, 0, ids(replicas))]
 
 
+# ------------------------------------------------- time-varying rates ----
+
+
+def diurnal_profile(m: int, span: float, points: int = 25, amp: float = 0.5,
+                    cycles: float = 1.0, phases: Optional[Sequence[float]] = None):
+    """Rate profile (rate_t [points], rate_f [m, points]) with
+    f_j(t) = 1 + amp sin(2 pi cycles t / span + phase_j) at `points` equally
+    spaced times over [0, span]; phases default to 2 pi j / m, so the type
+    mix turns over the cycle as well as the total load."""
+    t = np.linspace(0.0, span, points)
+    if phases is None:
+        phases = [2.0 * math.pi * j / m for j in range(m)]
+    f = np.stack([1.0 + amp * np.sin(2.0 * math.pi * cycles * t / span + ph)
+                  for ph in phases])
+    return t, np.maximum(f, 0.0)
+
+
+def with_profile(wl: Workload, rate_t, rate_f) -> Workload:
+    return dataclasses.replace(wl, rate_t=np.asarray(rate_t, dtype=np.float64),
+                               rate_f=np.asarray(rate_f, dtype=np.float64))
+
+
+# Simulated time spanned by the cyclic workload's profile: 10^5 batches of the
+# Llama-shaped WAIT mix near the fluid boundary cover about 6-9 x 10^8 ms.
+TV_SPAN = 8.0e8
+
+
+def config_cyclic(replicas: int = 1024, n_rates: int = 32, rate_index=None,
+                  record_capacity: int = 1 << 15, span: float = TV_SPAN) -> List[Job]:
+    """config2's WAIT jobs with time-varying rates: type j arrives at
+    lam_j (1 + 0.5 sin(4 pi t / span + 2 pi j / 3)), two cycles over [0, span],
+    piecewise linear through 25 points."""
+    rt, rf = diurnal_profile(3, span, points=25, cycles=2.0)
+    return [Job(with_profile(j.wl, rt, rf), j.seed, j.replica_ids)
+            for j in config2(replicas, n_rates, rate_index, record_capacity)]
+
+
 # ------------------------------------------------------------- traces ----
 
 
