@@ -14,6 +14,12 @@
   p_k = (sum_{r > k} rate_r) / (sum_{r >= k} rate_r) (Section 6).
 * ``calibrate_nested`` / ``calibrate_wait``: the Section 6 allocation of a
   system-wide batch-size cap tl to per-stage thresholds.
+* time-varying rates (appendix, time-varying arrival rates): expected window
+  arrivals ``window_arrivals``, the worst window load ``window_load_sup``
+  (Lambda^pi), worst continuation probabilities ``continuation_sup`` (p*_k),
+  the time-averaged fluid throughput ``fluid_throughput_tv``, a full batch's
+  duration ``full_batch_time`` and the threshold conditions
+  ``check_time_varying``.
 """
 from __future__ import annotations
 
@@ -126,3 +132,164 @@ def calibrate_wait(tl: int, out_len: int) -> dict:
     stages = out_len + 1
     return {"stage_caps": _spread(int(tl), stages),
             "threshold": max(1, int(tl) // stages)}
+
+
+# ------------------------------------------------- time-varying rates ----
+# Intensities lam_j f_j(t), f_j linear between the profile points rate_t and
+# constant outside them (the simulator's rate profile).  The appendix on
+# time-varying rates replaces constant-rate threshold conditions by conditions
+# on the expected arrivals in service windows:
+#   A_j(t, h) = zeta * integral_t^{min(T, t + h / zeta)} lam_j^u du,
+#   Lambda^pi = sup_t sum_j A_j(t, Delta^pi) < n_1,
+#   p_k^* = sup over windows of sum_{r >= k} A_r / sum_{r >= k-1} A_r
+#         < n_k / n_{k-1},
+# and benchmarks throughput by (1/T) integral_0^T sum_j lam_j^t l'_j dt.
+
+
+def _pl(rate_t, vals, t):
+    """Piecewise-linear profile value(s) at t (constant outside)."""
+    return np.interp(t, rate_t, vals)
+
+
+def _pl_integral(rate_t, vals, a: float, b: float) -> float:
+    """Exact integral over [a, b] (a <= b) of a piecewise-linear profile."""
+    if not b > a:
+        return 0.0
+    inner = [x for x in rate_t if a < x < b]
+    pts = np.array([a, *inner, b], dtype=np.float64)
+    v = _pl(rate_t, vals, pts)
+    return float(np.sum(np.diff(pts) * (v[1:] + v[:-1]) / 2.0))
+
+
+def profile_intensities(lam: Sequence[float], rate_t, rate_f) -> np.ndarray:
+    """lam_j f_j at the profile points, [m][P]."""
+    f = np.asarray(rate_f, dtype=np.float64).reshape(len(lam), len(rate_t))
+    return np.asarray(lam, dtype=np.float64)[:, None] * f
+
+
+def window_arrivals(lam, rate_t, rate_f, t: float, h: float, zeta: float = 1.0,
+                    T: float = math.inf) -> np.ndarray:
+    """A_j(t, h) for every type j."""
+    rt = np.asarray(rate_t, dtype=np.float64)
+    inten = profile_intensities(lam, rt, rate_f)
+    b = min(T, t + h / zeta)
+    return np.array([zeta * _pl_integral(rt, row, t, b) for row in inten])
+
+
+def window_load_sup(lam, rate_t, rate_f, h: float, T: float, zeta: float = 1.0):
+    """(Lambda, t*): the largest total expected arrivals sum_j A_j(t, h) over
+    window starts t in [0, T], and a start attaining it.  Exact: the window
+    integral is piecewise quadratic in t, its breakpoints are the profile
+    points, the points minus the window length and T minus it; the maximum
+    lies at a breakpoint or where the derivative (linear between breakpoints)
+    vanishes."""
+    rt = np.asarray(rate_t, dtype=np.float64)
+    tot = profile_intensities(lam, rt, rate_f).sum(axis=0)
+    w = h / zeta
+
+    def g(t):
+        return zeta * _pl_integral(rt, tot, t, min(T, t + w))
+
+    def dg(t, side):
+        # one-sided derivative of g at t (side = +1 right, -1 left)
+        e = side * 1e-12 * max(1.0, abs(t), w)
+        up = _pl(rt, tot, t + w) if t + e + w < T else 0.0
+        return zeta * (up - _pl(rt, tot, t))
+
+    cand = {0.0, float(T)}
+    for x in list(rt) + list(rt - w) + [T - w]:
+        if 0.0 <= x <= T:
+            cand.add(float(x))
+    pts = sorted(cand)
+    roots = []
+    for a, b in zip(pts[:-1], pts[1:]):
+        da, db = dg(a, +1), dg(b, -1)
+        if da > 0 > db:
+            roots.append(a + (b - a) * da / (da - db))
+    best = max(pts + roots, key=g)
+    return g(best), best
+
+
+def _ratio_sup(num, den, rate_t, T):
+    """sup over t in [0, T] with den(t) > 0 of num(t) / den(t), num and den
+    piecewise linear on the same points (0 <= num <= den).  On each piece the
+    ratio of two linear functions is monotone, so the supremum is at a piece
+    end, or a one-sided limit where den vanishes (ratio of the slopes)."""
+    rt = np.asarray(rate_t, dtype=np.float64)
+    pts = sorted({0.0, float(T), *[float(x) for x in rt if 0.0 < x < T]})
+    best = 0.0
+    for a, b in zip(pts[:-1], pts[1:]):
+        na, nb = _pl(rt, num, a), _pl(rt, num, b)
+        da, db = _pl(rt, den, a), _pl(rt, den, b)
+        if da <= 0.0 and db <= 0.0:
+            continue
+        for n_end, d_end in ((na, da), (nb, db)):
+            if d_end > 0.0:
+                best = max(best, n_end / d_end)
+            else:  # den -> 0 at this end: the limit is the ratio of slopes
+                best = max(best, (nb - na) / (db - da))
+    if len(pts) == 1 and _pl(rt, den, 0.0) > 0.0:  # T = 0: the single instant
+        best = _pl(rt, num, 0.0) / _pl(rt, den, 0.0)
+    return best
+
+
+def segment_intensities(lam, rate_t, rate_f, seg_end: Sequence[int],
+                        out_len: Optional[Sequence[int]] = None,
+                        cdf: Optional[np.ndarray] = None, cap: int = 0) -> np.ndarray:
+    """Intensity of requests whose final output length lies in each segment,
+    at the profile points, [L][P]."""
+    inten = profile_intensities(lam, rate_t, rate_f)
+    out = np.zeros((len(seg_end), len(rate_t)))
+    for j in range(len(lam)):
+        unit = [0.0] * len(lam)
+        unit[j] = 1.0
+        share = segment_rates(unit, seg_end, out_len=out_len, cdf=cdf, cap=cap)
+        out += np.outer(share, inten[j])
+    return out
+
+
+def continuation_sup(seg_inten: np.ndarray, rate_t, T: float) -> list:
+    """p*_k for k = 1..L-1 (the probability that a request reaching the end
+    of segment k goes on, at its worst over [0, T]): the supremum of the
+    instantaneous ratio sum_{r > k} / sum_{r >= k} of segment intensities,
+    which bounds the ratio over any window (a weighted average of it) and is
+    approached by short windows."""
+    S = np.asarray(seg_inten, dtype=np.float64)
+    return [_ratio_sup(S[k + 1:].sum(axis=0), S[k:].sum(axis=0), rate_t, T)
+            for k in range(S.shape[0] - 1)]
+
+
+def fluid_throughput_tv(lam, rate_t, rate_f, out_len: Sequence[float], T: float) -> float:
+    """(1/T) integral_0^T sum_j lam_j^t l'_j dt (decode tokens per unit time)."""
+    rt = np.asarray(rate_t, dtype=np.float64)
+    inten = profile_intensities(lam, rt, rate_f)
+    return float(sum(lp * _pl_integral(rt, row, 0.0, T)
+                     for lp, row in zip(out_len, inten)) / T)
+
+
+def full_batch_time(d0: float, d1: float, prompt_len: float, seg_end: Sequence[int],
+                    n: Sequence[float]) -> float:
+    """Duration of a batch holding n_k prompts at every stage of segment k:
+    segment 1 spans stages 0..r_1 (prefill charges l, stage s charges l + s),
+    segment k the stages r_{k-1}+1..r_k."""
+    tokens, lo = 0.0, 0
+    for k, (r, nk) in enumerate(zip(seg_end, n)):
+        stages = range(lo, r + 1)
+        tokens += nk * sum(prompt_len + s for s in stages)
+        lo = r + 1
+    return d0 + d1 * tokens
+
+
+def check_time_varying(lam, rate_t, rate_f, n: Sequence[float], delta: float, T: float,
+                       seg_inten: Optional[np.ndarray] = None, zeta: float = 1.0) -> dict:
+    """The threshold conditions for time-varying rates: Lambda^pi < n_1 with
+    Lambda^pi the worst expected arrivals in a window of length delta (a full
+    batch's service time), and p*_k < n_{k+1} / n_k at every boundary (when
+    segment intensities are given)."""
+    Lam, t_star = window_load_sup(lam, rate_t, rate_f, delta, T, zeta)
+    out = {"Lambda_pi": Lam, "t_star": t_star, "load_ok": Lam < n[0]}
+    if seg_inten is not None:
+        p = continuation_sup(seg_inten, rate_t, T)
+        out["p_star"] = p
+        out["continuation_ok"] = all(pk < n[k + 1] / n[k] for k, pk in enumerate(p))
+    return out
