@@ -196,23 +196,17 @@ struct RateProfLds {
   double fmax[MT];
 };
 
-// -1 before the first point, P-1 from the last point on, else the i with
-// rt[i] <= t < rt[i+1] (rt strictly increasing).
-__device__ __forceinline__ int rate_seg(const double *rt, int P, double t) {
-  if (t < rt[0]) return -1;
-  if (!(t < rt[P - 1])) return P - 1;
-  int lo = 0, hi = P - 1;  // rt[lo] <= t < rt[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (t < rt[mid])
-      hi = mid;
-    else
-      lo = mid;
-  }
-  return lo;
+// Piece of the profile that holds t: -1 before the first point, P-1 from the
+// last point on, else the i with rt[i] <= t < rt[i+1] (rt strictly
+// increasing).  A type's candidate times never decrease, so each type keeps a
+// cursor at its current piece and moves it forward: cur (-1 at the start of a
+// call) is the piece of an earlier time, and on return the piece of t.
+__device__ __forceinline__ int rate_seg_from(const double *rt, int P, double t, int &cur) {
+  while (cur < P - 1 && !(t < rt[cur + 1])) ++cur;
+  return cur;
 }
 
-// f(t) for t in piece i of rate_seg.
+// f(t) for t in piece i.
 __device__ __forceinline__ double rate_fac(const double *rt, const double *f, int P, int i,
                                            double t) {
   if (i < 0) return f[0];
@@ -221,39 +215,66 @@ __device__ __forceinline__ double rate_fac(const double *rt, const double *f, in
   return f[i] + (f[i + 1] - f[i]) * frac;
 }
 
-// Next arrival of a type with a rate profile, by thinning: starting from
-// candidate k (the clock at the previous candidate or arrival is t), draw
-// candidates of the Poisson process at the bound lam_c = lambda_j fmax and keep
-// the first with w3 fmax < f(t_k) 2^32.  Returns its time and leaves k at its
-// counter (and *L at its output length when a CDF row is given).  A candidate
-// inside a stretch where f is zero moves the clock to the stretch's end; a
-// zero intensity from the last point on, or kThinMax rejections in a row
-// (flagged), end the type's arrivals (time +inf).
+// Thinning decision for a candidate at time tc with fourth Philox word w3:
+// 0 = kept (t = tc); 1 = rejected with zero intensity from the last point on
+// (the type stops); 2 = rejected, t = the clock the next candidate starts
+// from (the end of a zero stretch that holds tc, else tc).
+__device__ __forceinline__ int thin_decide(double tc, uint32_t w3, double fmax,
+                                           const double *rt, const double *f, int P,
+                                           double &t, int &cur) {
+  const int i = rate_seg_from(rt, P, tc, cur);
+  if ((double)w3 * fmax < rate_fac(rt, f, P, i, tc) * 4294967296.0) {
+    t = tc;
+    return 0;
+  }
+  if (i == P - 1 && f[P - 1] == 0.0) return 1;
+  if (i < 0 && f[0] == 0.0)
+    t = rt[0];
+  else if (i >= 0 && i < P - 1 && f[i] == 0.0 && f[i + 1] == 0.0)
+    t = rt[i + 1];
+  else
+    t = tc;
+  return 2;
+}
+
+// Next arrival of a type with a rate profile, by thinning: from candidate k
+// on (the clock at the previous arrival is t), take candidates of the Poisson
+// process at the bound lambda_j fmax from cand(k, &gap, &w3) and keep the first
+// that thin_decide keeps.  Returns its time and leaves k at its counter (cur
+// at its piece).  A zero intensity from the last point on, or kThinMax
+// rejections in a row (flagged), end the type's arrivals (time +inf).
+template <typename Cand>
+__device__ __forceinline__ double next_thinned(uint32_t &k, double t, double fmax,
+                                               const double *rt, const double *f, int P,
+                                               int &cur, uint32_t &flags, Cand cand) {
+  if (!(fmax > 0.0)) return INFINITY;
+  for (uint32_t tries = 0;; ++tries) {
+    double g;
+    uint32_t w3;
+    cand(k, g, w3);
+    const int d = thin_decide(t + g, w3, fmax, rt, f, P, t, cur);
+    if (d == 0) return t;
+    if (tries + 1u >= kThinMax) {
+      flags |= kFlagThin;
+      return INFINITY;
+    }
+    if (d == 1) return INFINITY;
+    ++k;
+  }
+}
+
+// next_thinned with every candidate drawn here (output length into *L when a
+// CDF row is given).
 __device__ __forceinline__ double draw_thinned(uint64_t seed, uint32_t rid, uint32_t j,
                                                uint32_t &k, double t, double lam_c,
                                                double fmax, const double *rt,
                                                const double *f, int P,
                                                const uint32_t *row, int32_t cap,
-                                               int32_t *L, uint32_t &flags) {
-  if (!(fmax > 0.0)) return INFINITY;
-  for (uint32_t tries = 0;; ++tries) {
-    uint32_t w3;
-    const double tc = t + draw_gap(seed, rid, j, k, lam_c, row, cap, L, &w3);
-    const int i = rate_seg(rt, P, tc);
-    if ((double)w3 * fmax < rate_fac(rt, f, P, i, tc) * 4294967296.0) return tc;
-    if (tries + 1u >= kThinMax) {
-      flags |= kFlagThin;
-      return INFINITY;
-    }
-    if (i == P - 1 && f[P - 1] == 0.0) return INFINITY;
-    if (i < 0 && f[0] == 0.0)
-      t = rt[0];
-    else if (i >= 0 && i < P - 1 && f[i] == 0.0 && f[i + 1] == 0.0)
-      t = rt[i + 1];
-    else
-      t = tc;
-    ++k;
-  }
+                                               int32_t *L, int &cur, uint32_t &flags) {
+  return next_thinned(k, t, fmax, rt, f, P, cur, flags,
+                      [&](uint32_t kc, double &g, uint32_t &w3) {
+                        g = draw_gap(seed, rid, j, kc, lam_c, row, cap, L, &w3);
+                      });
 }
 
 // Histogram bin of a latency: number of edges <= lat (edges strictly

@@ -48,23 +48,23 @@ sim_known_kernel(KArgs A) {
   // Inter-arrival gaps are drawn ahead of use by the whole wavefront at once
   // (64 draws per pass, no divergence) into a ring of GR gaps per type and
   // lane; a lane whose ring runs dry draws the gap itself.
-  constexpr int GR = MT <= 4 ? 16 : 4;  // ring size per (type, lane)
+  // With time-varying rates the rings hold candidates of the thinning bound
+  // process with their fourth Philox words (the acceptance draws), and the
+  // rate profile sits in LDS beside them.
+  constexpr int GR = MT <= 4 ? (TV ? 8 : 16) : 4;  // ring size per (type, lane)
   constexpr int GU = GR / 2;            // gaps added per refill
   constexpr uint32_t kLow = GU / 2;     // a lane below this triggers a refill
   __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
   __shared__ uint8_t s_htab[kHistTab];
   __shared__ int s_hsteps;
-  // The gap rings, or for a job with time-varying intensities (whose lanes
-  // draw their own candidates) the rate profile in the same LDS.
-  __shared__ union {
-    double gap[MT][GR][LN];
-    RateProfLds<MT, TV ? kMaxRatePts : 1> prof;
-  } s_u;
-  double(&s_gap)[MT][GR][LN] = s_u.gap;
+  __shared__ double s_gap[MT][GR][LN];
   constexpr int NP = TV ? kMaxRatePts : 1;
-  double(&s_rt)[NP] = s_u.prof.t;
-  double(&s_rf)[MT][NP] = s_u.prof.f;
-  double(&s_fmax)[MT] = s_u.prof.fmax;
+  __shared__ uint32_t s_w3[TV ? MT : 1][TV ? GR : 1][TV ? LN : 1];
+  __shared__ RateProfLds<MT, NP> s_prof;
+  __shared__ int8_t s_cur[TV ? MT : 1][TV ? LN : 1];  // profile piece per type
+  double(&s_rt)[NP] = s_prof.t;
+  double(&s_rf)[MT][NP] = s_prof.f;
+  double(&s_fmax)[MT] = s_prof.fmax;
   __shared__ uint64_t s_seed[LN];
   __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   // The last WB records pushed on each resident deque are also kept in LDS,
@@ -187,8 +187,9 @@ sim_known_kernel(KArgs A) {
       tnext[j] = INFINITY;
       if (j < m && !trace && tv) {
         uint32_t k0 = 0;
+        int cur = -1;
         tnext[j] = draw_thinned(seed, rid, (uint32_t)j, k0, 0.0, lam[j], s_fmax[j], s_rt, s_rf[j],
-                                P, nullptr, 0, nullptr, flags);
+                                P, nullptr, 0, nullptr, cur, flags);
         kk[j] = k0;
       } else if (j < m && !trace) {
         tnext[j] = 0.0 + draw_gap(seed, rid, (uint32_t)j, 0u, lam[j], nullptr, 0, nullptr);
@@ -229,9 +230,11 @@ sim_known_kernel(KArgs A) {
       pend[j] = (uint32_t)slot_i(A, S_LNEXT + j, r);
     }
   }
-  // caches of the ring ends; the gap rings start empty
+  // caches of the ring ends; the gap rings start empty; profile cursors start
+  // before the first piece
 #pragma unroll
   for (int j = 0; j < MT; ++j) {
+    if constexpr (TV) s_cur[j][tx] = -1;
     gend[j] = kk[j] + 1u;
     wv[j] = 0;
     // unconditional loads: a slot past the tail holds a stale record that is
@@ -420,12 +423,28 @@ sim_known_kernel(KArgs A) {
   auto take = [&](int jn, double a) __attribute__((always_inline)) {
     if (trace) {
       tridx++;
-    } else if (tv) {  // thinning, drawn by the lane itself
-      uint32_t k = pick(kk, jn) + 1u;
-      const double tn = draw_thinned(seed, rid, (uint32_t)jn, k, pick(tnext, jn), pick(lam, jn),
-                                     s_fmax[jn], s_rt, s_rf[jn], P, nullptr, 0, nullptr, flags);
-      place(kk, jn, k);
-      place(tnext, jn, tn);
+    } else if (tv) {
+      if constexpr (TV) {  // thinning over the candidates in the ring
+        uint32_t k = pick(kk, jn) + 1u;
+        uint32_t ge = pick(gend, jn);
+        const double lamc = pick(lam, jn);
+        int cur = s_cur[jn][tx];
+        const double tn = next_thinned(k, pick(tnext, jn), s_fmax[jn], s_rt, s_rf[jn], P, cur, flags,
+                                       [&](uint32_t kc, double &g, uint32_t &w3) {
+                                         if (kc < ge) {
+                                           g = s_gap[jn][kc % GR][tx];
+                                           w3 = s_w3[jn][kc % GR][tx];
+                                         } else {
+                                           g = draw_gap(seed, rid, (uint32_t)jn, kc, lamc,
+                                                        nullptr, 0, nullptr, &w3);
+                                           ge = kc + 1u;
+                                         }
+                                       });
+        s_cur[jn][tx] = (int8_t)cur;
+        place(gend, jn, ge);
+        place(kk, jn, k);
+        place(tnext, jn, tn);
+      }
     } else {
       const uint32_t k = pick(kk, jn) + 1u;
       place(kk, jn, k);
@@ -452,7 +471,7 @@ sim_known_kernel(KArgs A) {
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- refill the gap rings, all active lanes together ----------------
-    if (!TRACE && !tv) {
+    if (!TRACE) {
       const uint64_t act = __ballot(1);
       const int nact = __popcll(act);
       const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
@@ -478,8 +497,10 @@ sim_known_kernel(KArgs A) {
           if (w < total) {
             const int ln = (int)s_req_lane[w / GU];
             const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
-            s_gap[j][k % GR][ln] =
-                draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lam[j], nullptr, 0, nullptr);
+            uint32_t w3;
+            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lam[j],
+                                            nullptr, 0, nullptr, TV ? &w3 : nullptr);
+            if constexpr (TV) s_w3[j][k % GR][ln] = w3;
           }
         }
         wave_lds_sync();

@@ -114,18 +114,18 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   __shared__ double s_tnext[MT][LN];
   __shared__ uint32_t s_k[MT][LN], s_gend[MT][LN];
   __shared__ int32_t s_Ln[MT][LN];
-  // The gap rings, or for a job with time-varying intensities (whose lanes
-  // draw their own candidates) the rate profile in the same LDS.
-  __shared__ union {
-    double gap[MT][GR][LN];
-    RateProfLds<MT, TV ? kMaxRatePts : 1> prof;
-  } s_u;
-  double(&s_gap)[MT][GR][LN] = s_u.gap;
-  constexpr int NP = TV ? kMaxRatePts : 1;
-  double(&s_rt)[NP] = s_u.prof.t;
-  double(&s_rf)[MT][NP] = s_u.prof.f;
-  double(&s_fmax)[MT] = s_u.prof.fmax;
+  // With time-varying rates the rings hold candidates of the thinning bound
+  // process with their fourth Philox words (the acceptance draws), and the
+  // rate profile sits in LDS beside them.
+  __shared__ double s_gap[MT][GR][LN];
   __shared__ int32_t s_glen[MT][GR][LN];
+  constexpr int NP = TV ? kMaxRatePts : 1;
+  __shared__ uint32_t s_w3[TV ? MT : 1][TV ? GR : 1][TV ? LN : 1];
+  __shared__ RateProfLds<MT, NP> s_prof;
+  __shared__ int8_t s_cur[TV ? MT : 1][TV ? LN : 1];  // profile piece per type
+  double(&s_rt)[NP] = s_prof.t;
+  double(&s_rf)[MT][NP] = s_prof.f;
+  double(&s_fmax)[MT] = s_prof.fmax;
   __shared__ uint64_t s_seed[LN];
   __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
@@ -253,8 +253,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         int32_t Lj = 1;
         if (tv) {
           uint32_t k0 = 0;
+          int cur = -1;
           s_tnext[j][tx] = draw_thinned(seed, rid, (uint32_t)j, k0, 0.0, J.lambda[j], s_fmax[j],
-                                        s_rt, s_rf[j], P, row_of(j), cap, &Lj, flags);
+                                        s_rt, s_rf[j], P, row_of(j), cap, &Lj, cur, flags);
           s_k[j][tx] = k0;
         } else {
           const double g = draw_gap(seed, rid, (uint32_t)j, 0u, J.lambda[j], row_of(j), cap, &Lj);
@@ -312,7 +313,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
   }
 
-  for (int j = 0; j < MT; ++j) s_gend[j][tx] = s_k[j][tx] + 1u;  // gap rings start empty
+  for (int j = 0; j < MT; ++j) {
+    s_gend[j][tx] = s_k[j][tx] + 1u;  // gap rings start empty
+    if constexpr (TV) s_cur[j][tx] = -1;  // profile cursors before the first piece
+  }
   for (int k = 0; k < LT; ++k) {
     s_yidx[k][tx] = kNil;
     if (k >= 1 && k < L && s_vt[k][tx] != s_vh[k][tx])
@@ -360,15 +364,31 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     if (trace) {
       Lr = known ? s_lp[jn] : tr_len[tridx];
       tridx++;
-    } else if (tv) {  // thinning, drawn by the lane itself
-      Lr = s_Ln[jn][tx];
-      uint32_t k = s_k[jn][tx] + 1u;
-      int32_t Lj = 1;
-      const double tn = draw_thinned(seed, rid, (uint32_t)jn, k, s_tnext[jn][tx], J.lambda[jn],
-                                     s_fmax[jn], s_rt, s_rf[jn], P, row_of(jn), cap, &Lj, flags);
-      s_k[jn][tx] = k;
-      s_tnext[jn][tx] = tn;
-      s_Ln[jn][tx] = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
+    } else if (tv) {
+      if constexpr (TV) {  // thinning over the candidates in the ring
+        Lr = s_Ln[jn][tx];
+        uint32_t k = s_k[jn][tx] + 1u;
+        uint32_t ge = s_gend[jn][tx];
+        int32_t Lj = 1;
+        int cur = s_cur[jn][tx];
+        const double tn = next_thinned(k, s_tnext[jn][tx], s_fmax[jn], s_rt, s_rf[jn], P, cur, flags,
+                                       [&](uint32_t kc, double &g, uint32_t &w3) {
+                                         if (kc < ge) {
+                                           g = s_gap[jn][kc % GR][tx];
+                                           w3 = s_w3[jn][kc % GR][tx];
+                                           Lj = s_glen[jn][kc % GR][tx];
+                                         } else {
+                                           g = draw_gap(seed, rid, (uint32_t)jn, kc, J.lambda[jn],
+                                                        row_of(jn), cap, &Lj, &w3);
+                                           ge = kc + 1u;
+                                         }
+                                       });
+        s_cur[jn][tx] = (int8_t)cur;
+        s_gend[jn][tx] = ge;
+        s_k[jn][tx] = k;
+        s_tnext[jn][tx] = tn;
+        s_Ln[jn][tx] = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
+      }
     } else {
       Lr = s_Ln[jn][tx];
       const uint32_t k = s_k[jn][tx] + 1u;
@@ -534,7 +554,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- refill the draw rings, all active lanes together -----------------
-    if (!trace && !tv) {
+    if (!trace) {
       const uint64_t act = __ballot(1);
       const int nact = __popcll(act);
       const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
@@ -562,8 +582,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             const int ln = (int)s_req_lane[w / GU];
             const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
             int32_t Lj = 1;
-            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lamj, row, cap, &Lj);
+            uint32_t w3;
+            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lamj, row, cap,
+                                            &Lj, TV ? &w3 : nullptr);
             s_glen[j][k % GR][ln] = Lj;
+            if constexpr (TV) s_w3[j][k % GR][ln] = w3;
           }
         }
         wave_lds_sync();
