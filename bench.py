@@ -40,11 +40,19 @@ ALU_PEAK = CUS * LANES_PER_CU_CLK * CLOCK_HZ          # 3.93e13 lane-ops/s
 HBM_PEAK = 8.0e12                                     # bytes/s
 
 CSRC = os.path.join(ROOT, "paper_2504_11320_amd", "csrc")
-# the sources that define the benchmark's kernel (hashed to tie the committed
-# HBM counter summary to the kernel it was measured on)
-KERNEL_SRCS = [os.path.join(CSRC, f)
-               for f in ("sim_known_impl.h", "sim_known_wait.hip", "sim_common.h")]
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "sim_known_wait_3type_32x1024x1e5_hbm.md")
+# Per workload: the committed rocprofv3 HBM counter summary of its dominant
+# kernel and the sources that define that kernel (hashed to tie the summary
+# to the kernel it was measured on).
+_WAIT_SRCS = ("sim_known_impl.h", "sim_known_wait.hip", "sim_common.h")
+PROFILES = {
+    "wait-llama": ("sim_known_wait_3type_32x1024x1e5", _WAIT_SRCS),
+    "wait-cyclic": ("sim_known_wait_tv_3type_cyclic_32x1024x1e5",
+                    ("sim_known_impl.h", "sim_known_wait_tv.hip", "sim_common.h")),
+    "nested-geometric": ("sim_nested_3type_geometric_32x1024x1e5",
+                         ("sim_nested_impl.h", "sim_nested.hip", "sim_common.h")),
+    "nested-heavytail": ("sim_nested_10type_lognormal_8192x1e6",
+                         ("sim_nested_impl.h", "sim_nested.hip", "sim_common.h")),
+}
 
 
 def op_model(m: int, cdf_cap: int = 0, rate_pts: int = 0, cand_per_arrival: float = 1.0) -> dict:
@@ -110,23 +118,26 @@ def algorithmic_bytes(res: dict) -> float:
     return float(16 * 2 * ev + 16 * res["completions"].sum())
 
 
-def source_hash() -> str:
+def source_hash(workload: str = "wait-llama") -> str:
     h = hashlib.sha256()
-    for path in KERNEL_SRCS:
-        with open(path, "rb") as f:
+    for name in PROFILES[workload][1]:
+        with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile():
-    """HBM bytes per launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source."""
-    if not os.path.exists(PMC_SUMMARY):
+def traffic_from_profile(workload: str):
+    """HBM bytes per launch from the workload's committed rocprofv3 counter
+    summary, if there is one and it was taken on the current kernel source."""
+    if workload not in PROFILES:
         return None
-    txt = open(PMC_SUMMARY).read()
+    path = os.path.join(ROOT, "profiles", PROFILES[workload][0] + "_hbm.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
     h = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt)
     b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
-    if not h or not b or h.group(1) != source_hash():
+    if not h or not b or h.group(1) != source_hash(workload):
         return None
     return float(b.group(1))
 
@@ -270,7 +281,8 @@ def main() -> int:
 
     ops = algorithmic_ops(res, m, cdf_cap, rate_pts, cpa)
     achieved = ops / (ms_step / 1e3)
-    traffic = traffic_from_profile() if args.workload == "wait-llama" else None
+    full = args.horizon == horizon0 and args.replicas == 1024
+    traffic = traffic_from_profile(args.workload) if full else None
     roofline = {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK,
                 "unit": "lane-ops/s", "frac": achieved / ALU_PEAK,
                 "traffic": traffic,
