@@ -14,6 +14,11 @@
   p_k = (sum_{r > k} rate_r) / (sum_{r >= k} rate_r) (Section 6).
 * ``calibrate_nested`` / ``calibrate_wait``: the Section 6 allocation of a
   system-wide batch-size cap tl to per-stage thresholds.
+* segment-design memory bound (Section 5.2 and the appendix on the
+  segment-wise design): ``segment_design`` (delta_k, sbar_k), ``base_memory``
+  (M^pi), ``theta_root``, ``memory_requirement`` (M^pi, the deterministic
+  boundary term, the logarithmic buffer), ``fluid_segment_thresholds``,
+  ``equal_rate_cuts`` and ``memory_vs_segments`` (the decomposition against L).
 * time-varying rates (appendix, time-varying arrival rates): expected window
   arrivals ``window_arrivals``, the worst window load ``window_load_sup``
   (Lambda^pi), worst continuation probabilities ``continuation_sup`` (p*_k),
@@ -293,3 +298,131 @@ def check_time_varying(lam, rate_t, rate_f, n: Sequence[float], delta: float, T:
         out["p_star"] = p
         out["continuation_ok"] = all(pk < n[k + 1] / n[k] for k, pk in enumerate(p))
     return out
+
+
+# ------------------------------------------- segment-design memory bound ----
+# Nested WAIT over L segments with boundaries r_1 < ... < r_L (Section 5.2 and
+# the appendix on the segment-wise design): delta_1 = r_1 + 1, sbar_1 = r_1 / 2,
+# delta_k = r_k - r_{k-1}, sbar_k = (r_{k-1} + 1 + r_k) / 2 for k >= 2;
+#   M^pi = sum_k n_k (lbar_k + sbar_k) delta_k,
+#   M_req = M^pi + sum_{k>=2} (lbar_k + r_{k-1}) n_k
+#         + sum_{k>=2} (lbar_k + r_{k-1}) / theta_k * ln(m (1 + zeta T / d0) / delta),
+# theta_k > 0 solving exp(-theta n_k) (1 - p_k + p_k e^theta)^{n_{k-1}} = 1.
+
+
+def segment_design(seg_end: Sequence[int]) -> list:
+    """(delta_k, sbar_k) per segment."""
+    out, prev = [], 0
+    for k, r in enumerate(seg_end):
+        out.append((r + 1, r / 2.0) if k == 0 else (r - prev, (prev + 1 + r) / 2.0))
+        prev = r
+    return out
+
+
+def _per_segment(l_bar, L):
+    return list(l_bar) if isinstance(l_bar, (list, tuple, np.ndarray)) else [l_bar] * L
+
+
+def base_memory(n: Sequence[float], seg_end: Sequence[int], l_bar) -> float:
+    """M^pi, with a common prompt length or per-segment envelopes lbar_k."""
+    lb = _per_segment(l_bar, len(seg_end))
+    return float(sum(nk * (lk + sb) * dk
+                     for nk, lk, (dk, sb) in zip(n, lb, segment_design(seg_end))))
+
+
+def theta_root(n_k: float, n_prev: float, p_k: float) -> float:
+    """The positive root of h(theta) = n_prev ln(1 - p + p e^theta) - theta n_k
+    (h(0) = 0, h'(0) = n_prev p - n_k < 0, h convex and eventually
+    increasing), found by bracketing and Brent's method."""
+    from scipy.optimize import brentq
+    if not (0.0 < p_k < 1.0 and n_prev * p_k < n_k):
+        raise ValueError("theta_k needs 0 < p_k < 1 and n_{k-1} p_k < n_k")
+
+    def h(th):
+        # ln(1 - p + p e^th) = th + ln(p + (1 - p) e^-th), stable for large th
+        return n_prev * (th + math.log(p_k + (1.0 - p_k) * math.exp(-th))) - th * n_k
+
+    a = 1e-9 * max(1.0, 1.0 / n_k)
+    while h(a) >= 0.0:   # step inside the negative region right of 0
+        a *= 0.5
+    b = 1.0
+    while h(b) <= 0.0:
+        b *= 2.0
+    return float(brentq(h, a, b, xtol=1e-15, rtol=1e-15, maxiter=500))
+
+
+def memory_requirement(n: Sequence[float], seg_end: Sequence[int], l_bar,
+                       p: Sequence[float], m: int, zeta_T: float, d0: float,
+                       delta: float) -> dict:
+    """The three terms of the segment-design memory bound and their sum;
+    p[k-1] is the continuation probability into segment k + 1 (k = 1..L-1)."""
+    L = len(seg_end)
+    lb = _per_segment(l_bar, L)
+    term1 = base_memory(n, seg_end, lb)
+    log_term = math.log(m * (1.0 + zeta_T / d0) / delta)
+    term2 = term3 = 0.0
+    thetas = []
+    for k in range(1, L):
+        th = theta_root(n[k], n[k - 1], p[k - 1])
+        thetas.append(th)
+        w = lb[k] + seg_end[k - 1]
+        term2 += w * n[k]
+        term3 += w * log_term / th
+    return {"term1": term1, "term2": term2, "term3": term3,
+            "total": term1 + term2 + term3, "theta": thetas}
+
+
+def fluid_segment_thresholds(seg_rates: Sequence[float], seg_end: Sequence[int], l_bar,
+                             d0: float, d1: float, eta: float = 0.05,
+                             slack: float = 0.05) -> Optional[list]:
+    """Thresholds meeting the segment-design conditions: n_k = n_1 prod_{r<k} q_r
+    with q_k = min(p_k + eta, 0.99) (so p_k < n_k / n_{k-1} < 1), and n_1 a
+    factor (1 + slack) above the smallest value with
+    d0 + d1 M^pi(n) < n_1 / sum_k lam'_k.  None when no n_1 satisfies it
+    (d1 M^pi per unit n_1 at least 1 / sum lam')."""
+    p = continuation_probabilities(seg_rates)
+    rel = [1.0]
+    for x in p:
+        rel.append(rel[-1] * min(x + eta, 0.99))
+    S = base_memory(rel, seg_end, l_bar)        # M^pi per unit n_1
+    gap = 1.0 / sum(seg_rates) - d1 * S
+    if gap <= 0.0:
+        return None
+    n1 = (1.0 + slack) * d0 / gap
+    return [n1 * r for r in rel]
+
+
+def equal_rate_cuts(out_len: Sequence[int], rates: Sequence[float], L: int) -> list:
+    """Segment boundaries for L segments over output-length classes sorted by
+    length: cut after the class where the cumulative arrival rate first reaches
+    k / L of the total (each boundary a class's output length, strictly
+    increasing; fewer than L segments if classes are too coarse)."""
+    order = np.argsort(out_len)
+    lens = np.asarray(out_len)[order]
+    cum = np.cumsum(np.asarray(rates, dtype=np.float64)[order])
+    cuts = []
+    for k in range(1, L):
+        i = int(np.searchsorted(cum, k / L * cum[-1] * (1 - 1e-12)))
+        r = int(lens[min(i, len(lens) - 1)])
+        if (not cuts or r > cuts[-1]) and r < lens[-1]:
+            cuts.append(r)
+    return cuts + [int(lens[-1])]
+
+
+def memory_vs_segments(prompt_len: float, out_len: Sequence[int], rates: Sequence[float],
+                       L_values: Sequence[int], d0: float, d1: float, zeta_T: float,
+                       delta: float, eta: float = 0.05, slack: float = 0.05) -> list:
+    """The decomposition of the memory bound against the number of segments L
+    (common prompt length): for each L, equal-rate cuts, fluid thresholds and
+    the three terms.  Rows with infeasible thresholds are omitted."""
+    rows = []
+    for L in L_values:
+        seg_end = equal_rate_cuts(out_len, rates, L)
+        seg_rates = segment_rates(rates, seg_end, out_len=out_len)
+        n = fluid_segment_thresholds(seg_rates, seg_end, prompt_len, d0, d1, eta, slack)
+        if n is None:
+            continue
+        p = continuation_probabilities(seg_rates)
+        mr = memory_requirement(n, seg_end, prompt_len, p, len(out_len), zeta_T, d0, delta)
+        rows.append({"L": len(seg_end), "seg_end": seg_end, "n": n, **mr})
+    return rows
