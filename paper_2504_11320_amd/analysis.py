@@ -16,6 +16,8 @@ returns (``Simulation.results`` / ``run_batch``).
 * ``lambda_hat``: the stability point of a rate sweep, read as the largest
   tested rate up to which every rate's completion rate stays within a
   tolerance of its arrival rate.
+* ``review_process``: a side simulator of the embedded review process of the
+  critical threshold queue, for the identity E[W^B] = n E[B_stuck].
 """
 from __future__ import annotations
 
@@ -82,3 +84,24 @@ def lambda_hat(rates: Sequence[float], completion_rates: Sequence[float],
         else:
             break
     return best
+
+
+def review_process(n: int, B: int, reps: int, seed: int = 0) -> dict:
+    """The embedded review process of the critical single-type threshold
+    queue (the lemma on queue length and stuck time, Section 4.3): X^b ~
+    Poisson(n) arrivals per review interval, W^{b+1} = W^b + X^b - n 1{W^b + X^b
+    >= n}, W^0 = 0; a review is stuck when W^b + X^b < n.  Simulated for `reps`
+    independent paths of B reviews (numpy, vectorised over paths).  Returns W^B,
+    the stuck counts and the arrival totals per path."""
+    rng = np.random.default_rng(seed)
+    W = np.zeros(reps, dtype=np.int64)
+    stuck = np.zeros(reps, dtype=np.int64)
+    total = np.zeros(reps, dtype=np.int64)
+    for _ in range(B):
+        X = rng.poisson(n, reps)
+        total += X
+        s = W + X
+        served = s >= n
+        W = s - n * served
+        stuck += ~served
+    return {"W": W, "stuck": stuck, "arrivals": total}
