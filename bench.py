@@ -167,6 +167,10 @@ def _workloads():
                         "time-varying rates lam_j (1 + 0.5 sin(4 pi t / 8e8 ms + 2 pi j / 3)), "
                         "32 rates 0.5-1.2x fluid boundary, 1024 replicas each",
                         lambda reps: W.config_cyclic(replicas=reps), 100000, "wait", [0, 31]),
+        "pd-decode": ("decode-only p630d20 (PD-disaggregated decode server: 630-token "
+                      "context, 20 generated tokens), WAIT with fluid thresholds and FCFS "
+                      "with a 1% reserve, 9 rates 0.1-0.5/ms, 1024 replicas each",
+                      lambda reps: W.config_pd(replicas=reps), 100000, "wait+fcfs", [8, 17]),
         "wait-small": ("WAIT, 2 types (16/8, 32/16), C = 2048, 64 replicas",
                        lambda reps: W.config1(), 10000, "wait", [0]),
     }
@@ -206,7 +210,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="wait-llama",
                     help="wait-llama (the benchmark), nested-geometric, wait-sweep, "
-                         "nested-heavytail, nowait-llama, wait-cyclic, wait-small")
+                         "nested-heavytail, nowait-llama, wait-cyclic, pd-decode, wait-small")
     ap.add_argument("--horizon", type=int, default=0, help="batches (0: the workload's)")
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -217,6 +217,39 @@ def config5(replicas: int = 8192, record_capacity: int = 1 << 18) -> List[Job]:
     return [Job(wl, 0, ids(replicas))]
 
 
+# ------------------------------------- decode-only (PD-disaggregated) ----
+
+# A decode server behind a separate prefill service receives each request with
+# its context already cached (630 tokens) and generates 20 tokens.  In the
+# model that is prompt length 630 and output length 19: the model's first
+# processing (time and memory charge l) is the first decode step over the
+# 630-token context, its stage s the step over 630 + s tokens, 20 processings
+# per request; end-to-end latency is unchanged, a request's generated tokens
+# are its model output length + 1, and its first token is the end of the first
+# processing.  Time model 10 ms + 5e-5 ms per cached token, KV budget 137,000
+# tokens (an A100 80 GB serving Llama-2-7B after weights and a 1 % margin).
+PD_CONTEXT, PD_DECODE = 630, 20
+PD_RATES = [0.10 + 0.05 * i for i in range(9)]     # 100-500 requests/s, per ms
+# WAIT thresholds ceil(n*) with n* = lam d0 / (1 - d1 lam (l'+1)(l + l'/2))
+# (single-type fluid model), computed once per rate; a CPU test recomputes them.
+PD_THRESHOLDS = [2, 2, 3, 3, 4, 5, 6, 7, 8]
+
+
+def config_pd(replicas: int = 1024, record_capacity: int = 1 << 15) -> List[Job]:
+    """Decode-only p630d20 at 9 rates: WAIT with the fluid thresholds, then
+    FCFS with a 1 % admission reserve (the decode-only baseline), on the same
+    replica streams."""
+    jobs = []
+    for pol in ("wait", "fcfs"):
+        for lam, n in zip(PD_RATES, PD_THRESHOLDS):
+            wl = Workload(prompt_len=[PD_CONTEXT], lam=[lam], d0=10.0, d1=5e-5, C=137000,
+                          policy=pol, n=[n] if pol == "wait" else [],
+                          out_len=[PD_DECODE - 1], reserve=0.01 if pol == "fcfs" else 0.0,
+                          hist_edges=default_edges(10.0), record_capacity=record_capacity)
+            jobs.append(Job(wl, 0, ids(replicas)))
+    return jobs
+
+
 # ------------------------------------------------- time-varying rates ----
 
 
