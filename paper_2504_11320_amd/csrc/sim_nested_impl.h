@@ -915,6 +915,8 @@ hipError_t launch_ml(const KArgs &A, hipStream_t s) {
     hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 16, TV>), g, b, 0, s, A);
   else if (A.lanes == 8)
     hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 8, TV>), g, b, 0, s, A);
+  else if (A.lanes == 4)
+    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 4, TV>), g, b, 0, s, A);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

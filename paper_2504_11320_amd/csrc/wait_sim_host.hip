@@ -58,13 +58,18 @@ int fail(int code, const std::string &msg) {
 // Replicas per 64-lane wavefront.  A replica is a serial chain of events, so
 // a wavefront's time per batch is set by latency, not by how many of its lanes
 // are busy: when a launch has few replicas they are spread over more
-// wavefronts (64, 32, 16 or 8 per wavefront) until the launch has at least
-// kTargetWaves wavefronts or reaches 8 per wavefront.  A wavefront never has
-// more lanes than the largest job has replicas (fewer lanes, less LDS).
+// wavefronts (64, 32, 16 or 8 per wavefront; Nested WAIT 32 down to 4) until
+// the launch has at least the target number of wavefronts or reaches the
+// smallest width.  The WAIT/FCFS kernel targets one wavefront per SIMD (1024):
+// a second one per SIMD costs more in LDS occupancy than it hides.  The Nested
+// WAIT kernel, which waits on dependent loads of records, targets two per SIMD
+// (2048).  A wavefront never has more lanes than the largest job has replicas
+// (fewer lanes, less LDS).
 #ifndef WS_TARGET_WAVES
 #define WS_TARGET_WAVES 1024
 #endif
 constexpr int64_t kTargetWaves = WS_TARGET_WAVES;
+constexpr int64_t kTargetWavesNested = 2 * WS_TARGET_WAVES;
 
 int ceil_log2(uint64_t x) {
   int k = 0;
@@ -345,9 +350,11 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
       if (launch_kind(jobs[i].pol) == pk) nmax = std::max(nmax, jobs[i].n);
     // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32
     int lanes = pk == WS_NESTED_WAIT ? 32 : 64;
+    const int min_lanes = pk == WS_NESTED_WAIT ? 4 : 8;
+    const int64_t target = pk == WS_NESTED_WAIT ? kTargetWavesNested : kTargetWaves;
     if (!any_trace || pk == WS_NESTED_WAIT) {  // known-length replays keep 64
-      while (lanes > 8 && lanes / 2 >= nmax) lanes /= 2;
-      while (lanes > 8 && waves(lanes) < kTargetWaves) lanes /= 2;
+      while (lanes > min_lanes && lanes / 2 >= nmax) lanes /= 2;
+      while (lanes > min_lanes && waves(lanes) < target) lanes /= 2;
     }
     Lo.lanes[pk] = lanes;
     const int64_t count = waves(lanes) * 64;
