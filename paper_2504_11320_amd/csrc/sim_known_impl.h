@@ -68,8 +68,10 @@ sim_known_kernel(KArgs A) {
   __shared__ uint64_t s_seed[LN];
   __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
   // The last WB records pushed on each resident deque are also kept in LDS,
-  // so LIFO evictions (which pop the back) rarely read HBM.
-  constexpr int WB = MT <= 4 ? 16 : 2;
+  // so LIFO evictions (which pop the back) rarely read HBM.  Launches with
+  // time-varying rates run two wavefronts per SIMD at 16 replicas each; a
+  // window of 8 lets eight workgroups share a CU's LDS.
+  constexpr int WB = MT <= 4 ? (TV && LN <= 16 ? 8 : 16) : 2;
   __shared__ DRec s_win[MT][WB][LN];
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

@@ -61,9 +61,10 @@ int fail(int code, const std::string &msg) {
 // wavefronts (64, 32, 16 or 8 per wavefront; Nested WAIT 32 down to 4) until
 // the launch has at least the target number of wavefronts or reaches the
 // smallest width.  The WAIT/FCFS kernel targets one wavefront per SIMD (1024):
-// a second one per SIMD costs more in LDS occupancy than it hides.  The Nested
-// WAIT kernel, which waits on dependent loads of records, targets two per SIMD
-// (2048).  A wavefront never has more lanes than the largest job has replicas
+// a second one per SIMD gains nothing there; with time-varying rates (longer
+// chains of dependent LDS reads per arrival) it targets two per SIMD.  The
+// Nested WAIT kernel, which waits on dependent loads of records, targets two
+// per SIMD (2048).  A wavefront never has more lanes than the largest job has replicas
 // (fewer lanes, less LDS).
 #ifndef WS_TARGET_WAVES
 #define WS_TARGET_WAVES 1024
@@ -351,7 +352,11 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32
     int lanes = pk == WS_NESTED_WAIT ? 32 : 64;
     const int min_lanes = pk == WS_NESTED_WAIT ? 4 : 8;
-    const int64_t target = pk == WS_NESTED_WAIT ? kTargetWavesNested : kTargetWaves;
+    bool any_tv = false;
+    for (int i = 0; i < n_jobs; ++i)
+      any_tv |= launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_rate_pts > 0;
+    const int64_t target =
+        pk == WS_NESTED_WAIT || any_tv ? kTargetWavesNested : kTargetWaves;
     if (!any_trace || pk == WS_NESTED_WAIT) {  // known-length replays keep 64
       while (lanes > min_lanes && lanes / 2 >= nmax) lanes /= 2;
       while (lanes > min_lanes && waves(lanes) < target) lanes /= 2;
