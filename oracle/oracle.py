@@ -15,7 +15,13 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "wait_oracle.c")
+HDR = os.path.join(HERE, "wait_oracle.h")
 LIB = os.path.join(HERE, "liboracle.so")
+
+
+def _stale() -> bool:
+    return (not os.path.exists(LIB)
+            or os.path.getmtime(LIB) < max(os.path.getmtime(SRC), os.path.getmtime(HDR)))
 
 POLICY = {"wait": 0, "nested": 1, "fcfs": 2, "wait-nowait": 3}
 FLAG_CAPACITY, FLAG_STALL, FLAG_OVERFLOW, FLAG_THIN_LIMIT = 1, 2, 4, 8
@@ -39,6 +45,7 @@ class _Config(C.Structure):
         ("policy", C.c_int32), ("n", C.c_void_p), ("nseg", C.c_int32),
         ("seg_end", C.c_void_p), ("reserve", C.c_double),
         ("n_rate_pts", C.c_int32), ("rate_t", C.c_void_p), ("rate_f", C.c_void_p),
+        ("chunk", C.c_int32),
     ]
 
 
@@ -65,7 +72,7 @@ _lib = None
 
 def build(force: bool = True) -> str:
     """Compile the oracle (plain C, -O2, no FP contraction, no fast-math)."""
-    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+    if force or _stale():
         cmd = ["gcc", "-O2", "-std=gnu11", "-Wall", "-ffp-contract=off",
                "-fno-fast-math", "-fPIC", "-shared", "-o", LIB + ".tmp", SRC,
                "-lpthread", "-lm"]
@@ -77,7 +84,7 @@ def build(force: bool = True) -> str:
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        if _stale():
             build(force=True)
         L = C.CDLL(LIB)
         L.oracle_run.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_uint32,
@@ -148,6 +155,7 @@ class _Pinned:
         else:
             c.seg_end, c.nseg = None, 0
         c.reserve = float(wl.reserve)
+        c.chunk = int(getattr(wl, "chunk", 0) or 0)
         if getattr(wl, "rate_t", None) is not None:
             rt = arr(wl.rate_t, np.float64)
             rf = arr(np.asarray(wl.rate_f, dtype=np.float64).reshape(wl.m, len(rt)),

@@ -22,7 +22,17 @@
  *     Algorithm 4 (Appendix B.1), with coarse segments (Appendix A, segment
  *     design);
  *   - FCFS: Section 4.1, with the exact behaviour spelled out in the proof of
- *     Proposition 3.
+ *     Proposition 3; optionally with chunked prefill (the Sarathi-style
+ *     baseline of Section 6: at most `chunk` prefill tokens per iteration,
+ *     partial prefills interleaved with decodes).  Reading: the budget goes
+ *     first to the partially prefilled prompt (at most one exists: it is the
+ *     last one admitted), then to admissions from the queue head, each taking
+ *     min(its remaining prompt, the budget left); admission still checks the
+ *     whole prompt against C minus the reserve; a chunk that brings a prompt
+ *     to p cached tokens charges p in the iteration time (the cache after it,
+ *     as a whole prefill charges l); a partial prompt holds p tokens, is the
+ *     most recently admitted for LIFO repair, and restarts from scratch when
+ *     evicted; the prompt reaches stage 1 when its last chunk is processed.
  *
  * Readings of points the paper leaves open (they are the model contract and
  * are listed with their evidence in the design notes):
@@ -227,7 +237,7 @@ static void vec_push(vec_t *a, int64_t x) {
 
 /* ------------------------------------------------------------ state ---- */
 
-enum { LOC_FREE = 0, LOC_QUEUE = 1, LOC_INT = 2, LOC_BND = 3 };
+enum { LOC_FREE = 0, LOC_QUEUE = 1, LOC_INT = 2, LOC_BND = 3, LOC_PRE = 4 };
 
 typedef struct {
   double a;     /* arrival time                                  */
@@ -239,6 +249,8 @@ typedef struct {
   int32_t seg;  /* Nested: segment (1-based) of LOC_INT/LOC_BND  */
   int32_t sel;  /* selected in the batch being formed            */
   int32_t sp;   /* processing stage when selected                */
+  int32_t pp;   /* LOC_PRE: prompt tokens cached so far          */
+  int32_t cq;   /* prefill tokens processed in the current batch */
   int64_t kb;   /* admission key: batch of last prefill          */
   int64_t kp;   /* admission key: position within that batch    */
   int64_t id;   /* request id (arrival order)                    */
@@ -319,6 +331,7 @@ static int64_t charge(const sim_t *S, const req_t *r) {
   int64_t l = c->l[r->j];
   if (r->loc == LOC_INT) return l + r->s;
   if (r->loc == LOC_BND) return l + c->seg_end[r->seg - 2];
+  if (r->loc == LOC_PRE) return r->pp;
   return 0;
 }
 
@@ -568,17 +581,41 @@ static int decide_wait(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
 /* FCFS: batch every resident prompt, then admit from the head of the
  * external FIFO while the launch memory stays within C minus the reserve;
  * stop at the first prompt that does not fit. */
+/* Select a prefill chunk of cq tokens for request r (cached before: pp). */
+static void select_chunk(sim_t *S, int64_t r, int32_t cq, int64_t *tokens) {
+  req_t *q = &S->R[r];
+  q->sel = 1;
+  q->sp = 0;
+  q->cq = cq;
+  vec_push(&S->sel, r);
+  *tokens += (int64_t)q->pp + cq;
+}
+
 static int decide_fcfs(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   const or_config *c = S->cfg;
   if (S->res.len == 0 && S->q[0].len == 0) return 0;
   ensure_tmp(S, S->res.len);
-  for (int64_t i = 0; i < S->res.len; i++) S->tmp[i] = S->res.v[i];
+  int64_t cnt = 0, part = -1;
+  for (int64_t i = 0; i < S->res.len; i++) {
+    if (S->R[S->res.v[i]].loc == LOC_PRE)
+      part = S->res.v[i];
+    else
+      S->tmp[cnt++] = S->res.v[i];
+  }
   t_sort_R = S->R;
-  qsort(S->tmp, (size_t)S->res.len, sizeof(int64_t), cmp_stage_key);
-  for (int64_t i = 0; i < S->res.len; i++)
-    select_req(S, S->tmp[i], S->R[S->tmp[i]].s, tokens);
+  qsort(S->tmp, (size_t)cnt, sizeof(int64_t), cmp_stage_key);
+  for (int64_t i = 0; i < cnt; i++) select_req(S, S->tmp[i], S->R[S->tmp[i]].s, tokens);
+  /* prefill budget of this iteration */
+  int64_t budget = c->chunk > 0 ? c->chunk : INT64_MAX;
+  if (part >= 0) {
+    const int64_t rest = c->l[S->R[part].j] - S->R[part].pp;
+    const int32_t cq = (int32_t)(rest < budget ? rest : budget);
+    budget -= cq;
+    select_chunk(S, part, cq, tokens);
+    *prefill_l += cq;
+  }
   int64_t p = 0;
-  while (S->q[0].len > 0) {
+  while (S->q[0].len > 0 && budget > 0) {
     int64_t r = dq_at(&S->q[0], 0);
     int64_t l = c->l[S->R[r].j];
     if (S->Mres + *prefill_l + l > c->C - S->reserve_tok) break;
@@ -586,8 +623,11 @@ static int decide_fcfs(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
     S->R[r].kb = S->b;
     S->R[r].kp = p++;
     S->R[r].s = 0;
-    select_req(S, r, 0, tokens);
-    *prefill_l += l;
+    S->R[r].pp = 0;
+    const int32_t cq = (int32_t)(l < budget ? l : budget);
+    budget -= cq;
+    select_chunk(S, r, cq, tokens);
+    *prefill_l += cq;
   }
   return S->sel.len > 0;
 }
@@ -724,6 +764,9 @@ static void evict(sim_t *S, int64_t r, int fallback) {
   if (q->loc == LOC_BND) {
     gen = S->cfg->seg_end[q->seg - 2];
     remove_boundary(S, r);
+  } else if (q->loc == LOC_PRE) {
+    gen = 0;
+    remove_resident(S, r);
   } else {
     gen = q->s - 1;
     remove_resident(S, r);
@@ -735,6 +778,7 @@ static void evict(sim_t *S, int64_t r, int fallback) {
   q->s = 0;
   q->seg = 0;
   q->sel = 0;
+  q->pp = 0;
   push_queue(S, r);
 }
 
@@ -768,6 +812,21 @@ static void transition(sim_t *S, double t_end) {
     int64_t l = c->l[q->j];
     int32_t sp = q->sp;
     q->sel = 0;
+    if (sp == 0 && c->policy == OR_FCFS) { /* a prefill chunk (or a whole prefill) */
+      const int64_t old = charge(S, q);
+      const int32_t after = q->pp + q->cq;
+      if (q->loc != LOC_PRE) vec_push(&S->res, r);
+      if (after == l) { /* prefill done: resident at stage 1 */
+        q->loc = LOC_INT;
+        q->s = 1;
+        q->pp = 0;
+      } else {
+        q->loc = LOC_PRE;
+        q->pp = after;
+      }
+      S->Mres += charge(S, q) - old;
+      continue;
+    }
     if (sp == 0) { /* prefill done: resident at stage 1 */
       q->loc = LOC_INT;
       q->s = 1;

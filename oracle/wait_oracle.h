@@ -61,6 +61,8 @@ typedef struct {
   int32_t n_rate_pts;
   const double *rate_t;
   const double *rate_f;
+  int32_t chunk;            /* FCFS: prefill tokens per iteration (chunked
+                               prefill), 0 = whole prefills                   */
 } or_config;
 
 typedef struct {

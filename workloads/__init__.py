@@ -39,6 +39,7 @@ class Workload:
     out_cdf: Optional[np.ndarray] = None     # uint32 [m, out_cap-1]
     seg_end: Optional[List[int]] = None      # Nested: r_1 < ... < r_L
     reserve: float = 0.0                     # FCFS admission reserve (fraction of C)
+    chunk: int = 0                           # FCFS prefill tokens per iteration (0: whole)
     hist_edges: Optional[np.ndarray] = None  # latency histogram edges (ms)
     record_capacity: int = 1 << 15           # external-queue capacity
     trace: Optional[tuple] = None            # (times f64, types i32, lengths i32)
