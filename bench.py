@@ -171,6 +171,11 @@ def _workloads():
                       "context, 20 generated tokens), WAIT with fluid thresholds and FCFS "
                       "with a 1% reserve, 9 rates 0.1-0.5/ms, 1024 replicas each",
                       lambda reps: W.config_pd(replicas=reps), 100000, "wait+fcfs", [8, 17]),
+        "fcfs-chunked": ("FCFS with a 1% reserve and 512-token chunked prefill (the "
+                         "Sarathi-style baseline) on the Llama-2-7B-shaped 3-type mix, 32 "
+                         "rates 0.5-1.2x fluid boundary, 1024 replicas each",
+                         lambda reps: W.config_chunked(replicas=reps), 100000, "fcfs",
+                         [0, 31]),
         "wait-small": ("WAIT, 2 types (16/8, 32/16), C = 2048, 64 replicas",
                        lambda reps: W.config1(), 10000, "wait", [0]),
     }
@@ -210,7 +215,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="wait-llama",
                     help="wait-llama (the benchmark), nested-geometric, wait-sweep, "
-                         "nested-heavytail, nowait-llama, wait-cyclic, pd-decode, wait-small")
+                         "nested-heavytail, nowait-llama, wait-cyclic, pd-decode, "
+                         "fcfs-chunked, wait-small")
     ap.add_argument("--horizon", type=int, default=0, help="batches (0: the workload's)")
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")

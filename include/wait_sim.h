@@ -17,7 +17,8 @@
  *     recently admitted prompt, which restarts from prefill;
  *   - policies: WAIT (Algorithm 1, Section 4.2), Nested WAIT (Algorithm 2,
  *     Section 5.1; event-driven form Algorithm 4, Appendix B.1) and the greedy
- *     FCFS evict-on-overflow baseline (Section 4.1);
+ *     FCFS evict-on-overflow baseline (Section 4.1), optionally with chunked
+ *     prefill (Section 6);
  *   - metrics: effective throughput, latency and time to first token
  *     censored at the horizon T (Section 2.4).
  *
@@ -142,6 +143,15 @@ typedef struct {
   int32_t L;             /* NESTED: number of segments, 1..WS_MAX_SEGMENTS   */
   const int32_t *seg_end;/* NESTED: r_1 < ... < r_L, r_L = largest output    */
   double fcfs_reserve;   /* FCFS: fraction of C kept free at admission, [0,1)*/
+  int32_t fcfs_chunk;    /* FCFS: chunked prefill (the Sarathi-style baseline
+                            of Section 6): at most this many prefill tokens
+                            per iteration, the partially prefilled prompt
+                            first, then admissions from the queue head, each
+                            taking min(its remaining prompt, the budget
+                            left); a chunk charges the prompt's cache after
+                            it; a partial prompt holds its cached tokens, is
+                            evicted first and restarts.  0: whole prefills.
+                            Must be 0 for the other policies.             */
 } ws_policy;
 
 /* One replica's random stream. */

@@ -47,7 +47,8 @@ class WsConfig(C.Structure):
 
 class WsPolicy(C.Structure):
     _fields_ = [("kind", C.c_int32), ("n", C.c_void_p), ("L", C.c_int32),
-                ("seg_end", C.c_void_p), ("fcfs_reserve", C.c_double)]
+                ("seg_end", C.c_void_p), ("fcfs_reserve", C.c_double),
+                ("fcfs_chunk", C.c_int32)]
 
 
 class WsStream(C.Structure):
@@ -152,6 +153,7 @@ class JobArray:
             pol.L = len(wl.seg_end) if wl.seg_end is not None else 0
             pol.seg_end = None if wl.seg_end is None else self._a(wl.seg_end, np.int32)
             pol.fcfs_reserve = float(wl.reserve)
+            pol.fcfs_chunk = int(getattr(wl, "chunk", 0) or 0)
             ids = np.asarray(job.replica_ids, dtype=np.uint32)
             st = (WsStream * max(1, len(ids)))()
             for x, rid in enumerate(ids):

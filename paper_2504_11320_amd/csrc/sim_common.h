@@ -27,6 +27,8 @@ struct JobDev {
   int32_t nseg, known, qcap_log2, rec_cap;
   int32_t nowait;  // WAIT: serve without waiting for a full cohort
   int32_t n_rate;  // rate-profile points (0: constant rates)
+  int32_t chunk;   // FCFS: prefill tokens per iteration (0: whole prefills)
+  int32_t pad_;
   double d0, d1;
   int64_t C, reserve_tok;
   int64_t n_trace;
@@ -56,6 +58,7 @@ enum Slot : int {
   S_T = 0, S_LAT, S_TTFT, S_LATSUM, S_MEM, S_BUSY,          // f64
   S_BATCHES, S_ARR, S_COMP, S_CTOK, S_EVICT, S_ETOK, S_FALLBACK, S_BTOK,
   S_PEAK, S_IDLE, S_N, S_U, S_MRES, S_TRIDX, S_FLAGS, S_PENDFT,
+  S_PARTA, S_PARTJ, S_PARTPP,        // FCFS chunked prefill: the partial prompt
   S_TNEXT,                           // + kMaxTypes f64: next arrival time
   S_K = S_TNEXT + kMaxTypes,         // arrival index of the pending arrival
   S_LNEXT = S_K + kMaxTypes,         // output length of the pending arrival

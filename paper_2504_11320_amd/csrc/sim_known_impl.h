@@ -88,6 +88,8 @@ sim_known_kernel(KArgs A) {
   const double d0 = J->d0, d1 = J->d1;
   const int32_t C = (int32_t)J->C;  // <= 2^30
   const int32_t cap_adm = (int32_t)(J->C - J->reserve_tok);
+  // FCFS with chunked prefill: prefill tokens per iteration (0: whole)
+  const int32_t chunk = WAIT ? 0 : J->chunk;
   const int n_hist = J->n_hist;
   const int P = TV ? J->n_rate : 0;  // rate-profile points, 0 for constant rates
   const bool tv = TV && P > 0;
@@ -170,6 +172,11 @@ sim_known_kernel(KArgs A) {
   int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, Mres, tridx;
   int32_t N, U;  // requests in system, and those without a first token
   uint32_t flags;
+  // FCFS chunked prefill: the partially prefilled prompt (at most one, the
+  // last admitted), outside the deques until its last chunk: arrival time
+  // with first-token flag, type (-1: none) and prompt tokens cached so far
+  double part_a;
+  int32_t part_j, part_pp;
 
   uint32_t bidx_cur = 0;  // index of the batch being formed
 
@@ -182,6 +189,9 @@ sim_known_kernel(KArgs A) {
     batches = arrivals = comps = ctok = evicts = etok = btok = peak = idle = 0;
     N = U = Mres = tridx = 0;
     flags = 0;
+    part_a = 0.0;
+    part_j = -1;
+    part_pp = 0;
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
       kk[j] = qh[j] = qt[j] = dh[j] = dt[j] = svc[j] = pend[j] = 0;
@@ -219,6 +229,9 @@ sim_known_kernel(KArgs A) {
     Mres = slot_i(A, S_MRES, r);
     tridx = slot_i(A, S_TRIDX, r);
     flags = (uint32_t)slot_i(A, S_FLAGS, r);
+    part_a = slot_f(A, S_PARTA, r);
+    part_j = (int32_t)slot_i(A, S_PARTJ, r);
+    part_pp = (int32_t)slot_i(A, S_PARTPP, r);
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
       tnext[j] = slot_f(A, S_TNEXT + j, r);
@@ -543,7 +556,7 @@ sim_known_kernel(KArgs A) {
         uint32_t resident = 0;
 #pragma unroll
         for (int j = 0; j < MT; ++j) resident += dt[j] - dh[j];
-        if (resident > 0 || qt[0] != qh[0]) elig = 1;
+        if (resident > 0 || qt[0] != qh[0] || part_j >= 0) elig = 1;
       }
       if (elig) break;
       int jn;
@@ -596,6 +609,52 @@ sim_known_kernel(KArgs A) {
         fresh[j] = (uint32_t)na;
         tokens += (int64_t)na * l[j] + Mj[j];
         prefill_l += (int64_t)na * l[j];
+      }
+    } else if (chunk > 0) {
+      // chunked prefill: the partial prompt first, then admissions from the
+      // head of the queue, within `chunk` prefill tokens; a chunk charges the
+      // prompt's cache after it
+      tokens = Mres - part_pp;  // decode residents
+      uint32_t p = 0;
+      int32_t budget = chunk;
+      if (part_j >= 0) {
+        const int32_t pl = pick(l, part_j);
+        const int32_t cq = min(pl - part_pp, budget);
+        budget -= cq;
+        const int32_t after = part_pp + cq;
+        tokens += after;
+        prefill_l += cq;
+        if (after == pl) {  // last chunk: a fresh resident of its type
+          dpush_dyn(part_j, part_a, bidx, p++);
+          place(fresh, part_j, pick(fresh, part_j) + 1u);
+          place(pendnew, part_j, pick(pendnew, part_j) + (has_ft(part_a) ? 0u : 1u));
+          part_j = -1;
+          part_pp = 0;
+        } else {
+          part_pp = after;
+        }
+      }
+      while (qt[0] != qh[0] && budget > 0) {
+        const QRec head = q0src ? q0pu : q0ld;
+        const int hj = head.j;
+        const int32_t hl = pick(l, hj);
+        if (Mres + prefill_l + hl > cap_adm) break;
+        qh[0]++;
+        q0src = false;
+        q0ld = qring0()[qh[0] & qmask];
+        const int32_t cq = min(hl, budget);
+        budget -= cq;
+        tokens += cq;
+        prefill_l += cq;
+        if (cq == hl) {
+          dpush_dyn(hj, head.a_ft, bidx, p++);
+          place(fresh, hj, pick(fresh, hj) + 1u);
+          place(pendnew, hj, pick(pendnew, hj) + (has_ft(head.a_ft) ? 0u : 1u));
+        } else {  // the budget ends inside this prompt
+          part_a = head.a_ft;
+          part_j = hj;
+          part_pp = cq;
+        }
       }
     } else {
       tokens = Mres;
@@ -667,12 +726,20 @@ sim_known_kernel(KArgs A) {
       Mj[j] += (int32_t)(before - done) + (int32_t)fresh[j] * (l[j] + 1) -
                (int32_t)done * (l[j] + lp[j]);
     }
-    Mres = 0;
+    Mres = WAIT ? 0 : part_pp;
 #pragma unroll
     for (int j = 0; j < MT; ++j) Mres += Mj[j];
     if (Mres > peak) peak = Mres;
 
     // ---- repair: evict the most recently admitted resident ------------
+    // (FCFS: a partially prefilled prompt first; it restarts from scratch)
+    if (!WAIT && part_j >= 0 && Mres > C) {
+      Mres -= part_pp;
+      evicts++;
+      push_fcfs(part_a, part_j, pick(lp, part_j));
+      part_j = -1;
+      part_pp = 0;
+    }
     while (Mres > C) {
       int jb = -1;
       uint32_t bb = 0, bp = 0;
@@ -710,6 +777,9 @@ sim_known_kernel(KArgs A) {
   put_i(A, S_COMP, r, comps);
   put_i(A, S_CTOK, r, ctok);
   put_i(A, S_EVICT, r, evicts);
+  put_f(A, S_PARTA, r, part_a);
+  put_i(A, S_PARTJ, r, part_j);
+  put_i(A, S_PARTPP, r, part_pp);
   put_i(A, S_ETOK, r, etok);
   put_i(A, S_FALLBACK, r, 0);
   put_i(A, S_BTOK, r, btok);
@@ -738,11 +808,13 @@ template <int MT, int POL, bool TV>
 hipError_t launch_mt(const KArgs &A, hipStream_t s) {
   const int blocks = (A.n_list + 63) / 64;
   const dim3 g(blocks), b(64);
-  if (TV && A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
-    if (A.lanes != 64) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64, TV>), g, b, 0, s, A);
-  } else if (A.any_trace) {
-    return hipErrorInvalidValue;  // replays run on the TV kernels
+  if (A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
+    if constexpr (TV) {
+      if (A.lanes != 64) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64, TV>), g, b, 0, s, A);
+    } else {
+      return hipErrorInvalidValue;  // replays run on the TV kernels
+    }
   } else if (A.lanes == 64) {
     hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64, TV>), g, b, 0, s, A);
   } else if (A.lanes == 32) {

@@ -38,6 +38,7 @@ __global__ void __launch_bounds__(256) export_kernel(KArgs A, uint8_t *out) {
     }
   } else {
     for (int j = 0; j < J.m; ++j) resident += slot_i(A, S_DT + j, r) - slot_i(A, S_DH + j, r);
+    if (J.policy == WS_FCFS && slot_i(A, S_PARTJ, r) >= 0) resident += 1;  // partial prefill
   }
   oi[9 * R + r] = waiting;
   oi[10 * R + r] = resident;
@@ -196,6 +197,8 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
   }
   int64_t reserve_tok = 0;
+  if (kind != WS_FCFS && p.fcfs_chunk != 0)
+    return fail(WS_EINVAL, at + "fcfs_chunk applies to FCFS only");
   if (kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
     return fail(WS_EUNSUPPORTED, at + "WAIT and FCFS take at most " +
                                      std::to_string(WS_MAX_TYPES_KNOWN) + " request types");
@@ -208,6 +211,7 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     if (!(p.fcfs_reserve >= 0.0 && p.fcfs_reserve < 1.0))
       return fail(WS_EINVAL, at + "fcfs_reserve must be in [0,1)");
     reserve_tok = (int64_t)std::ceil(p.fcfs_reserve * (double)c.C);
+    if (p.fcfs_chunk < 0) return fail(WS_EINVAL, at + "fcfs_chunk must be >= 0");
     for (int j = 0; j < c.m; ++j)
       if (c.prompt_len[j] > c.C - reserve_tok)
         return fail(WS_EINVAL, at + "a prompt does not fit below the FCFS reserve");
@@ -236,6 +240,7 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   d.m = c.m;
   d.policy = kind;
   d.nowait = p.kind == WS_WAIT_NOWAIT ? 1 : 0;
+  d.chunk = kind == WS_FCFS ? p.fcfs_chunk : 0;
   d.n_hist = c.n_hist;
   d.out_cap = c.out_cap;
   d.nseg = kind == WS_NESTED_WAIT ? p.L : 0;

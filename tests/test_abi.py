@@ -118,3 +118,12 @@ def test_rate_profile_validation():
     tr = W.trace_workload("wait", [16], [4], 5.0, 0.01, 1000, [1], [0.0], [0])
     tr.rate_t, tr.rate_f = np.array([0.0]), np.array([[1.0]])
     assert _err([W.Job(tr, 0, W.ids(1))]).code == B.WS_EINVAL
+
+
+def test_chunk_validation():
+    """fcfs_chunk >= 0, FCFS only."""
+    from paper_2504_11320_amd import binding as B
+    fc = _job(policy="fcfs", n=[], chunk=-1)
+    assert _err(fc).code == B.WS_EINVAL
+    assert _err(_job(chunk=64)).code == B.WS_EINVAL        # WAIT
+    assert B.workspace_bytes(B.JobArray(_job(policy="fcfs", n=[], chunk=64))) > 0

@@ -218,6 +218,18 @@ def config5(replicas: int = 8192, record_capacity: int = 1 << 18) -> List[Job]:
     return [Job(wl, 0, ids(replicas))]
 
 
+def config_chunked(replicas: int = 1024, n_rates: int = 32, chunk: int = 512,
+                   record_capacity: int = 1 << 15) -> List[Job]:
+    """The Sarathi-style baseline of Section 6 on the Llama-shaped mix:
+    config2's types and rates under FCFS with a 1 % admission reserve and
+    chunked prefill (at most `chunk` prefill tokens per iteration)."""
+    jobs = []
+    for j in config2(replicas, n_rates, None, record_capacity):
+        wl = dataclasses.replace(j.wl, policy="fcfs", n=[], reserve=0.01, chunk=chunk)
+        jobs.append(Job(wl, j.seed, j.replica_ids))
+    return jobs
+
+
 # ------------------------------------- decode-only (PD-disaggregated) ----
 
 # A decode server behind a separate prefill service receives each request with
