@@ -52,6 +52,8 @@ PROFILES = {
                          ("sim_nested_impl.h", "sim_nested.hip", "sim_common.h")),
     "nested-heavytail": ("sim_nested_10type_lognormal_8192x1e6",
                          ("sim_nested_impl.h", "sim_nested.hip", "sim_common.h")),
+    "fcfs-chunked": ("sim_known_fcfs_3type_chunk512_32x1024x1e5",
+                     ("sim_known_impl.h", "sim_known_fcfs.hip", "sim_common.h")),
 }
 
 
