@@ -1,5 +1,5 @@
-"""Full-size launches of the Nested WAIT, policy-sweep, heavy-tailed and
-cyclic time-varying workloads, exactly as configured (every replica, the full horizon, one
+"""Full-size launches of the Nested WAIT, policy-sweep, heavy-tailed, cyclic
+time-varying, chunked-prefill FCFS and decode-only workloads, exactly as configured (every replica, the full horizon, one
 launch): properties that hold for every replica are checked on all of them,
 and sampled replicas are recomputed one by one by the oracle and compared
 field by field (integers exact, fp64 within 1e-12 relative)."""
@@ -107,3 +107,24 @@ def test_cyclic_full_size(B):
     _invariants(g, 100000, "cyclic")
     picks = [(0, 0), (0, 1023), (15, 511), (31, 7), (31, 1000)]
     _sampled(g, jobs, 100000, picks, "cyclic full size")
+
+
+def test_fcfs_chunked_full_size(B):
+    """FCFS with a 1 % reserve and 512-token chunked prefill on the
+    Llama-shaped mix: 32 rates x 1024 replicas x 1e5 batches, the benchmark's
+    launch."""
+    jobs = W.config_chunked()
+    g = _run(B, jobs, 100000, "fcfs-chunked full size")
+    _invariants(g, 100000, "fcfs-chunked")
+    picks = [(0, 0), (16, 512), (31, 1023)]
+    _sampled(g, jobs, 100000, picks, "fcfs-chunked full size")
+
+
+def test_pd_decode_full_size(B):
+    """Decode-only p630d20, WAIT and FCFS at 9 rates x 1024 replicas x 1e5
+    batches."""
+    jobs = W.config_pd()
+    g = _run(B, jobs, 100000, "pd-decode full size")
+    _invariants(g, 100000, "pd-decode")
+    picks = [(0, 0), (8, 1023), (9, 5), (17, 700)]
+    _sampled(g, jobs, 100000, picks, "pd-decode full size")

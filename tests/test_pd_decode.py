@@ -3,7 +3,7 @@
 entering with a 630-token context and 20 tokens to generate is the model's
 type (l = 630, l' = 19).  Pinned by a single request's latency (the sum of
 its 20 decode steps over contexts 630..649) and by the fluid thresholds; the
-workload's constants are this build's (the appendix's simulator profiles are
+workload's time constants are chosen here (the appendix's simulator profiles are
 not available), so its latency comparison is not asserted."""
 import math
 
