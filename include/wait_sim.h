@@ -212,6 +212,29 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                      int32_t resume, void *d_workspace, size_t ws_bytes,
                      void *d_results, size_t results_bytes, void *hip_stream);
 
+/* Test hook: per-batch trace.  One record per replica and batch: the
+ * batch's launch time, duration, tokens,
+ * prefill processings (FCFS chunks included), selected prompts, completions,
+ * evictions before the launch (Nested WAIT's projected-state repair) and
+ * after the completion, and the resident memory, waiting and resident prompts
+ * after the repair. */
+typedef struct {
+  double t_launch, tau;
+  int64_t tokens, prefills, selected, completions, evict_pre, evict_post,
+      mem_after, waiting_after, resident_after, pad;
+} ws_batch_rec;
+
+/* wait_sim_advance, also writing ws_batch_rec records to d_btrace (DEVICE
+ * memory owned by the caller, btrace_cap records per replica, replica r's
+ * batch b at index r * btrace_cap + b, b counted from the replica's start
+ * across resumed calls; batches b >= btrace_cap are not recorded, records of
+ * batches not run are left as they are).  btrace_cap = 0: no trace.  Runs
+ * the kernels' general instantiations (slower than wait_sim_advance). */
+int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                            int32_t resume, void *d_workspace, size_t ws_bytes,
+                            void *d_results, size_t results_bytes, void *d_btrace,
+                            int64_t btrace_cap, void *hip_stream);
+
 /* prepare + advance(resume = 0) for one job. */
 int wait_sim_run(const ws_config *cfg, const ws_policy *pol,
                  const ws_stream *streams, int32_t n_replicas, int64_t horizon,

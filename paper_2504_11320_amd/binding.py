@@ -32,6 +32,13 @@ F64_FIELDS = ["t_end", "busy_time", "lat_area", "ttft_area",
               "lat_completed_sum", "mem_area"]
 
 
+# ws_batch_rec (include/wait_sim.h)
+BATCH_REC = np.dtype([("t_launch", np.float64), ("tau", np.float64)] + [
+    (f, np.int64) for f in ("tokens", "prefills", "selected", "completions", "evict_pre",
+                            "evict_post", "mem_after", "waiting_after", "resident_after",
+                            "pad")])
+
+
 class WsConfig(C.Structure):
     _fields_ = [
         ("m", C.c_int32), ("prompt_len", C.c_void_p), ("lam", C.c_void_p),
@@ -90,6 +97,9 @@ def lib():
                                    C.c_void_p, C.c_size_t, C.c_void_p]
         L.wait_sim_run_batch.argtypes = [jp, C.c_int32, C.c_int64, C.c_void_p,
                                          C.c_size_t, C.c_void_p, C.c_size_t, C.c_void_p]
+        L.wait_sim_advance_traced.argtypes = [jp, C.c_int32, C.c_int64, C.c_int32,
+                                              C.c_void_p, C.c_size_t, C.c_void_p,
+                                              C.c_size_t, C.c_void_p, C.c_int64, C.c_void_p]
         L.wait_sim_last_error.restype = C.c_char_p
         L.wait_sim_abi_version.restype = C.c_int
         if L.wait_sim_abi_version() != WS_ABI_VERSION:
@@ -225,6 +235,23 @@ class Simulation:
                                           1 if resume else 0, self.ws.data_ptr(),
                                           self.ws_bytes, self.res.data_ptr(), self.res_bytes,
                                           _stream_handle(self.torch, self.device)))
+
+    def advance_traced(self, horizon: int, btrace_cap: int, resume: bool = False) -> np.ndarray:
+        """advance() that also returns the per-batch trace: a structured array
+        [replicas][btrace_cap] of ws_batch_rec (records of batches not run are
+        zero)."""
+        if not self.prepared:
+            self.prepare()
+        torch = self.torch
+        nbytes = BATCH_REC.itemsize * self.R * int(btrace_cap)
+        buf = torch.zeros(max(nbytes, 1), dtype=torch.uint8, device=self.device)
+        with torch.cuda.device(self.device):
+            _check(lib().wait_sim_advance_traced(
+                self.ja.ptr, self.ja.n_jobs, int(horizon), 1 if resume else 0,
+                self.ws.data_ptr(), self.ws_bytes, self.res.data_ptr(), self.res_bytes,
+                buf.data_ptr(), int(btrace_cap), _stream_handle(torch, self.device)))
+        host = buf.cpu().numpy()[:nbytes]
+        return host.view(BATCH_REC).reshape(self.R, int(btrace_cap))
 
     def results(self) -> dict:
         """Per-replica results as numpy arrays (synchronises the stream)."""

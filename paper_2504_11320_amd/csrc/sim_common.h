@@ -89,7 +89,17 @@ struct KArgs {
   int32_t any_trace;   // some job of this launch replays a fixed arrival list
   int32_t any_tv;      // some job of this launch has time-varying rates
   int32_t lanes;       // replicas per wavefront (lanes >= this are padding)
+  uint8_t *btrace;     // per-batch trace [R][btrace_cap] records, or null
+  int64_t btrace_cap;
 };
+
+// One record of the per-batch trace (layout of ws_batch_rec).
+struct BatchRec {
+  double t_launch, tau;
+  int64_t tokens, prefills, selected, completions, evict_pre, evict_post, mem_after,
+      waiting_after, resident_after, pad;
+};
+static_assert(sizeof(BatchRec) == 96, "ws_batch_rec layout");
 
 __device__ __forceinline__ int64_t slot_i(const KArgs &A, int s, int64_t r) {
   return ((const int64_t *)(A.ws + A.off_state))[s * A.R + r];

@@ -588,6 +588,7 @@ sim_known_kernel(KArgs A) {
     const uint32_t bidx = (uint32_t)batches;
     bidx_cur = bidx;
     int64_t tokens = 0, prefill_l = 0;
+    int64_t bt_pre = 0;  // per-batch trace: prefill processings
 #pragma unroll
     for (int j = 0; j < MT; ++j) fresh[j] = pendnew[j] = 0;
     if (WAIT) {
@@ -607,6 +608,7 @@ sim_known_kernel(KArgs A) {
           pendnew[j] += has_ft(a_ft) ? 0u : 1u;
         }
         fresh[j] = (uint32_t)na;
+        bt_pre += na;
         tokens += (int64_t)na * l[j] + Mj[j];
         prefill_l += (int64_t)na * l[j];
       }
@@ -618,6 +620,7 @@ sim_known_kernel(KArgs A) {
       uint32_t p = 0;
       int32_t budget = chunk;
       if (part_j >= 0) {
+        bt_pre++;
         const int32_t pl = pick(l, part_j);
         const int32_t cq = min(pl - part_pp, budget);
         budget -= cq;
@@ -646,6 +649,7 @@ sim_known_kernel(KArgs A) {
         budget -= cq;
         tokens += cq;
         prefill_l += cq;
+        bt_pre++;
         if (cq == hl) {
           dpush_dyn(hj, head.a_ft, bidx, p++);
           place(fresh, hj, pick(fresh, hj) + 1u);
@@ -671,6 +675,7 @@ sim_known_kernel(KArgs A) {
         place(fresh, hj, pick(fresh, hj) + 1u);
         place(pendnew, hj, pick(pendnew, hj) + (has_ft(head.a_ft) ? 0u : 1u));
         prefill_l += hl;
+        bt_pre++;
       }
       tokens += prefill_l;
     }
@@ -698,10 +703,15 @@ sim_known_kernel(KArgs A) {
     t = t_end;
 
     // ---- completion transition ------------------------------------------
+    // (per-batch trace: selected prompts and completions of this batch)
+    int64_t bt_sel = 0;
+    const int64_t bt_comps0 = comps;
+    if constexpr (TV) bt_sel = !WAIT && part_j >= 0 ? 1 : 0;
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
       const bool served = WAIT ? ((elig >> j) & 1u) != 0 : j < m;
       if (!served) continue;
+      if constexpr (TV) bt_sel += dt[j] - dh[j];  // every resident of a served type
       // the stage-1 cohort produces its first tokens
       U -= pend[j];
       pend[j] = pendnew[j];
@@ -733,6 +743,7 @@ sim_known_kernel(KArgs A) {
 
     // ---- repair: evict the most recently admitted resident ------------
     // (FCFS: a partially prefilled prompt first; it restarts from scratch)
+    const int64_t bt_ev0 = evicts;
     if (!WAIT && part_j >= 0 && Mres > C) {
       Mres -= part_pp;
       evicts++;
@@ -760,6 +771,30 @@ sim_known_kernel(KArgs A) {
 #pragma unroll
       for (int j = 0; j < MT; ++j)
         if (jb == j) evict(j);
+    }
+    if constexpr (TV) {
+      if (A.btrace != nullptr && batches < A.btrace_cap) {
+        BatchRec br;
+        br.t_launch = t_end - tau;
+        br.tau = tau;
+        br.tokens = tokens;
+        br.prefills = bt_pre;
+        br.selected = bt_sel;
+        br.completions = comps - bt_comps0;
+        br.evict_pre = 0;
+        br.evict_post = evicts - bt_ev0;
+        br.mem_after = Mres;
+        int64_t w = 0, res = !WAIT && part_j >= 0 ? 1 : 0;
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+          if (WAIT || j == 0) w += qt[j] - qh[j];
+          res += dt[j] - dh[j];
+        }
+        br.waiting_after = w;
+        br.resident_after = res;
+        br.pad = 0;
+        ((BatchRec *)A.btrace)[r * A.btrace_cap + batches] = br;
+      }
     }
     batches++;
     btok += tokens;

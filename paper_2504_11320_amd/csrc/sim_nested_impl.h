@@ -636,6 +636,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const uint32_t bidx = (uint32_t)batches;
     int64_t tokens = 0, prefill_l = 0, mplus = Mres;
     int64_t pend_new = 0;
+    // per-batch trace: every interior prompt of a served segment and the
+    // entering cohorts are processed
+    int64_t bt_sel = 0;
+    const int64_t bt_ev0 = evicts;
+    if constexpr (TV)
+      for (int k = 0; k < kmax; ++k) bt_sel += (int64_t)s_I[k][tx] + s_seg[k].n;
     for (int k = 0; k < kmax; ++k) {
       const int32_t delta = s_seg[k].delta;
       const int32_t nk = s_seg[k].n;
@@ -757,6 +763,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       mplus -= freed;
     }
     if (mplus > C) flags |= kFlagOverflow;
+    const int64_t bt_ev1 = evicts;
+    const int64_t bt_comps0 = comps;
 
     const int64_t m_launch = Mres + prefill_l;
     if (m_launch > peak) peak = m_launch;
@@ -858,6 +866,29 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     // ---- repair: boundary prompts first, then interior prompts -------------
     while (Mres > C) {
       if (evict_lifo(0, true) == 0) break;
+    }
+    if constexpr (TV) {
+      if (A.btrace != nullptr && batches < A.btrace_cap) {
+        BatchRec br;
+        br.t_launch = t_end - tau;
+        br.tau = tau;
+        br.tokens = tokens;
+        br.prefills = s_seg[0].n;
+        br.selected = bt_sel;
+        br.completions = comps - bt_comps0;
+        br.evict_pre = bt_ev1 - bt_ev0;
+        br.evict_post = evicts - bt_ev1;
+        br.mem_after = Mres;
+        br.waiting_after = qt - qh;
+        int64_t res = 0;
+        for (int k = 0; k < L; ++k) {
+          res += s_I[k][tx];
+          if (k > 0) res += s_vt[k][tx] - s_vh[k][tx];
+        }
+        br.resident_after = res;
+        br.pad = 0;
+        ((BatchRec *)A.btrace)[r * A.btrace_cap + batches] = br;
+      }
     }
     batches++;
     btok += tokens;

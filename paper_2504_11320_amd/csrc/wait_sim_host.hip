@@ -541,6 +541,14 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
 int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                      int32_t resume, void *d_workspace, size_t ws_bytes,
                      void *d_results, size_t results_bytes, void *hip_stream) {
+  return wait_sim_advance_traced(jobs, n_jobs, horizon, resume, d_workspace, ws_bytes,
+                                 d_results, results_bytes, nullptr, 0, hip_stream);
+}
+
+int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                            int32_t resume, void *d_workspace, size_t ws_bytes,
+                            void *d_results, size_t results_bytes, void *d_btrace,
+                            int64_t btrace_cap, void *hip_stream) {
   g_err.clear();
   Layout Lo;
   int rc = make_layout(jobs, n_jobs, Lo);
@@ -549,10 +557,14 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
   if (!d_workspace || !d_results) return fail(WS_EINVAL, "device buffers must be non-NULL");
   if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
   if (results_bytes < results_size(Lo)) return fail(WS_EWORKSPACE, "result buffer too small");
+  if (btrace_cap < 0) return fail(WS_EINVAL, "btrace_cap must be >= 0");
+  if (btrace_cap > 0 && !d_btrace) return fail(WS_EINVAL, "d_btrace must be non-NULL");
   hipStream_t s = (hipStream_t)hip_stream;
   KArgs A = base_args(Lo, d_workspace);
   A.horizon = horizon;
   A.resume = resume ? 1 : 0;
+  A.btrace = btrace_cap > 0 ? (uint8_t *)d_btrace : nullptr;
+  A.btrace_cap = btrace_cap;
   for (int pk = 0; pk < 3; ++pk) {
     if (Lo.list_count[pk] == 0) continue;
     KArgs B = A;
