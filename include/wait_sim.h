@@ -206,7 +206,12 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
 
 /* Advance every replica of a prepared workspace by `horizon` batches.
  * resume = 0 starts every replica from the empty system at t = 0;
- * resume = 1 continues from the state the previous call left.  Asynchronous
+ * resume = 1 continues from the state the previous call left.
+ * Checkpoints: the workspace holds each replica's complete state (clock,
+ * counters, sums, queues and resident records, histogram); a byte copy of it
+ * taken between calls (device to device, or to host and back into a workspace
+ * of the same jobs) is a checkpoint, and resume = 1 on the restored copy
+ * continues exactly as the original would.  Asynchronous
  * on hip_stream; `jobs` must be the ones given to wait_sim_prepare. */
 int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                      int32_t resume, void *d_workspace, size_t ws_bytes,

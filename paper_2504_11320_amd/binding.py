@@ -236,6 +236,20 @@ class Simulation:
                                           self.ws_bytes, self.res.data_ptr(), self.res_bytes,
                                           _stream_handle(self.torch, self.device)))
 
+    def checkpoint(self, to_host: bool = False):
+        """A copy of the workspace (every replica's state) taken after the
+        calls issued so far: a device tensor, or host memory with to_host."""
+        self.torch.cuda.current_stream(self.device).synchronize()
+        return self.ws.cpu() if to_host else self.ws.clone()
+
+    def restore(self, state) -> None:
+        """Load a checkpoint of a Simulation of the same jobs; continue with
+        advance(..., resume=True)."""
+        if state.numel() != self.ws.numel():
+            raise ValueError("checkpoint of a different workspace layout")
+        self.ws.copy_(state.to(self.device))
+        self.prepared = True
+
     def advance_traced(self, horizon: int, btrace_cap: int, resume: bool = False) -> np.ndarray:
         """advance() that also returns the per-batch trace: a structured array
         [replicas][btrace_cap] of ws_batch_rec (records of batches not run are

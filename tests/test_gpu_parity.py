@@ -207,3 +207,24 @@ def test_rate_sweep_stability_point(sim):
     print(f"[gpu] sweep: lambda_hat / Lambda* = {lam_hat / W.LAM_STAR_C2:.3f}", flush=True)
     assert rates[0] <= lam_hat < rates[-1]
     assert comp[0] >= 0.95 * rates[0] and comp[-1] < 0.95 * rates[-1]
+
+
+def test_checkpoint_restore(sim):
+    """A workspace copy taken between calls is a checkpoint: restored into a
+    new Simulation of the same jobs (through host memory) and resumed, it ends
+    where the original run ends, bit for bit, for every policy."""
+    B = sim
+    from tests.test_gpu_random import random_workload
+    rng = np.random.default_rng(99)
+    jobs = [W.Job(random_workload(rng), 3, W.ids(9)) for _ in range(8)]
+    ref = B.run_batch(jobs, 1000)
+    a = B.Simulation(jobs)
+    a.prepare()
+    a.advance(400)
+    ck = a.checkpoint(to_host=True)
+    b = B.Simulation(jobs)
+    b.restore(ck)
+    b.advance(600, resume=True)
+    got = b.results()
+    for k in ref:
+        assert np.array_equal(ref[k], got[k]), k
