@@ -169,7 +169,11 @@ sim_known_kernel(KArgs A) {
   uint32_t s1src = 0;
 
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
-  int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, Mres, tridx;
+  int64_t batches, arrivals, comps, ctok, evicts, etok, btok, peak, idle, tridx;
+  // resident memory: at most C after a repair, plus one batch's growth (at
+  // most C/2: every resident holds >= 2 tokens) and admissions (FCFS: within
+  // C; WAIT: sum_j n_j (l_j + 1) < 2^29, checked on the host), so < 2^31
+  int32_t Mres;
   int32_t N, U;  // requests in system, and those without a first token
   uint32_t flags;
   // FCFS chunked prefill: the partially prefilled prompt (at most one, the
@@ -187,7 +191,8 @@ sim_known_kernel(KArgs A) {
   if (!A.resume) {
     t = lat_area = ttft_area = lat_sum = mem_area = busy = 0.0;
     batches = arrivals = comps = ctok = evicts = etok = btok = peak = idle = 0;
-    N = U = Mres = tridx = 0;
+    N = U = Mres = 0;
+    tridx = 0;
     flags = 0;
     part_a = 0.0;
     part_j = -1;
@@ -226,7 +231,7 @@ sim_known_kernel(KArgs A) {
     idle = slot_i(A, S_IDLE, r);
     N = (int32_t)slot_i(A, S_N, r);
     U = (int32_t)slot_i(A, S_U, r);
-    Mres = slot_i(A, S_MRES, r);
+    Mres = (int32_t)slot_i(A, S_MRES, r);
     tridx = slot_i(A, S_TRIDX, r);
     flags = (uint32_t)slot_i(A, S_FLAGS, r);
     part_a = slot_f(A, S_PARTA, r);
@@ -680,7 +685,7 @@ sim_known_kernel(KArgs A) {
       tokens += prefill_l;
     }
 
-    const int64_t m_launch = Mres + prefill_l;
+    const int64_t m_launch = (int64_t)Mres + prefill_l;
     if (m_launch > peak) peak = m_launch;
     const double tau = d0 + d1 * (double)tokens;
     const double t_end = t + tau;

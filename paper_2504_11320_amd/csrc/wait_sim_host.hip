@@ -205,8 +205,13 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   if (kind == WS_WAIT) {
     if (!known) return fail(WS_EINVAL, at + "WAIT needs known output lengths");
     if (!p.n) return fail(WS_EINVAL, at + "thresholds required");
-    for (int j = 0; j < c.m; ++j)
+    int64_t fresh = 0;  // memory one batch can admit
+    for (int j = 0; j < c.m; ++j) {
       if (p.n[j] < 1) return fail(WS_EINVAL, at + "thresholds must be >= 1");
+      fresh += (int64_t)p.n[j] * (c.prompt_len[j] + 1);
+    }
+    if (fresh >= (int64_t(1) << 29))
+      return fail(WS_EUNSUPPORTED, at + "sum_j n_j (l_j + 1) must stay below 2^29");
   } else if (kind == WS_FCFS) {
     if (!(p.fcfs_reserve >= 0.0 && p.fcfs_reserve < 1.0))
       return fail(WS_EINVAL, at + "fcfs_reserve must be in [0,1)");

@@ -127,3 +127,12 @@ def test_chunk_validation():
     assert _err(fc).code == B.WS_EINVAL
     assert _err(_job(chunk=64)).code == B.WS_EINVAL        # WAIT
     assert B.workspace_bytes(B.JobArray(_job(policy="fcfs", n=[], chunk=64))) > 0
+
+
+def test_wait_admission_bound():
+    """WAIT: one batch may admit sum_j n_j (l_j + 1) tokens; at 2^29 or more the
+    library's 32-bit resident-memory counters could overflow:
+    WS_EUNSUPPORTED."""
+    from paper_2504_11320_amd import binding as B
+    assert _err(_job(n=[1 << 22, 1, 1])).code == B.WS_EUNSUPPORTED   # 2^22 x 129
+    assert B.workspace_bytes(B.JobArray(_job(n=[1000, 1, 1]))) > 0
