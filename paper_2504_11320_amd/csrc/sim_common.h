@@ -290,25 +290,12 @@ __device__ __forceinline__ double draw_thinned(uint64_t seed, uint32_t rid, uint
                       });
 }
 
-// Histogram bin of a latency: number of edges <= lat (edges strictly
-// increasing, n <= 255).  Branch-free: a fixed sequence of 8 halving steps
-// over the virtual array padded with +infinity up to 255 entries.
-__device__ __forceinline__ int hist_bin(const double *edges, int n, double lat) {
-  int pos = 0;  // number of edges known to be <= lat
-#pragma unroll
-  for (int step = 128; step >= 1; step >>= 1) {
-    const int probe = pos + step;  // 1-based candidate count
-    const bool le = probe <= n && edges[probe <= n ? probe - 1 : 0] <= lat;
-    pos = le ? probe : pos;
-  }
-  return pos;
-}
-
 // Histogram bin through a bucket index: the non-negative edges are bucketed
 // by the top bits of their IEEE patterns (which order non-negative doubles
 // like their values), so a latency (always >= 0) finds its bin with one table
 // read and a few comparisons instead of a chain of dependent searches.  The
-// result equals hist_bin: the number of edges <= lat.
+// result is the number of edges <= lat (edges strictly increasing, at most
+// 255 of them).
 constexpr int kHistTab = 512;  // bucket-table entries
 
 struct HistIdx {
