@@ -230,6 +230,35 @@ def config_chunked(replicas: int = 1024, n_rates: int = 32, chunk: int = 512,
     return jobs
 
 
+# ------------------------------------------- single-type p512d20 sweep ----
+
+# The paper's single-type synthetic workload p512d20 (prompt 512, 20 decode
+# tokens) in the linear time model: d0 = 10 ms and d1 chosen once so that the
+# fluid boundary (the rate at which M* = C = 137,000 tokens) is 22 requests/s,
+# the operating point the paper reports for WAIT on this workload.  Rates are
+# fractions of that boundary; WAIT thresholds are ceil(n*) of the single-type
+# fluid model at each rate (a CPU test recomputes them).
+P512_LAMSTAR = 0.022                      # per ms
+P512_D1 = 0.004073563169963875            # ms per cached token
+P512_FRACS = [0.6, 0.7, 0.8, 0.85, 0.9, 0.95, 1.0]
+P512_THRESHOLDS = [1, 1, 1, 2, 2, 4, 13]
+
+
+def config_p512d20(replicas: int = 2048, record_capacity: int = 1 << 16) -> List[Job]:
+    """p512d20 at 7 rates (0.6-1.0 of the fluid boundary) under WAIT (fluid
+    thresholds), FCFS with a 1 % reserve, and FCFS with 512-token chunked
+    prefill, on the same replica streams; job order: policy-major."""
+    jobs = []
+    for pol, chunk in (("wait", 0), ("fcfs", 0), ("fcfs", 512)):
+        for frac, n in zip(P512_FRACS, P512_THRESHOLDS):
+            wl = Workload(prompt_len=[512], lam=[frac * P512_LAMSTAR], d0=10.0, d1=P512_D1,
+                          C=137000, policy=pol, n=[n] if pol == "wait" else [], out_len=[20],
+                          reserve=0.01 if pol == "fcfs" else 0.0, chunk=chunk,
+                          hist_edges=default_edges(10.0), record_capacity=record_capacity)
+            jobs.append(Job(wl, 0, ids(replicas)))
+    return jobs
+
+
 # ------------------------------------- decode-only (PD-disaggregated) ----
 
 # A decode server behind a separate prefill service receives each request with
