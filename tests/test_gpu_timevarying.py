@@ -130,3 +130,21 @@ def test_thinning_limit_flag(B):
                     rate_t=np.array([0.0, 1.0]), rate_f=np.array([[1.0, 2.0 ** -30]]))
     g, o = check(B, [W.Job(wl, 4, W.ids(2))], 50, "thinning rejection limit")
     assert np.all(g["flags"] & 8)
+
+
+def test_random_profiles_with_chunked_fcfs(B):
+    """Random profiles combined with chunked-prefill FCFS (budgets 5-200
+    tokens) and with the other policies, in one launch per policy."""
+    from tests.test_gpu_random import random_workload
+    rng = np.random.default_rng(78)
+    jobs = []
+    while len(jobs) < 20:
+        wl = random_workload(rng)
+        if wl.policy == "fcfs":
+            wl.chunk = int(rng.integers(5, 200))
+        elif len(jobs) % 3:
+            continue
+        rt, rf = _profile(rng, wl.m, float(rng.uniform(50.0, 5000.0)))
+        jobs.append(W.Job(W.with_profile(wl, rt, rf), int(rng.integers(0, 2**63)),
+                          W.ids(int(rng.integers(1, 40)))))
+    check(B, jobs, 600, "random profiles with chunked FCFS")
