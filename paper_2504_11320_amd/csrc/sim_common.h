@@ -89,6 +89,7 @@ struct KArgs {
   int32_t any_trace;   // some job of this launch replays a fixed arrival list
   int32_t any_tv;      // some job of this launch has time-varying rates
   int32_t lanes;       // replicas per wavefront (lanes >= this are padding)
+  int32_t unit_n;      // WAIT launch whose jobs all have thresholds n_j = 1
   uint8_t *btrace;     // per-batch trace [R][btrace_cap] records, or null
   int64_t btrace_cap;
 };

@@ -40,8 +40,11 @@ namespace {
 // MT: type slots (>= m, at most 8); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
 // launch replays an arrival list; LN: replicas per wavefront (lanes LN..63
 // are padding), which sizes the per-lane LDS arrays; TV: jobs with
-// time-varying rates are supported (compiled out of the common kernels).
-template <int MT, int POL, bool TRACE, int LN, bool TV>
+// time-varying rates are supported (compiled out of the common kernels);
+// ONE: WAIT with every threshold n_j = 1 (at most one admission and one
+// completion per type and batch), which defers ring reloads to the ends of
+// the admission and completion phases.
+template <int MT, int POL, bool TRACE, int LN, bool TV, bool ONE>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
 sim_known_kernel(KArgs A) {
   constexpr bool WAIT = POL == WS_WAIT;
@@ -305,12 +308,23 @@ sim_known_kernel(KArgs A) {
     bkc[j] = kc;
     dt[j]++;
   };
-  auto dpop_front = [&](int j) __attribute__((always_inline)) {
+  // Front pop: the new front is the cached second record.  dpop_front loads
+  // the next second record at once (used by a further pop in the same batch
+  // or at the next iteration).  With unit thresholds (ONE) a type completes
+  // at most one prompt per batch, and dpop_front_cached leaves the reload to
+  // the end of the completion phase: no load is then issued inside the
+  // phase, where the compiler's waits for a pending load (one in-order
+  // counter per wavefront) would also wait for every earlier memory
+  // operation.
+  auto dpop_front_cached = [&](int j) __attribute__((always_inline)) {
     dh[j]++;
     const bool pushed = (s1src >> j) & 1u;
     fa[j] = pushed ? s1pa[j] : s1a[j];
     fadm[j] = pushed ? s1padm[j] : s1adm[j];
     s1src &= ~(1u << j);
+  };
+  auto dpop_front = [&](int j) __attribute__((always_inline)) {
+    dpop_front_cached(j);
     const DRec n = dring(j)[(dh[j] + 1u) & dmask[j]];  // next second record
     s1a[j] = n.a_ft;
     s1adm[j] = WAIT ? n.kc : n.kb;
@@ -487,7 +501,7 @@ sim_known_kernel(KArgs A) {
   };
 
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
-  uint32_t fresh[MT], pendnew[MT];
+  uint32_t fresh[MT], pendnew[MT], popped[MT];
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- refill the gap rings, all active lanes together ----------------
@@ -604,11 +618,13 @@ sim_known_kernel(KArgs A) {
         // admissions: n_j (WAIT), at most n_j of those waiting (no-wait)
         const uint32_t waiting = qt[j] - qh[j];
         const int32_t na = nowait && waiting < (uint32_t)nth[j] ? (int32_t)waiting : nth[j];
-        for (int x = 0; x < na; ++x) {
+        // each admission takes the cached head and loads the next one (ONE:
+        // at most one admission, and the reload follows all admissions)
+        for (int x = 0; x < (ONE ? min(na, 1) : na); ++x) {
           const double a_ft = ((qsrc >> j) & 1u) ? qpu[j] : qld[j];
           qsrc &= ~(1u << j);
           qh[j]++;
-          qld[j] = qring(j)[qh[j] & qmask];  // the next head, used at a later admission
+          if (!ONE) qld[j] = qring(j)[qh[j] & qmask];  // the next head
           dpush(j, a_ft, bidx, c);
           pendnew[j] += has_ft(a_ft) ? 0u : 1u;
         }
@@ -616,6 +632,11 @@ sim_known_kernel(KArgs A) {
         bt_pre += na;
         tokens += (int64_t)na * l[j] + Mj[j];
         prefill_l += (int64_t)na * l[j];
+      }
+      if (ONE) {  // reload the heads of the queues that admitted
+#pragma unroll
+        for (int j = 0; j < MT; ++j)
+          if (fresh[j] > 0u) qld[j] = qring(j)[qh[j] & qmask];
       }
     } else if (chunk > 0) {
       // chunked prefill: the partial prompt first, then admissions from the
@@ -713,6 +734,8 @@ sim_known_kernel(KArgs A) {
     const int64_t bt_comps0 = comps;
     if constexpr (TV) bt_sel = !WAIT && part_j >= 0 ? 1 : 0;
 #pragma unroll
+    for (int j = 0; j < MT; ++j) popped[j] = 0;
+#pragma unroll
     for (int j = 0; j < MT; ++j) {
       const bool served = WAIT ? ((elig >> j) & 1u) != 0 : j < m;
       if (!served) continue;
@@ -726,8 +749,7 @@ sim_known_kernel(KArgs A) {
       const uint32_t before = (dt[j] - dh[j]) - fresh[j];  // residents at launch
       uint32_t done = 0;
       // completions: processed at stage l'_j (fresh records never qualify)
-      while (done < before) {
-        if (fadm[j] + (uint32_t)lp[j] != now) break;
+      auto complete_front = [&]() __attribute__((always_inline)) {
         const double lat = t_end - arrival_of(fa[j]);
         lat_sum += lat;
         __hip_atomic_fetch_add(&hist[hist_bin_idx(edges, s_htab, hidx, lat)], 1u, __ATOMIC_RELAXED,
@@ -735,11 +757,35 @@ sim_known_kernel(KArgs A) {
         comps++;
         ctok += lp[j];
         N--;
-        dpop_front(j);
-        done++;
+      };
+      if constexpr (ONE) {
+        // unit thresholds: one admission per service, so at most one resident
+        // of the type reaches its last stage in a batch
+        if (before > 0u && fadm[j] + (uint32_t)lp[j] == now) {
+          complete_front();
+          dpop_front_cached(j);
+          done = 1;
+        }
+      } else {
+        while (done < before) {
+          if (fadm[j] + (uint32_t)lp[j] != now) break;
+          complete_front();
+          dpop_front(j);
+          done++;
+        }
       }
+      popped[j] = done;
       Mj[j] += (int32_t)(before - done) + (int32_t)fresh[j] * (l[j] + 1) -
                (int32_t)done * (l[j] + lp[j]);
+    }
+    // ONE: reload the second records of the deques that popped
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+      if (ONE && popped[j] > 0u) {
+        const DRec n = dring(j)[(dh[j] + 1u) & dmask[j]];
+        s1a[j] = n.a_ft;
+        s1adm[j] = WAIT ? n.kc : n.kb;
+      }
     }
     Mres = WAIT ? 0 : part_pp;
 #pragma unroll
@@ -844,29 +890,38 @@ sim_known_kernel(KArgs A) {
   }
 }
 
-template <int MT, int POL, bool TV>
-hipError_t launch_mt(const KArgs &A, hipStream_t s) {
+template <int MT, int POL, bool TV, bool ONE>
+hipError_t launch_lanes(const KArgs &A, hipStream_t s) {
   const int blocks = (A.n_list + 63) / 64;
   const dim3 g(blocks), b(64);
   if (A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
     if constexpr (TV) {
       if (A.lanes != 64) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64, TV>), g, b, 0, s, A);
+      hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64, TV, ONE>), g, b, 0, s, A);
     } else {
       return hipErrorInvalidValue;  // replays run on the TV kernels
     }
   } else if (A.lanes == 64) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64, TV>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64, TV, ONE>), g, b, 0, s, A);
   } else if (A.lanes == 32) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 32, TV>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 32, TV, ONE>), g, b, 0, s, A);
   } else if (A.lanes == 16) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 16, TV>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 16, TV, ONE>), g, b, 0, s, A);
   } else if (A.lanes == 8) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 8, TV>), g, b, 0, s, A);
+    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 8, TV, ONE>), g, b, 0, s, A);
   } else {
     return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// The unit-threshold kernels exist for constant-rate WAIT only.
+template <int MT, int POL, bool TV>
+hipError_t launch_mt(const KArgs &A, hipStream_t s) {
+  if constexpr (POL == WS_WAIT && !TV) {
+    if (A.unit_n) return launch_lanes<MT, POL, TV, true>(A, s);
+  }
+  return launch_lanes<MT, POL, TV, false>(A, s);
 }
 
 template <int POL, bool TV>

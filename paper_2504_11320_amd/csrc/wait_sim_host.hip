@@ -577,10 +577,14 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     B.n_list = Lo.list_count[pk];
     B.lanes = Lo.lanes[pk];
     B.any_trace = B.any_tv = 0;
+    B.unit_n = pk == WS_WAIT ? 1 : 0;
     for (int i = 0; i < n_jobs; ++i) {
       if (launch_kind(jobs[i].pol) != pk) continue;
       if (jobs[i].cfg->n_trace > 0) B.any_trace = 1;
       if (jobs[i].cfg->n_rate_pts > 0) B.any_tv = 1;
+      if (pk == WS_WAIT)
+        for (int j = 0; j < jobs[i].cfg->m; ++j)
+          if (jobs[i].pol->n[j] != 1) B.unit_n = 0;
     }
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)

@@ -60,3 +60,33 @@ def test_wait_nowait_sweep():
         wl.n = [2, 1, 1]
         jobs.append(W.Job(wl, 0, W.ids(70)))
     check(B, jobs, 3000, "WAIT-no-wait, 3 rates x70 x3000")
+
+
+@pytest.mark.parametrize("m", [1, 2, 3, 4, 6, 8])
+def test_unit_thresholds(m):
+    """WAIT and WAIT-no-wait launches whose jobs all have n_j = 1 run the
+    unit-threshold kernels (at most one admission and one completion per type
+    and batch): random models with m types against the oracle, at 8 replicas
+    per wavefront; a launch of 66,000 replicas (64 per wavefront) gives the
+    same replicas bit-identical results."""
+    B = sim_module()
+    rng = np.random.default_rng(500 + m)
+    jobs = []
+    for i in range(6):
+        l = [int(x) for x in rng.integers(1, 60, m)]
+        lp = [int(x) for x in rng.integers(1, 30, m)]
+        wl = W.Workload(prompt_len=l, lam=[float(x) for x in rng.uniform(0.02, 0.6, m)],
+                        d0=float(rng.uniform(0.5, 5.0)), d1=float(rng.uniform(0.0, 0.02)),
+                        C=int(max(a + b for a, b in zip(l, lp)) * rng.uniform(1.0, 4.0)),
+                        policy="wait" if i % 3 else "wait-nowait", n=[1] * m, out_len=lp,
+                        hist_edges=W.default_edges(1.0, int(rng.integers(1, 100))),
+                        record_capacity=1 << 14)
+        jobs.append(W.Job(wl, int(rng.integers(0, 2**63)), W.ids(int(rng.integers(1, 40)))))
+    check(B, jobs, 1500, f"unit thresholds, {m} types")
+    R = 11000
+    g = B.run_batch([W.Job(j.wl, j.seed, W.ids(R)) for j in jobs], 600)
+    picks = np.concatenate([np.arange(5), np.arange(R - 5, R)]).astype(np.uint32)
+    small = B.run_batch([W.Job(j.wl, j.seed, picks) for j in jobs], 600)
+    idx = np.concatenate([R * k + picks.astype(np.int64) for k in range(len(jobs))])
+    for k in g:
+        assert np.array_equal(g[k][idx], small[k]), k
