@@ -174,6 +174,19 @@ __device__ __forceinline__ double ln_unit(double u) {
 
 // Gap to the k-th arrival of type j, and its output length when a CDF row is
 // given (smallest s in 1..cap-1 with w2 < T[s], else cap).
+// Remainder by a divisor that is fixed per job (Lemire, Kaser and Kurz,
+// "Faster remainder by direct computation", 2019): with M = floor((2^64 - 1)
+// / d) + 1 (0 for d = 1), n mod d is the high 64 bits of (M n mod 2^64) d,
+// exact for every 32-bit n and d >= 1; three 32-bit multiply steps instead of
+// a reciprocal-based division.
+__host__ __device__ __forceinline__ uint64_t fastmod_magic(uint32_t d) { return ~0ull / d + 1ull; }
+__device__ __forceinline__ uint32_t fastmod(uint32_t n, uint64_t M, uint32_t d) {
+  const uint64_t low = M * (uint64_t)n;
+  const uint64_t lo_part = (uint64_t)(uint32_t)low * d;
+  const uint64_t hi_part = (low >> 32) * d + (lo_part >> 32);  // < 2^64
+  return (uint32_t)(hi_part >> 32);
+}
+
 // Output length from a CDF row: the smallest s in 1..cap-1 with w2 < T[s]
 // (T[s] at row[s - 1], nondecreasing), else cap.  The table sits in global
 // memory, so each probe is a dependent load: an 8-way search probes 7 points

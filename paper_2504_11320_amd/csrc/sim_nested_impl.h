@@ -38,6 +38,7 @@ namespace {
 // lane-dependent (it starts at a lane's own prefix length), and LDS serves
 // such reads without a round trip to the job table in memory.
 struct SegConst {
+  uint64_t dmagic;  // fastmod multiplier for delta
   int32_t end;      // r_k
   int32_t n;        // n_k
   int32_t delta;    // processing stages (cohort slots)
@@ -184,6 +185,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       c.end = on ? J.seg_end[k] : 0;
       c.n = on ? J.seg_n[k] : 0;
       c.delta = on ? J.seg_delta[k] : 1;
+      c.dmagic = fastmod_magic((uint32_t)c.delta);
       c.entry = on ? J.seg_entry[k] : 0;
       c.vmask = on && k >= 1 ? (1u << J.vcap_log2[k]) - 1u : 0u;
       c.off_rec = on ? (uint32_t)J.off_rec[k] : 0u;
@@ -444,7 +446,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const uint32_t svc = s_svc[k][tx];
     const NRec *rc = recs(k);
     for (int32_t back = 0; back < delta && (int64_t)svc - back >= 1; ++back) {
-      const uint32_t slot = (svc - (uint32_t)back) % (uint32_t)delta;
+      const uint32_t slot = fastmod(svc - (uint32_t)back, s_seg[k].dmagic, (uint32_t)delta);
       // a record with L = 0 has left the segment (exit or eviction)
       for (int32_t i = nk - 1; i >= 0; --i) {
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
@@ -536,14 +538,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       if (!may_launch(k)) continue;
       const int32_t delta = s_seg[k].delta;
       const uint32_t x = s_svc[k][tx] + 1u;  // the segment's next service
-      copy4_to_lds(bkts(k) + x % (uint32_t)delta, &s_bh[k][0]);
+      copy4_to_lds(bkts(k) + fastmod(x, s_seg[k].dmagic, (uint32_t)delta), &s_bh[k][0]);
       if (k >= 1) {
         const NRec *f = vring(k) + (s_vh[k][tx] & vmask(k));
         copy16_to_lds(f, &s_vfa[k][0]);
         copy16_to_lds((const uint8_t *)f + 16, &s_vfb[k][0]);
       }
       if (s_seg[k].n == 1) {
-        const NRec *tr = recs(k) + (x - (uint32_t)(delta - 1)) % (uint32_t)delta;
+        const NRec *tr = recs(k) + fastmod(x - (uint32_t)(delta - 1), s_seg[k].dmagic, (uint32_t)delta);
         copy16_to_lds(tr, &s_tra[k][0]);
         copy16_to_lds((const uint8_t *)tr + 16, &s_trb[k][0]);
       }
@@ -648,7 +650,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       const int32_t rk = s_seg[k].end;
       const int32_t ent = s_seg[k].entry;
       const uint32_t x = s_svc[k][tx] + 1u;
-      const uint32_t slot = x % (uint32_t)delta;
+      const uint64_t dmg = s_seg[k].dmagic;
+      const uint32_t slot = fastmod(x, dmg, (uint32_t)delta);
       NRec *rc = recs(k);
       uint32_t *bk = bkts(k);
       tokens += s_M[k][tx];
@@ -688,7 +691,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
-        const uint32_t b = (x + (uint32_t)(pexit - ent)) % (uint32_t)delta;
+        const uint32_t b = fastmod(x + (uint32_t)(pexit - ent), dmg, (uint32_t)delta);
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
         if (b == slot) {  // exits at this very service: heads the bucket served now
           e.next = s_bh[k][tx];
@@ -723,7 +726,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         uint32_t T = 0, Tl = 0;
         if ((int64_t)x - (delta - 1) >= 1) {
           // the terminal cohort slot: its prompts still in the segment
-          const uint32_t ts = (x - (uint32_t)(delta - 1)) % (uint32_t)delta;
+          const uint32_t ts = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
           if (nk == 1) {  // prefetched
             const int32_t trL = (int32_t)s_trb[k][tx].y, trj = (int32_t)s_trb[k][tx].x;
             T = trL != 0 ? 1u : 0u;
@@ -812,7 +815,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       // prompts whose exit is at this service: the bucket's head was
       // prefetched, the list's records are read on demand
       uint32_t *bk = bkts(k);
-      const uint32_t b = x % (uint32_t)delta;
+      const uint32_t b = fastmod(x, s_seg[k].dmagic, (uint32_t)delta);
       uint32_t idx = s_bh[k][tx];
       bk[b] = kNil;
       while (idx != kNil) {
