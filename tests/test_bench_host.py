@@ -1,0 +1,75 @@
+"""Host logic of bench.py (no GPU): the operation and byte models behind the
+roofline figures, the thinning candidate ratio, the profile-summary lookup and
+the refusal of more than one GPU."""
+import os
+import re
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+import workloads as W  # noqa: E402
+
+
+def test_op_model_constants():
+    c = bench.op_model(3)
+    # Philox4x32-10 (10 rounds of 2 wide multiplies at 4, 4 xor, 2 adds) +
+    # uniform + ln + gap = 214 per draw, + 12 bookkeeping + 2m
+    assert c["arrival"] == 140 + 10 + 50 + 14 + 12 + 2 * 3
+    assert c["batch"] == 24 + 6 * 3
+    assert c["completion"] == 35
+    assert c["eviction"] == 14 + 3 * 3
+    assert c["idle"] == 15 + 4 * 3
+    # a 2048-entry CDF row adds 2 ops per halving step (11 steps)
+    assert bench.op_model(3, cdf_cap=2048)["arrival"] - c["arrival"] == 22
+    # a profile of 25 points: search of 5 halvings at 3 ops + 24 per candidate
+    tv = bench.op_model(3, rate_pts=25, cand_per_arrival=1.5)
+    assert tv["arrival"] == pytest.approx(1.5 * (214 + 15 + 24) + 12 + 6)
+
+
+def test_algorithmic_counts_are_linear_in_events():
+    res = {k: np.array([v]) for k, v in dict(batches=1000, arrivals=590, completions=550,
+                                              evictions=1780, idle_waits=80).items()}
+    c = bench.op_model(3)
+    want = (1000 * c["batch"] + 590 * c["arrival"] + 550 * c["completion"]
+            + 1780 * c["eviction"] + 80 * c["idle"])
+    assert bench.algorithmic_ops(res, 3) == pytest.approx(want)
+    # the benchmark's event mix gives about 241 lane-operations per batch
+    assert 235 < want / 1000 < 245
+    assert bench.algorithmic_bytes(res) == 16 * 2 * (590 + 1780) + 16 * 550
+
+
+def test_candidates_per_arrival():
+    base = W.config2(replicas=4, rate_index=[3])[0].wl
+    assert bench.candidates_per_arrival([W.Job(base, 0, W.ids(4))]) == 1.0
+    # a triangle 0 -> 2 -> 0: mean 1, bound 2, for every type
+    tri = W.with_profile(base, [0.0, 1.0, 2.0], np.tile([0.0, 2.0, 0.0], (base.m, 1)))
+    assert bench.candidates_per_arrival([W.Job(tri, 0, W.ids(4))]) == pytest.approx(2.0)
+
+
+def test_profile_summary_lookup(monkeypatch):
+    path = os.path.join(ROOT, "profiles", bench.PROFILES["wait-llama"][0] + "_hbm.md")
+    txt = open(path).read()
+    h = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt).group(1)
+    b = float(re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt).group(1))
+    got = bench.traffic_from_profile("wait-llama")
+    if h == bench.source_hash("wait-llama"):
+        assert got == b
+    else:
+        assert got is None
+    # a summary taken on other sources is not used
+    monkeypatch.setattr(bench, "source_hash", lambda workload="wait-llama": "0" * 16)
+    assert bench.traffic_from_profile("wait-llama") is None
+    assert bench.traffic_from_profile("no-such-workload") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert p.returncode == 2
+    assert "one GPU" in p.stderr
+    assert p.stdout.strip() == ""
