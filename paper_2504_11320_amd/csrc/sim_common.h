@@ -180,7 +180,7 @@ __device__ __forceinline__ double ln_unit(double u) {
 // exact for every 32-bit n and d >= 1; three 32-bit multiply steps instead of
 // a reciprocal-based division.
 __host__ __device__ __forceinline__ uint64_t fastmod_magic(uint32_t d) { return ~0ull / d + 1ull; }
-__device__ __forceinline__ uint32_t fastmod(uint32_t n, uint64_t M, uint32_t d) {
+__host__ __device__ __forceinline__ uint32_t fastmod(uint32_t n, uint64_t M, uint32_t d) {
   const uint64_t low = M * (uint64_t)n;
   const uint64_t lo_part = (uint64_t)(uint32_t)low * d;
   const uint64_t hi_part = (low >> 32) * d + (lo_part >> 32);  // < 2^64
@@ -193,7 +193,8 @@ __device__ __forceinline__ uint32_t fastmod(uint32_t n, uint64_t M, uint32_t d) 
 // of the interval at once (independent loads, one round trip) and keeps the
 // part between the last probe with T <= w2 and the first with T > w2, so a
 // 2048-entry row takes 4 round trips instead of the 11 of a binary search.
-__device__ __forceinline__ int32_t cdf_search(const uint32_t *row, int32_t cap, uint32_t w2) {
+__host__ __device__ __forceinline__ int32_t cdf_search(const uint32_t *row, int32_t cap,
+                                                     uint32_t w2) {
   constexpr int K = 8;
   int32_t lo = 1, hi = cap;  // the answer lies in [lo, hi]
   while (lo < hi) {
