@@ -138,6 +138,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // a scan when next needed).  LIFO selections then read no HBM.
   __shared__ NRec s_vb[LT][LN], s_yi[LT][LN];
   __shared__ uint32_t s_yidx[LT][LN];
+  // Per lane and segment: the index of the last youngest interior record that
+  // left the segment (kNil: none known).  Every record entered after it has
+  // left too, so the scan for the next youngest starts just below it; s_yi
+  // still holds it while s_yidx is kNil.
+  __shared__ uint32_t s_ydead[LT][LN];
   // Prefetch landing slots, one per lane, filled by asynchronous copies from
   // HBM (global_load_lds) issued at the end of an iteration and waited for at
   // the start of the next: the head of Q_{1,0}; per segment that can launch
@@ -321,6 +326,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   }
   for (int k = 0; k < LT; ++k) {
     s_yidx[k][tx] = kNil;
+    s_ydead[k][tx] = kNil;
     if (k >= 1 && k < L && s_vt[k][tx] != s_vh[k][tx])
       s_vb[k][tx] = vring(k)[(s_vt[k][tx] - 1u) & vmask(k)];
   }
@@ -443,12 +449,24 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
     const int32_t delta = s_seg[k].delta;
     const int32_t nk = s_seg[k].n;
+    const uint64_t dmg = s_seg[k].dmagic;
     const uint32_t svc = s_svc[k][tx];
     const NRec *rc = recs(k);
-    for (int32_t back = 0; back < delta && (int64_t)svc - back >= 1; ++back) {
-      const uint32_t slot = fastmod(svc - (uint32_t)back, s_seg[k].dmagic, (uint32_t)delta);
+    // start just below the youngest that left last (its cohort entered at
+    // service c, no later cohort has entered since: an entering cohort sets
+    // the cache), else at the newest cohort slot
+    int32_t back = 0, ifrom = nk - 1;
+    const uint32_t dead = s_ydead[k][tx];
+    if (dead != kNil) {
+      const uint32_t c0 = s_yi[k][tx].c;
+      back = (int32_t)(svc - c0);
+      ifrom = (int32_t)(dead - fastmod(c0, dmg, (uint32_t)delta) * (uint32_t)nk) - 1;
+      ifrom = ifrom < nk - 1 ? ifrom : nk - 1;  // indices stay inside the cohort slot
+    }
+    for (; back < delta && (int64_t)svc - back >= 1; ++back, ifrom = nk - 1) {
+      const uint32_t slot = fastmod(svc - (uint32_t)back, dmg, (uint32_t)delta);
       // a record with L = 0 has left the segment (exit or eviction)
-      for (int32_t i = nk - 1; i >= 0; --i) {
+      for (int32_t i = ifrom; i >= 0; --i) {
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
         const NRec rec = rc[idx];
         if (rec.L != 0) {
@@ -467,6 +485,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     NRec *rc = recs(k);
     NRec rec = s_yi[k][tx];  // idx is the segment's youngest live interior record
     s_yidx[k][tx] = kNil;
+    s_ydead[k][tx] = idx;
     const int32_t delta = s_seg[k].delta;
     const int32_t nk = s_seg[k].n;
     const int64_t stage = (int64_t)s_seg[k].entry + (int64_t)(s_svc[k][tx] - rec.c) + 1;
@@ -822,7 +841,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         const NRec rec = rc[idx];
         const uint32_t nxt = rec.next;
         if (rec.L != 0) {  // holes left by evictions are skipped
-          if (idx == s_yidx[k][tx]) s_yidx[k][tx] = kNil;  // the youngest leaves
+          if (idx == s_yidx[k][tx]) {  // the youngest leaves
+            s_ydead[k][tx] = idx;
+            s_yidx[k][tx] = kNil;
+          }
           const int64_t le = s_l[rec.j];
           const int32_t p = rec.L < rk ? rec.L : rk;
           if (rec.c != x) {  // an interior prompt: it had advanced to p + 1
