@@ -837,9 +837,21 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       const uint32_t b = fastmod(x, s_seg[k].dmagic, (uint32_t)delta);
       uint32_t idx = s_bh[k][tx];
       bk[b] = kNil;
+      // Each record is loaded whole (both 16-byte halves at once) one node
+      // ahead: the next record's load is issued before this node's stores,
+      // so waiting for it does not wait for them.
+      uint4 clo = make_uint4(0u, 0u, 0u, 0u), chi = make_uint4(0u, 0u, 0u, kNil);
+      if (idx != kNil) {
+        clo = ((const uint4 *)(rc + idx))[0];
+        chi = ((const uint4 *)(rc + idx))[1];
+      }
       while (idx != kNil) {
-        const NRec rec = rc[idx];
+        const NRec rec = nrec_of(opaque4(clo), opaque4(chi));
         const uint32_t nxt = rec.next;
+        if (nxt != kNil) {
+          clo = ((const uint4 *)(rc + nxt))[0];
+          chi = ((const uint4 *)(rc + nxt))[1];
+        }
         if (rec.L != 0) {  // holes left by evictions are skipped
           if (idx == s_yidx[k][tx]) {  // the youngest leaves
             s_ydead[k][tx] = idx;
