@@ -468,7 +468,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       // a record with L = 0 has left the segment (exit or eviction)
       for (int32_t i = ifrom; i >= 0; --i) {
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
-        const NRec rec = rc[idx];
+        // the whole record in one round trip (both halves issued together)
+        uint4 lo = ((const uint4 *)(rc + idx))[0], hi = ((const uint4 *)(rc + idx))[1];
+        lo = opaque4(lo);
+        hi = opaque4(hi);
+        const NRec rec = nrec_of(lo, hi);
         if (rec.L != 0) {
           kb = rec.kb;
           kp = rec.kp;
@@ -703,7 +707,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             e = nrec_of(s_vfa[k][tx], s_vfb[k][tx]);  // the front, prefetched
           } else {
             const NRec *src = vring(k) + ((s_vh[k][tx] + (uint32_t)i) & vmask(k));
-            const uint4 lo = opaque4(*(const uint4 *)src), hi = opaque4(((const uint4 *)src)[1]);
+            uint4 lo = ((const uint4 *)src)[0], hi = ((const uint4 *)src)[1];
+            lo = opaque4(lo);  // both halves in flight before the wait
+            hi = opaque4(hi);
             e = nrec_of(lo, hi);
           }
           tokens += (int64_t)s_l[e.j] + s_seg[k - 1].end + 1;
@@ -752,10 +758,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             Tl = trL != 0 ? (uint32_t)s_l[trj] : 0u;
           } else {
             for (int32_t i = 0; i < nk; ++i) {
-              const NRec tr = rc[ts * (uint32_t)nk + (uint32_t)i];
-              const bool live = tr.L != 0;
+              // j and L (the second half's first two words) in one load
+              const uint2 jl = opaque(*(const uint2 *)((const uint8_t *)(rc + ts * (uint32_t)nk +
+                                                                          (uint32_t)i) + 16));
+              const bool live = (int32_t)jl.y != 0;
               T += live ? 1u : 0u;
-              Tl += live ? (uint32_t)s_l[tr.j] : 0u;
+              Tl += live ? (uint32_t)s_l[(int32_t)jl.x] : 0u;
             }
           }
         }
