@@ -73,8 +73,11 @@ sim_known_kernel(KArgs A) {
   // The last WB records pushed on each resident deque are also kept in LDS,
   // so LIFO evictions (which pop the back) rarely read HBM.  Launches with
   // time-varying rates run two wavefronts per SIMD at 16 replicas each; a
-  // window of 8 lets eight workgroups share a CU's LDS.
-  constexpr int WB = MT <= 4 ? (TV && LN <= 16 ? 8 : 16) : 2;
+  // window of 8 lets eight workgroups share a CU's LDS.  Constant-rate
+  // launches at 16 replicas per wavefront (jobs of 16 replicas, as in
+  // threshold sweeps) also run two per SIMD: a window of 14 keeps the
+  // 3-type kernel within a CU's LDS for eight workgroups.
+  constexpr int WB = MT <= 4 ? (TV && LN <= 16 ? 8 : (LN == 16 ? 14 : 16)) : 2;
   __shared__ DRec s_win[MT][WB][LN];
   const int tx = threadIdx.x;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
