@@ -511,13 +511,17 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return ch;
   };
 
-  // Evict the most recently admitted prompt among boundary queues
-  // h in [hlo, L) and, if fallback is set and none exists, among the interior
-  // of segments [klo, L).  Returns the memory freed, 0 if nothing was left.
-  auto evict_lifo = [&](int klo, bool allow_interior) __attribute__((always_inline)) -> int64_t {
+  // Evict the most recently admitted prompt among the boundary queues and,
+  // if allow_interior is set and none holds a prompt, among the interior of
+  // segments [klo, L).  Returns the memory freed, 0 if nothing was left.
+  // `boundary` is cleared once the boundary queues are found empty: within
+  // one repair they stay empty (evicted prompts go back to the entry queue),
+  // so later calls skip that scan.
+  auto evict_lifo = [&](int klo, bool allow_interior, bool &boundary)
+                        __attribute__((always_inline)) -> int64_t {
     int hb = -1;
     uint32_t bkb = 0, bkp = 0;
-    for (int h = 1; h < L; ++h) {
+    for (int h = 1; boundary && h < L; ++h) {
       if (s_vt[h][tx] == s_vh[h][tx]) continue;
       const uint32_t rkb = s_vb[h][tx].kb, rkp = s_vb[h][tx].kp;
       if (hb < 0 || rkb > bkb || (rkb == bkb && rkp > bkp)) {
@@ -527,6 +531,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       }
     }
     if (hb >= 0) return evict_boundary(hb);
+    boundary = false;
     if (!allow_interior) return 0;
     int kbest = -1;
     uint32_t ibest = kNil;
@@ -782,13 +787,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
 
     // ---- pre-launch repair on the projected state ----------------------------
+    bool bnd_pre = true;
     while (mplus > C) {
-      const int64_t freed = evict_lifo(kmax, false);
+      const int64_t freed = evict_lifo(kmax, false, bnd_pre);
       if (freed == 0) break;
       mplus -= freed;
     }
     while (mplus > C) {  // unselected interior prompts (segments after the prefix)
-      const int64_t freed = evict_lifo(kmax, true);
+      const int64_t freed = evict_lifo(kmax, true, bnd_pre);
       if (freed == 0) break;
       mplus -= freed;
     }
@@ -909,8 +915,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     if (Mres > peak) peak = Mres;
 
     // ---- repair: boundary prompts first, then interior prompts -------------
+    bool bnd_post = true;
     while (Mres > C) {
-      if (evict_lifo(0, true) == 0) break;
+      if (evict_lifo(0, true, bnd_post) == 0) break;
     }
     if constexpr (TV) {
       if (A.btrace != nullptr && batches < A.btrace_cap) {
