@@ -193,10 +193,10 @@ __host__ __device__ __forceinline__ uint32_t fastmod(uint32_t n, uint64_t M, uin
 // of the interval at once (independent loads, one round trip) and keeps the
 // part between the last probe with T <= w2 and the first with T > w2, so a
 // 2048-entry row takes 4 round trips instead of the 11 of a binary search.
-__host__ __device__ __forceinline__ int32_t cdf_search(const uint32_t *row, int32_t cap,
-                                                     uint32_t w2) {
+__host__ __device__ __forceinline__ int32_t cdf_search_in(const uint32_t *row, int32_t lo,
+                                                        int32_t hi, uint32_t w2) {
   constexpr int K = 8;
-  int32_t lo = 1, hi = cap;  // the answer lies in [lo, hi]
+  // the answer lies in [lo, hi] (1 <= lo <= hi <= cap)
   while (lo < hi) {
     const int32_t span = hi - lo;
     int32_t pos[K - 1];
@@ -219,17 +219,34 @@ __host__ __device__ __forceinline__ int32_t cdf_search(const uint32_t *row, int3
   }
   return lo;
 }
+__host__ __device__ __forceinline__ int32_t cdf_search(const uint32_t *row, int32_t cap,
+                                                     uint32_t w2) {
+  return cdf_search_in(row, 1, cap, w2);
+}
+
+// A guide narrows the search before the first round trip: G[b] (b = 0..64)
+// is the length drawn for w2 = b * 2^26, the smallest s with T[s] > b * 2^26
+// (G[64] = cap).  Every w2 in [b * 2^26, (b + 1) * 2^26) then draws a
+// length in [G[b], G[b + 1]]: T[s] <= w2 below G[b], and T[G[b + 1]] > w2.
+constexpr int kCdfGuide = 64;
+__host__ __device__ __forceinline__ int32_t cdf_guide_entry(const uint32_t *row, int32_t cap,
+                                                          int b) {
+  return b >= kCdfGuide ? cap : cdf_search(row, cap, (uint32_t)b << 26);
+}
 
 __device__ __forceinline__ double draw_gap(uint64_t seed, uint32_t rid,
                                            uint32_t j, uint32_t k, double lam,
                                            const uint32_t *row, int32_t cap,
-                                           int32_t *L, uint32_t *w3 = nullptr) {
+                                           int32_t *L, uint32_t *w3 = nullptr,
+                                           const uint16_t *guide = nullptr) {
   uint32_t w[4];
   philox10(k, j, rid, 0u, (uint32_t)seed, (uint32_t)(seed >> 32), w);
   if (w3 != nullptr) *w3 = w[3];
   const uint64_t x = ((uint64_t)w[0] << 20) | (uint64_t)(w[1] >> 12);
   const double u = (double)(2 * x + 1) * 0x1p-53;
-  if (row != nullptr) *L = cdf_search(row, cap, w[2]);
+  if (row != nullptr)
+    *L = guide != nullptr ? cdf_search_in(row, guide[w[2] >> 26], guide[(w[2] >> 26) + 1], w[2])
+                          : cdf_search(row, cap, w[2]);
   return -ln_unit(u) / lam;
 }
 

@@ -143,6 +143,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // left too, so the scan for the next youngest starts just below it; s_yi
   // still holds it while s_yidx is kNil.
   __shared__ uint32_t s_ydead[LT][LN];
+  // per type: the guide of its output-length CDF row (kCdfGuide + 1 entries)
+  __shared__ uint16_t s_cdfg[MT][kCdfGuide + 1];
   // Prefetch landing slots, one per lane, filled by asynchronous copies from
   // HBM (global_load_lds) issued at the end of an iteration and waited for at
   // the start of the next: the head of Q_{1,0}; per segment that can launch
@@ -198,6 +200,15 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       c.off_v = on && k >= 1 ? (uint32_t)J.off_v[k] : 0u;
       s_seg[k] = c;
     }
+    if (J.known == 0 && J.n_trace == 0 && J.out_cap > 1 && J.out_cap <= 65535) {
+      const uint32_t *cdf_g = (const uint32_t *)(A.ws + J.off_cdf);
+      for (int x = tx; x < MT * (kCdfGuide + 1); x += 64) {
+        const int j = x / (kCdfGuide + 1), b = x % (kCdfGuide + 1);
+        s_cdfg[j][b] = j < m ? (uint16_t)cdf_guide_entry(cdf_g + (size_t)j * (size_t)(J.out_cap - 1),
+                                                         J.out_cap, b)
+                             : (uint16_t)0;
+      }
+    }
     if (tv) {
       const double *rg = (const double *)(A.ws + J.off_rate);
       for (int i = tx; i < P; i += 64) s_rt[i] = rg[i];
@@ -240,6 +251,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
     return (known || cap <= 1) ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
   };
+  const bool use_guide = !known && !trace && cap > 1 && cap <= 65535;
+  auto guide_of = [&](int j) __attribute__((always_inline)) -> const uint16_t * {
+    return use_guide ? s_cdfg[j] : nullptr;
+  };
 
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
   int64_t batches, arrivals, comps, ctok, evicts, etok, fallback, btok, peak, idle, N, U,
@@ -265,7 +280,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
                                         s_rt, s_rf[j], P, row_of(j), cap, &Lj, cur, flags);
           s_k[j][tx] = k0;
         } else {
-          const double g = draw_gap(seed, rid, (uint32_t)j, 0u, J.lambda[j], row_of(j), cap, &Lj);
+          const double g = draw_gap(seed, rid, (uint32_t)j, 0u, J.lambda[j], row_of(j), cap, &Lj,
+                                    nullptr, guide_of(j));
           s_tnext[j][tx] = 0.0 + g;
         }
         s_Ln[j][tx] = known ? J.lp[j] : (cap <= 1 ? 1 : Lj);
@@ -407,7 +423,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         g = s_gap[jn][k % GR][tx];
         Lj = s_glen[jn][k % GR][tx];
       } else {
-        g = draw_gap(seed, rid, (uint32_t)jn, k, J.lambda[jn], row_of(jn), cap, &Lj);
+        g = draw_gap(seed, rid, (uint32_t)jn, k, J.lambda[jn], row_of(jn), cap, &Lj, nullptr,
+                     guide_of(jn));
         s_gend[jn][tx] = k + 1u;
       }
       s_tnext[jn][tx] = s_tnext[jn][tx] + g;
@@ -614,7 +631,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             int32_t Lj = 1;
             uint32_t w3;
             s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lamj, row, cap,
-                                            &Lj, TV ? &w3 : nullptr);
+                                            &Lj, TV ? &w3 : nullptr, guide_of(j));
             s_glen[j][k % GR][ln] = Lj;
             if constexpr (TV) s_w3[j][k % GR][ln] = w3;
           }

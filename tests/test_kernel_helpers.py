@@ -6,7 +6,9 @@ kernels' own header with hipcc for the host; no GPU needed):
 * cdf_search: the 8-way search of a CDF row must return the smallest s in
   1..cap-1 with w2 < T[s], else cap (the definition of an output-length draw),
   on random nondecreasing rows with ties, saturation and boundary values of
-  w2, for every row length up to 70 and sampled lengths up to 4100.
+  w2, for every row length up to 70 and sampled lengths up to 4100; and so
+  must the search narrowed by the row's 64-bucket guide (cdf_guide_entry,
+  cdf_search_in), as the Nested WAIT kernel draws.
 """
 import os
 import shutil
@@ -65,7 +67,12 @@ int main() {
           case 3: w2 = (q & 1) ? 0u : 0xffffffffu; break;
           default: w2 = (uint32_t)(g() % 2000);
         }
-        ++n2; bad2 += cdf_search(row.data(), cap, w2) != linear(row.data(), cap, w2);
+        const int32_t want = linear(row.data(), cap, w2);
+        ++n2; bad2 += cdf_search(row.data(), cap, w2) != want;
+        const int b = (int)(w2 >> 26);
+        const int32_t glo = cdf_guide_entry(row.data(), cap, b);
+        const int32_t ghi = cdf_guide_entry(row.data(), cap, b + 1);
+        ++n2; bad2 += cdf_search_in(row.data(), glo, ghi, w2) != want;
       }
     }
   }
