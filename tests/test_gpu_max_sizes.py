@@ -77,3 +77,21 @@ def test_wait_and_fcfs_8_types_at_64_per_wavefront():
     print(f"[gpu] 8 types, WAIT and FCFS, {R} replicas each", flush=True)
     _sampled(B, [W.Job(wait, 3, W.ids(R)), W.Job(fcfs, 4, W.ids(R))], 600,
              "WAIT and FCFS, 8 types, 64/wave")
+
+
+@pytest.mark.parametrize("cap", [65535, 70000])
+def test_nested_long_output_rows(cap):
+    """Output-length rows of 65,534 and 69,999 entries: the largest row the
+    kernel's 16-bit search guide covers, and one past it (the guide is then
+    off and the whole row is searched).  Short geometric lengths (mean 40)
+    with the rest of the row saturated, two segments, every replica against
+    the oracle."""
+    from tests.gpu_util import check
+    B = sim_module()
+    rng = np.random.default_rng(cap)
+    cdf = np.stack([W.geometric_cdf_table(40.0, cap), W.geometric_cdf_table(25.0, cap)])
+    wl = W.Workload(prompt_len=[16, 48], lam=[0.05, 0.03], d0=5.0, d1=0.001, C=cap + 4096,
+                    policy="nested", n=[2, 1], out_cap=cap, out_cdf=cdf, seg_end=[64, cap],
+                    hist_edges=W.default_edges(5.0, 40), record_capacity=1 << 12)
+    check(B, [W.Job(wl, int(rng.integers(0, 2**63)), W.ids(9))], 600,
+          f"nested, output rows of {cap - 1} entries")
