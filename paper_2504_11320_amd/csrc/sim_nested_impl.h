@@ -128,7 +128,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   double(&s_rf)[MT][NP] = s_prof.f;
   double(&s_fmax)[MT] = s_prof.fmax;
   __shared__ uint64_t s_seed[LN];
-  __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
+  __shared__ uint32_t s_rid[LN];
+  // refill requests of one pass, all types together: lane, type, first draw
+  __shared__ uint8_t s_req_lane[MT * LN], s_req_j[MT * LN];
+  __shared__ uint32_t s_req_k[MT * LN];
+  __shared__ double s_lam[MT];
   __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
   __shared__ int64_t s_M[LT][LN], s_B[LT][LN];
   __shared__ int32_t s_l[MT], s_lp[MT];
@@ -185,6 +189,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     for (int j = tx; j < MT; j += 64) {
       s_l[j] = j < m ? J.l[j] : 0;
       s_lp[j] = j < m ? J.lp[j] : 1;
+      s_lam[j] = j < m ? J.lambda[j] : 0.0;
     }
     for (int k = tx; k < LT; k += 64) {
       SegConst c;
@@ -606,38 +611,45 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       const int nact = __popcll(act);
       const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)act, 0u));
+      // the requests of every type are gathered first and drawn in one pass,
+      // so the types' memory round trips (CDF searches) overlap
+      int nreq = 0;  // wavefront-uniform
       for (int j = 0; j < m; ++j) {
         const uint32_t ge = s_gend[j][tx];
         const uint32_t avail = ge - s_k[j][tx] - 1u;
         if (__ballot(avail < kLow) == 0) continue;
         const bool room = avail <= (uint32_t)(GR - GU);
         const uint64_t need = __ballot(room);
-        const int p = __popcll(need);
         if (room) {
-          const int rk = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(need >> 32),
-                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
-          s_req_lane[rk] = (uint32_t)tx;
+          const int rk = nreq + (int)__builtin_amdgcn_mbcnt_hi(
+                                    (uint32_t)(need >> 32),
+                                    __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
+          s_req_lane[rk] = (uint8_t)tx;
+          s_req_j[rk] = (uint8_t)j;
           s_req_k[rk] = ge;
+          s_gend[j][tx] = ge + GU;  // read again only after the pass
         }
+        nreq += __popcll(need);
+      }
+      if (nreq > 0) {
         wave_lds_sync();
-        const int total = p * GU;
-        const double lamj = J.lambda[j];
-        const uint32_t *row = row_of(j);
+        const int total = nreq * GU;
         for (int base = 0; base < total; base += nact) {
           const int w = base + wrank;
           if (w < total) {
             const int ln = (int)s_req_lane[w / GU];
+            const int j = (int)s_req_j[w / GU];
             const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
             int32_t Lj = 1;
             uint32_t w3;
-            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lamj, row, cap,
-                                            &Lj, TV ? &w3 : nullptr, guide_of(j));
+            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, s_lam[j],
+                                            row_of(j), cap, &Lj, TV ? &w3 : nullptr,
+                                            guide_of(j));
             s_glen[j][k % GR][ln] = Lj;
             if constexpr (TV) s_w3[j][k % GR][ln] = w3;
           }
         }
         wave_lds_sync();
-        if (room) s_gend[j][tx] = ge + GU;
       }
     }
 
