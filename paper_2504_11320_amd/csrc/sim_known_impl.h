@@ -69,7 +69,11 @@ sim_known_kernel(KArgs A) {
   double(&s_rf)[MT][NP] = s_prof.f;
   double(&s_fmax)[MT] = s_prof.fmax;
   __shared__ uint64_t s_seed[LN];
-  __shared__ uint32_t s_rid[LN], s_req_lane[LN], s_req_k[LN];
+  __shared__ uint32_t s_rid[LN];
+  // refill requests of one pass, all types together: lane, type, first draw
+  __shared__ uint8_t s_req_lane[MT * LN], s_req_j[MT * LN];
+  __shared__ uint32_t s_req_k[MT * LN];
+  __shared__ double s_lamj[MT];
   // The last WB records pushed on each resident deque are also kept in LDS,
   // so LIFO evictions (which pop the back) rarely read HBM.  Launches with
   // time-varying rates run two wavefronts per SIMD at 16 replicas each; a
@@ -106,6 +110,7 @@ sim_known_kernel(KArgs A) {
     const double *edges_g = (const double *)(A.ws + J->off_edges);
     for (int b = threadIdx.x; b <= n_hist; b += 64)
       s_edges[b] = b < n_hist ? edges_g[b] : INFINITY;
+    for (int j = threadIdx.x; j < MT; j += 64) s_lamj[j] = j < m ? J->lambda[j] : 0.0;
     if (tv) {
       const double *rg = (const double *)(A.ws + J->off_rate);
       for (int i = threadIdx.x; i < P; i += 64) s_rt[i] = rg[i];
@@ -513,6 +518,9 @@ sim_known_kernel(KArgs A) {
       const int nact = __popcll(act);
       const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)act, 0u));
+      // the requests of every type are gathered first and drawn in one pass
+      // (fewer passes when several types run low in the same batch)
+      int nreq = 0;  // wavefront-uniform
 #pragma unroll
       for (int j = 0; j < MT; ++j) {
         if (j >= m) continue;
@@ -520,28 +528,33 @@ sim_known_kernel(KArgs A) {
         if (__ballot(avail < kLow) == 0) continue;
         const bool room = avail <= (uint32_t)(GR - GU);
         const uint64_t need = __ballot(room);
-        const int p = __popcll(need);
         if (room) {
-          const int rk = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(need >> 32),
-                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
-          s_req_lane[rk] = (uint32_t)tx;
+          const int rk = nreq + (int)__builtin_amdgcn_mbcnt_hi(
+                                    (uint32_t)(need >> 32),
+                                    __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
+          s_req_lane[rk] = (uint8_t)tx;
+          s_req_j[rk] = (uint8_t)j;
           s_req_k[rk] = gend[j];
+          gend[j] += GU;  // the draws land before the next use
         }
+        nreq += __popcll(need);
+      }
+      if (nreq > 0) {
         wave_lds_sync();
-        const int total = p * GU;
+        const int total = nreq * GU;
         for (int base = 0; base < total; base += nact) {
           const int w = base + wrank;
           if (w < total) {
             const int ln = (int)s_req_lane[w / GU];
+            const int j = (int)s_req_j[w / GU];
             const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
             uint32_t w3;
-            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, lam[j],
+            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, s_lamj[j],
                                             nullptr, 0, nullptr, TV ? &w3 : nullptr);
             if constexpr (TV) s_w3[j][k % GR][ln] = w3;
           }
         }
         wave_lds_sync();
-        if (room) gend[j] += GU;
       }
     }
 
