@@ -359,8 +359,10 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
     int32_t nmax = 0;  // largest job: no wavefront needs more lanes
     for (int i = 0; i < n_jobs; ++i)
       if (launch_kind(jobs[i].pol) == pk) nmax = std::max(nmax, jobs[i].n);
-    // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32
-    int lanes = pk == WS_NESTED_WAIT ? 32 : 64;
+    // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32; so
+    // do the known-length kernels with up to 4 types (their 64-lane LDS
+    // footprint would leave half of a CU's SIMDs idle), except replays
+    int lanes = pk == WS_NESTED_WAIT ? 32 : (Lo.max_m[pk] <= 4 && !any_trace ? 32 : 64);
     const int min_lanes = pk == WS_NESTED_WAIT ? 4 : 8;
     bool any_tv = false;
     for (int i = 0; i < n_jobs; ++i)

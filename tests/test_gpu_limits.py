@@ -2,10 +2,12 @@
 
 * Maximum model sizes against the oracle: 8 request types for WAIT and FCFS,
   16 types and 16 segments for Nested WAIT, 255 histogram edges.
-* Launches large enough that the host packs 16, 32 or 64 replicas per
-  wavefront: a replica's outputs depend only on (model, policy, seed,
-  replica id, horizon), so the same replicas run alone (8 per wavefront) must
-  give bit-identical results.
+* Launches large enough that the host packs 16 or 32 replicas per wavefront
+  (known-length kernels with up to 4 types stop at 32 and add wavefronts;
+  64 per wavefront is covered with 8 types in test_gpu_max_sizes.py): a
+  replica's outputs depend only on (model, policy, seed, replica id,
+  horizon), so the same replicas run alone (8 per wavefront) must give
+  bit-identical results.
 """
 import numpy as np
 import pytest
@@ -69,7 +71,7 @@ def _subset_equal(B, jobs, horizon, picks, ctx):
     print(f"[gpu] {ctx}: {len(idx)} replicas identical to a separate launch", flush=True)
 
 
-@pytest.mark.parametrize("reps", [512, 1024, 2048])   # 16, 32, 64 per wavefront
+@pytest.mark.parametrize("reps", [512, 1024, 2048])   # 16, 32, 32 (4,096 wavefronts)
 def test_wait_layouts_agree(B, reps):
     jobs = W.config2(replicas=reps)
     _subset_equal(B, jobs, 400, [(0, 0, 33), (17, reps - 40, reps), (31, 5, 9)],

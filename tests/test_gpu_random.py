@@ -67,8 +67,8 @@ def test_unit_thresholds(m):
     """WAIT and WAIT-no-wait launches whose jobs all have n_j = 1 run the
     unit-threshold kernels (at most one admission and one completion per type
     and batch): random models with m types against the oracle, at 8 replicas
-    per wavefront; a launch of 66,000 replicas (64 per wavefront) gives the
-    same replicas bit-identical results."""
+    per wavefront; a launch of 66,000 replicas (64 per wavefront with 6 or 8
+    types, 32 with fewer) gives the same replicas bit-identical results."""
     B = sim_module()
     rng = np.random.default_rng(500 + m)
     jobs = []
