@@ -71,7 +71,7 @@ def _subset_equal(B, jobs, horizon, picks, ctx):
     print(f"[gpu] {ctx}: {len(idx)} replicas identical to a separate launch", flush=True)
 
 
-@pytest.mark.parametrize("reps", [512, 1024, 2048])   # 16, 32, 32 (4,096 wavefronts)
+@pytest.mark.parametrize("reps", [512, 1024, 2048])   # 16, 32, 32 (2,048 wavefronts)
 def test_wait_layouts_agree(B, reps):
     jobs = W.config2(replicas=reps)
     _subset_equal(B, jobs, 400, [(0, 0, 33), (17, reps - 40, reps), (31, 5, 9)],
