@@ -73,3 +73,22 @@ def test_more_than_one_gpu_is_refused():
     assert p.returncode == 2
     assert "one GPU" in p.stderr
     assert p.stdout.strip() == ""
+
+
+def test_every_workload_runs_on_the_oracle(oracle_lib):
+    """Each workload bench.py can time builds its jobs, the policy label and
+    the CPU-baseline job picks are consistent with them, and one replica of
+    each sampled job runs 50 batches on the oracle without a flag."""
+    from oracle import oracle as O
+    table = bench._workloads()
+    assert next(iter(table)) == "wait-llama"
+    for name, (desc, build, horizon, policy, picks) in table.items():
+        jobs = build(4)
+        assert desc and horizon > 0, name
+        assert all(0 <= p < len(jobs) for p in picks), name
+        pols = {j.wl.policy for j in jobs}
+        assert pols <= set(policy.split("+")), (name, pols, policy)
+        for p in picks:
+            j = jobs[p]
+            r = O.run_job(W.Job(j.wl, j.seed, j.replica_ids[:1]), 50)
+            assert r["batches"][0] == 50 and r["flags"][0] == 0, (name, p)
