@@ -4,6 +4,8 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -445,6 +447,34 @@ uint64_t results_hist_offset(const Layout &Lo) {
       return fail(WS_EDEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
   } while (0)
 
+// Side streams (default priority) on which the launches of a call's second
+// and third policy kinds run beside the first: the kinds touch disjoint
+// replicas, so they can share the GPU.  Created once per device and kept for
+// the life of the process; each call orders them with events of its own.
+hipError_t side_streams(hipStream_t out[2]) {
+  static std::mutex mu;
+  static std::map<int, std::pair<hipStream_t, hipStream_t>> streams;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = streams.find(dev);
+  if (it == streams.end()) {
+    hipStream_t a = nullptr, b = nullptr;
+    e = hipStreamCreateWithFlags(&a, hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+    e = hipStreamCreateWithFlags(&b, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      (void)hipStreamDestroy(a);
+      return e;
+    }
+    it = streams.emplace(dev, std::make_pair(a, b)).first;
+  }
+  out[0] = it->second.first;
+  out[1] = it->second.second;
+  return hipSuccess;
+}
+
 KArgs base_args(const Layout &Lo, void *d_ws) {
   KArgs A;
   std::memset(&A, 0, sizeof(A));
@@ -572,8 +602,25 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
   A.resume = resume ? 1 : 0;
   A.btrace = btrace_cap > 0 ? (uint8_t *)d_btrace : nullptr;
   A.btrace_cap = btrace_cap;
+  // a call with several policy kinds runs the second and third kinds on side
+  // streams, forked from and joined back into the caller's stream
+  int kinds = 0;
+  for (int pk = 0; pk < 3; ++pk) kinds += Lo.list_count[pk] > 0 ? 1 : 0;
+  hipStream_t side[2] = {nullptr, nullptr};
+  hipEvent_t fork = nullptr;
+  if (kinds > 1) {
+    HIP_TRY(side_streams(side));
+    HIP_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+    HIP_TRY(hipEventRecord(fork, s));
+  }
+  int launched = 0;
   for (int pk = 0; pk < 3; ++pk) {
     if (Lo.list_count[pk] == 0) continue;
+    hipStream_t ls = s;
+    if (launched > 0) {
+      ls = side[launched - 1];
+      HIP_TRY(hipStreamWaitEvent(ls, fork, 0));
+    }
     KArgs B = A;
     B.off_list = Lo.list_off[pk];
     B.n_list = Lo.list_count[pk];
@@ -590,12 +637,21 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     }
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)
-      e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, s);
+      e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, ls);
     else
-      e = pk == WS_WAIT ? launch_known_wait(Lo.max_m[pk], B, s)
-                        : launch_known_fcfs(Lo.max_m[pk], B, s);
+      e = pk == WS_WAIT ? launch_known_wait(Lo.max_m[pk], B, ls)
+                        : launch_known_fcfs(Lo.max_m[pk], B, ls);
     if (e != hipSuccess) return fail(WS_EDEVICE, std::string("launch: ") + hipGetErrorString(e));
+    if (launched > 0) {  // join: the caller's stream waits for this kind
+      hipEvent_t join = nullptr;
+      HIP_TRY(hipEventCreateWithFlags(&join, hipEventDisableTiming));
+      HIP_TRY(hipEventRecord(join, ls));
+      HIP_TRY(hipStreamWaitEvent(s, join, 0));
+      HIP_TRY(hipEventDestroy(join));  // released once it has completed
+    }
+    launched++;
   }
+  if (fork != nullptr) HIP_TRY(hipEventDestroy(fork));
   const int tb = 256;
   hipLaunchKernelGGL(export_kernel, dim3((unsigned)((Lo.R + tb - 1) / tb)), dim3(tb), 0, s, A,
                      (uint8_t *)d_results);
