@@ -212,7 +212,13 @@ int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
  * taken between calls (device to device, or to host and back into a workspace
  * of the same jobs) is a checkpoint, and resume = 1 on the restored copy
  * continues exactly as the original would.  Asynchronous
- * on hip_stream; `jobs` must be the ones given to wait_sim_prepare. */
+ * on hip_stream; `jobs` must be the ones given to wait_sim_prepare.  When the
+ * jobs use more than one policy kind, the kinds' kernels run concurrently:
+ * the second and third on two side streams that the library creates once per
+ * device and keeps, forked from hip_stream after its earlier work and joined
+ * back into it before the call's later work, so hip_stream still orders
+ * everything.  Calls from several host threads share those side streams
+ * (their work serialises there). */
 int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                      int32_t resume, void *d_workspace, size_t ws_bytes,
                      void *d_results, size_t results_bytes, void *hip_stream);
