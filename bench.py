@@ -1,21 +1,26 @@
 #!/usr/bin/env python3
 """Benchmark: simulated replica-iterations per second on one MI355X.
 
-One step is one pass of the whole simulation over the benchmark workload:
-the Llama-2-7B-shaped WAIT workload (3 request types, prompts 128/512/1024,
-outputs 64/256/512, mix 0.5/0.3/0.2, KV budget 131072 tokens, iteration time
-15 ms + 0.05 ms/token, thresholds (1,1,1)) at 32 arrival rates spanning
-0.5-1.2x the fluid stability boundary, 1024 replicas per rate, 1e5 batches
-per replica: 3.2768e9 replica-iterations per step.  Inputs (job tables) are
-copied to HBM before the timed region; every replica starts from the empty
-system in every step.
+The benchmark workload is the largest single-GPU configuration: Nested WAIT
+on a heavy-tailed 10-type mix (prompt lengths the decile medians of
+LogNormal(6, 0.8), output lengths clamp(ceil(LogNormal(5.5, 1.0)), 1, 4096),
+segments (128, 256, 512, 1024, 2048, 4096), thresholds 1, KV budget 262144
+tokens, iteration time 15 ms + 0.05 ms/token, rate 0.9x the fluid stability
+boundary), 8192 replicas x 1e6 batches = 8.19e9 replica-iterations.
+
+The job's horizon is split over the timed steps: step i advances every
+replica by its share of the horizon, resuming from the state the previous
+step left (step 0 starts from the empty system), so the K timed steps
+together run the whole job once.  Warmup steps run the same chunks on a
+separate workspace.  Job tables are copied to HBM before the timed region.
 
 Prints one JSON line.  The roofline object prices the simulation kernel
 against the ALU peak with an explicit operation model (lane-operations the
-method needs per arrival, batch, completion, eviction and idle wait; see the
-design notes), using the event counts the kernel itself returns.  The
-cpu_baseline object times the CPU oracle on a bounded sample of the same
-workload (2 rates x 256 replicas x the full horizon) on the host's cores.
+method needs per arrival, batch, completion, eviction and idle wait) and
+against the HBM peak with the record-traffic model (32 bytes per arrival and
+per completion), both from the event counts the kernel itself returns; the
+larger fraction binds.  The cpu_baseline object times the CPU oracle on a
+bounded sample of the same workload on the host threads the box allots.
 """
 from __future__ import annotations
 
@@ -114,10 +119,46 @@ def algorithmic_ops(res: dict, m: int, cdf_cap: int = 0, rate_pts: int = 0,
 
 
 def algorithmic_bytes(res: dict) -> float:
-    """Record traffic the method needs: 16 B written and read per queued
-    request (arrival and re-queue) and per admission/completion."""
-    ev = res["arrivals"].sum() + res["evictions"].sum()
-    return float(16 * 2 * ev + 16 * res["completions"].sum())
+    """Record traffic the method needs: 32 bytes per arrival and per
+    completion (a request record written when it queues and read when it
+    leaves, both ends of its life)."""
+    return float(32 * (res["arrivals"].sum() + res["completions"].sum()))
+
+
+def chunks(horizon: int, steps: int):
+    """Split a horizon into `steps` consecutive chunks (sizes differ by at most
+    one batch)."""
+    return [(i + 1) * horizon // steps - i * horizon // steps for i in range(steps)]
+
+
+def host_cpu() -> dict:
+    """The host's CPU model, logical CPU count and the CPUs this process may
+    run on."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        allowed = os.cpu_count() or 1
+    return {"model": model, "nproc": os.cpu_count() or 1, "allowed": allowed}
+
+
+def baseline_threads() -> int:
+    """Oracle threads: the CPUs this process may use, capped by the per-GPU
+    thread allotment the environment states (OMP_NUM_THREADS), else 16."""
+    cap = 16
+    try:
+        cap = max(1, int(os.environ.get("OMP_NUM_THREADS", "16")))
+    except ValueError:
+        pass
+    return max(1, min(host_cpu()["allowed"], cap))
 
 
 def source_hash(workload: str = "wait-llama") -> str:
@@ -128,9 +169,11 @@ def source_hash(workload: str = "wait-llama") -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(workload: str):
-    """HBM bytes per launch from the workload's committed rocprofv3 counter
-    summary, if there is one and it was taken on the current kernel source."""
+def traffic_from_profile(workload: str, rep_its_per_launch: float):
+    """Measured HBM bytes per launch: the DRAM bytes per replica-iteration of
+    the workload's committed rocprofv3 counter summary, times the
+    replica-iterations of one launch here; None if there is no summary or it
+    was not taken on the current kernel sources."""
     if workload not in PROFILES:
         return None
     path = os.path.join(ROOT, "profiles", PROFILES[workload][0] + "_hbm.md")
@@ -138,48 +181,55 @@ def traffic_from_profile(workload: str):
         return None
     txt = open(path).read()
     h = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt)
-    b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    b = re.search(r"hbm_bytes_per_replica_iteration:\s*([0-9.eE+]+)", txt)
     if not h or not b or h.group(1) != source_hash(workload):
         return None
-    return float(b.group(1))
+    return float(b.group(1)) * rep_its_per_launch
 
 
 # Workloads this script can time (the first is the benchmark's).  Each entry:
-# (description, job builder, horizon, policy, jobs sampled by the CPU baseline)
+# (description, job builder, horizon, policy, jobs sampled by the CPU
+# baseline, replicas of each sampled job the CPU baseline runs)
 def _workloads():
     import workloads as W
     return {
+        "nested-heavytail": ("Nested WAIT, heavy-tailed 10-type mix: prompts the decile "
+                             "medians of LogNormal(6, 0.8), outputs clamp(ceil(LogNormal"
+                             "(5.5, 1.0)), 1, 4096), segments (128, 256, 512, 1024, 2048, "
+                             "4096), thresholds 1, C = 262144, 0.9x the fluid boundary, "
+                             "8192 replicas x 1e6 batches",
+                             lambda reps: W.config5(), 1000000, "nested", [0], 128),
         "wait-llama": ("WAIT, Llama-2-7B-shaped 3-type synthetic mix, 32 rates "
                        "0.5-1.2x fluid boundary, 1024 replicas each",
-                       lambda reps: W.config2(replicas=reps), 100000, "wait", [0, 31]),
+                       lambda reps: W.config2(replicas=reps), 100000, "wait", [0, 31], 256),
         "nested-geometric": ("Nested WAIT, 3 types, geometric outputs capped at 2048, "
                              "segments (64,256,1024,2048), 32 rates x 1024 replicas",
-                             lambda reps: W.config3(replicas=reps), 100000, "nested", [0, 31]),
+                             lambda reps: W.config3(replicas=reps), 100000, "nested", [0, 31],
+                             128),
         "wait-sweep": ("WAIT threshold grid 16x16 x 16 rates x 16 replicas plus FCFS "
                        "on the same streams",
-                       lambda reps: W.config4(), 100000, "wait+fcfs", [0, 4096]),
-        "nested-heavytail": ("Nested WAIT, 10 lognormal-decile prompt types, lognormal "
-                             "outputs capped at 4096, 6 segments, 8192 replicas",
-                             lambda reps: W.config5(), 1000000, "nested", [0]),
+                       lambda reps: W.config4(), 100000, "wait+fcfs", [0, 4096], 16),
         "nowait-llama": ("WAIT-no-wait (thresholds 1, 1, 1) on the Llama-2-7B-shaped "
                          "3-type mix, 32 rates 0.5-1.2x fluid boundary, 1024 replicas each",
                          lambda reps: _nowait(W.config2(replicas=reps)), 100000,
-                         "wait-nowait", [0, 31]),
+                         "wait-nowait", [0, 31], 256),
         "wait-cyclic": ("WAIT on the Llama-2-7B-shaped 3-type mix with cyclic "
                         "time-varying rates lam_j (1 + 0.5 sin(4 pi t / 8e8 ms + 2 pi j / 3)), "
                         "32 rates 0.5-1.2x fluid boundary, 1024 replicas each",
-                        lambda reps: W.config_cyclic(replicas=reps), 100000, "wait", [0, 31]),
+                        lambda reps: W.config_cyclic(replicas=reps), 100000, "wait", [0, 31],
+                        256),
         "pd-decode": ("decode-only p630d20 (PD-disaggregated decode server: 630-token "
                       "context, 20 generated tokens), WAIT with fluid thresholds and FCFS "
                       "with a 1% reserve, 9 rates 0.1-0.5/ms, 1024 replicas each",
-                      lambda reps: W.config_pd(replicas=reps), 100000, "wait+fcfs", [8, 17]),
+                      lambda reps: W.config_pd(replicas=reps), 100000, "wait+fcfs", [8, 17],
+                      64),
         "fcfs-chunked": ("FCFS with a 1% reserve and 512-token chunked prefill (the "
                          "Sarathi-style baseline) on the Llama-2-7B-shaped 3-type mix, 32 "
                          "rates 0.5-1.2x fluid boundary, 1024 replicas each",
                          lambda reps: W.config_chunked(replicas=reps), 100000, "fcfs",
-                         [0, 31]),
+                         [0, 31], 256),
         "wait-small": ("WAIT, 2 types (16/8, 32/16), C = 2048, 64 replicas",
-                       lambda reps: W.config1(), 10000, "wait", [0]),
+                       lambda reps: W.config1(), 10000, "wait", [0], 64),
     }
 
 
@@ -190,8 +240,8 @@ def _nowait(jobs):
 
 
 def cpu_baseline(jobs, pick, horizon: int, replicas: int, threads: int) -> dict:
-    """The oracle on a bounded sample: `replicas` replicas of each picked job,
-    the full horizon (at most 1e5 batches)."""
+    """The oracle on a bounded sample: `replicas` replicas of each picked job
+    over the first min(horizon, 1e5) batches."""
     from oracle import oracle as O
     import numpy as np
     import workloads as W
@@ -205,24 +255,28 @@ def cpu_baseline(jobs, pick, horizon: int, replicas: int, threads: int) -> dict:
         total += int(r["batches"].sum())
     dt = time.perf_counter() - t0
     n = min(replicas, min(jobs[i].n for i in pick))
+    cpu = host_cpu()
     return {"value": total / dt, "unit": UNIT, "cores": threads, "kind": "oracle",
             "sample": f"jobs {pick} of {len(jobs)} x {n} replicas x {horizon} batches "
-                      f"({total} replica-iterations, {dt:.1f} s)"}
+                      f"({total} replica-iterations, {dt:.1f} s)",
+            "cpu_model": cpu["model"], "nproc": cpu["nproc"], "cpus_allowed": cpu["allowed"]}
 
 
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="wait-llama",
-                    help="wait-llama (the benchmark), nested-geometric, wait-sweep, "
-                         "nested-heavytail, nowait-llama, wait-cyclic, pd-decode, "
-                         "fcfs-chunked, wait-small")
-    ap.add_argument("--horizon", type=int, default=0, help="batches (0: the workload's)")
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="nested-heavytail",
+                    help="nested-heavytail (the benchmark), wait-llama, nested-geometric, "
+                         "wait-sweep, nowait-llama, wait-cyclic, pd-decode, fcfs-chunked, "
+                         "wait-small")
+    ap.add_argument("--horizon", type=int, default=0,
+                    help="batches per replica over all timed steps (0: the workload's)")
     ap.add_argument("--replicas", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-replicas", type=int, default=256)
+    ap.add_argument("--cpu-replicas", type=int, default=0,
+                    help="replicas per sampled job in the CPU baseline (0: the workload's)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (used to "
                          "scale the HBM byte counters)")
@@ -244,6 +298,9 @@ def main() -> int:
               f"supported (replicas shard across GPUs with no communication; this "
               f"benchmark measures a single MI355X)", file=sys.stderr)
         return 2
+    if args.steps < 1:
+        print("bench.py: --steps must be at least 1", file=sys.stderr)
+        return 2
 
     import numpy as np
     import torch
@@ -259,26 +316,34 @@ def main() -> int:
     if args.workload not in table:
         print(f"bench.py: unknown workload {args.workload}", file=sys.stderr)
         return 2
-    desc, build, horizon0, policy, pick = table[args.workload]
-    args.horizon = args.horizon or horizon0
+    desc, build, horizon0, policy, pick, cpu_reps = table[args.workload]
+    horizon = args.horizon or horizon0
     jobs = build(args.replicas)
     m = max(j.wl.m for j in jobs)
     cdf_cap = max((j.wl.out_cap for j in jobs if j.wl.out_cdf is not None), default=0)
     rate_pts = max((len(j.wl.rate_t) for j in jobs if j.wl.rate_t is not None), default=0)
     cpa = candidates_per_arrival(jobs)
+    parts = chunks(horizon, args.steps)
+    stream = torch.cuda.current_stream()
+
+    if args.warmup > 0:  # the same chunks on a workspace of its own
+        warm = B.Simulation(jobs)
+        warm.prepare()
+        for i in range(args.warmup):
+            warm.advance(parts[i % len(parts)], resume=i > 0)
+        torch.cuda.synchronize()
+        del warm
+        torch.cuda.empty_cache()
+
     sim = B.Simulation(jobs)
     sim.prepare()
-    stream = torch.cuda.current_stream()
-    for _ in range(args.warmup):
-        sim.advance(args.horizon, resume=False)
     torch.cuda.synchronize()
-
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        sim.advance(args.horizon, resume=False)
+    for i, h in enumerate(parts):
+        sim.advance(h, resume=i > 0)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -287,25 +352,33 @@ def main() -> int:
 
     res = sim.results()
     rep_its = int(res["batches"].sum())
-    if rep_its != len(res["batches"]) * args.horizon or np.any(res["flags"] & 3):
+    if rep_its != len(res["batches"]) * horizon or np.any(res["flags"] & 3):
         print("bench.py: some replicas stopped early (flags set)", file=sys.stderr)
-    value = rep_its / (ms_step / 1e3)
+    value = rep_its / (ms_total / 1e3)
 
+    # Roofline of the simulation kernel: algorithmic work of the whole job
+    # over the time of its launches (one launch per step).
+    secs = ms_total / 1e3
     ops = algorithmic_ops(res, m, cdf_cap, rate_pts, cpa)
-    achieved = ops / (ms_step / 1e3)
-    full = args.horizon == horizon0 and args.replicas == 1024
-    traffic = traffic_from_profile(args.workload) if full else None
-    roofline = {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK,
-                "unit": "lane-ops/s", "frac": achieved / ALU_PEAK,
+    nbytes = algorithmic_bytes(res)
+    alu = {"achieved": ops / secs, "peak": ALU_PEAK, "unit": "lane-ops/s"}
+    hbm = {"achieved": nbytes / secs, "peak": HBM_PEAK, "unit": "B/s"}
+    alu["frac"] = alu["achieved"] / ALU_PEAK
+    hbm["frac"] = hbm["achieved"] / HBM_PEAK
+    bind, bound = (alu, "alu") if alu["frac"] >= hbm["frac"] else (hbm, "hbm")
+    full = args.horizon in (0, horizon0) and args.replicas == 1024
+    traffic = traffic_from_profile(args.workload, rep_its / args.steps) if full else None
+    roofline = {"bound": bound, "achieved": bind["achieved"], "peak": bind["peak"],
+                "unit": bind["unit"], "frac": bind["frac"],
+                # measured DRAM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE,
+                # scaled by a plain copy's counters), null if not taken on these sources
                 "traffic": traffic,
+                "alu_frac": alu["frac"], "hbm_frac": hbm["frac"],
                 "algorithmic_ops_per_replica_iteration": ops / rep_its,
-                "algorithmic_bytes_per_launch": algorithmic_bytes(res),
-                # the HBM side of the same launch: algorithmic record bytes and
-                # the measured DRAM bytes (traffic), each per second over the
-                # 8 TB/s peak
-                "hbm_algorithmic_frac": algorithmic_bytes(res) / (ms_step / 1e3) / HBM_PEAK,
-                "hbm_measured_frac": (traffic / (ms_step / 1e3) / HBM_PEAK
+                "algorithmic_bytes_per_replica_iteration": nbytes / rep_its,
+                "hbm_measured_frac": (traffic * args.steps / secs / HBM_PEAK
                                       if traffic is not None else None),
+                "launches": args.steps,
                 "kernel": (f"sim_nested_kernel ({m} types)" if policy == "nested"
                            else f"sim_known_kernel ({policy}, {m} types)")
                           + (f", time-varying rates ({rate_pts} points, "
@@ -317,14 +390,14 @@ def main() -> int:
            "dtype": "f64", "data": "synthetic",
            "config": {"workload": desc, "name": args.workload,
                       "replicas": len(res["batches"]), "jobs": len(jobs),
-                      "horizon_batches": args.horizon,
-                      "replica_iterations_per_step": rep_its, "policy": policy,
+                      "horizon_batches": horizon, "batches_per_step": parts[0],
+                      "replica_iterations": rep_its, "policy": policy,
                       "kv_budget_tokens": int(max(j.wl.C for j in jobs))},
            "roofline": roofline,
            "wall_s_timed": wall}
     if not args.no_cpu_baseline:
-        threads = max(1, min(os.cpu_count() or 1, 16))
-        out["cpu_baseline"] = cpu_baseline(jobs, pick, args.horizon, args.cpu_replicas, threads)
+        out["cpu_baseline"] = cpu_baseline(jobs, pick, horizon, args.cpu_replicas or cpu_reps,
+                                           baseline_threads())
     print(json.dumps(out), flush=True)
     return 0
 

@@ -227,12 +227,14 @@ int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
  * batch's launch time, duration, tokens,
  * prefill processings (FCFS chunks included), selected prompts, completions,
  * evictions before the launch (Nested WAIT's projected-state repair) and
- * after the completion, and the resident memory, waiting and resident prompts
- * after the repair. */
+ * after the completion, the resident memory, waiting and resident prompts
+ * after the repair, and (Nested WAIT; 0 for the other policies) the
+ * projected resident memory M_res(Q+) after the pre-launch repair
+ * (Algorithm 4, Appendix B.1). */
 typedef struct {
   double t_launch, tau;
   int64_t tokens, prefills, selected, completions, evict_pre, evict_post,
-      mem_after, waiting_after, resident_after, pad;
+      mem_after, waiting_after, resident_after, mplus;
 } ws_batch_rec;
 
 /* wait_sim_advance, also writing ws_batch_rec records to d_btrace (DEVICE

@@ -59,12 +59,18 @@ class _BatchRec(C.Structure):
     _fields_ = [("t_launch", C.c_double), ("tau", C.c_double)] + [
         (f, C.c_int64) for f in ("tokens", "prefills", "selected", "completions",
                                  "evict_pre", "evict_post", "mem_after",
-                                 "waiting_after", "resident_after", "pad")]
+                                 "waiting_after", "resident_after", "mplus")]
 
 
 class _ReqLog(C.Structure):
     _fields_ = [("arr", C.c_void_p), ("done", C.c_void_p),
-                ("first", C.c_void_p), ("cap", C.c_int64)]
+                ("first", C.c_void_p), ("cap", C.c_int64),
+                ("ev_id", C.c_void_p), ("ev_batch", C.c_void_p),
+                ("ev_kind", C.c_void_p), ("ev_cap", C.c_int64), ("n_ev", C.c_int64)]
+
+
+# eviction kinds of the eviction log (wait_oracle.h)
+EV_POST, EV_POST_FALLBACK, EV_PRE, EV_PRE_FALLBACK = 0, 1, 2, 3
 
 
 _lib = None
@@ -81,31 +87,37 @@ def build(force: bool = True) -> str:
     return LIB
 
 
+def load(path: str):
+    """Load an oracle library built from wait_oracle.c and declare its
+    functions."""
+    L = C.CDLL(path)
+    L.oracle_run.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_uint32,
+                             C.c_int64, C.POINTER(_Result), C.c_void_p,
+                             C.c_void_p, C.c_int64, C.c_void_p]
+    L.oracle_run_many.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_void_p,
+                                  C.c_int32, C.c_int64, C.c_void_p,
+                                  C.c_void_p, C.c_int32]
+    L.oracle_philox4x32_10.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
+    L.oracle_uniform.argtypes = [C.c_uint32, C.c_uint32]
+    L.oracle_uniform.restype = C.c_double
+    L.oracle_ln.argtypes = [C.c_double]
+    L.oracle_ln.restype = C.c_double
+    L.oracle_arrival_times.argtypes = [C.POINTER(_Config), C.c_uint64,
+                                       C.c_uint32, C.c_int32, C.c_int64,
+                                       C.c_void_p, C.c_void_p, C.c_void_p]
+    L.oracle_arrival_times.restype = C.c_int
+    L.oracle_draw.argtypes = [C.c_uint64, C.c_uint32, C.c_int32, C.c_uint32,
+                              C.c_double, C.c_void_p, C.c_int32,
+                              C.POINTER(C.c_double), C.POINTER(C.c_int32)]
+    return L
+
+
 def lib():
     global _lib
     if _lib is None:
         if _stale():
             build(force=True)
-        L = C.CDLL(LIB)
-        L.oracle_run.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_uint32,
-                                 C.c_int64, C.POINTER(_Result), C.c_void_p,
-                                 C.c_void_p, C.c_int64, C.c_void_p]
-        L.oracle_run_many.argtypes = [C.POINTER(_Config), C.c_uint64, C.c_void_p,
-                                      C.c_int32, C.c_int64, C.c_void_p,
-                                      C.c_void_p, C.c_int32]
-        L.oracle_philox4x32_10.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
-        L.oracle_uniform.argtypes = [C.c_uint32, C.c_uint32]
-        L.oracle_uniform.restype = C.c_double
-        L.oracle_ln.argtypes = [C.c_double]
-        L.oracle_ln.restype = C.c_double
-        L.oracle_arrival_times.argtypes = [C.POINTER(_Config), C.c_uint64,
-                                           C.c_uint32, C.c_int32, C.c_int64,
-                                           C.c_void_p, C.c_void_p, C.c_void_p]
-        L.oracle_arrival_times.restype = C.c_int
-        L.oracle_draw.argtypes = [C.c_uint64, C.c_uint32, C.c_int32, C.c_uint32,
-                                  C.c_double, C.c_void_p, C.c_int32,
-                                  C.POINTER(C.c_double), C.POINTER(C.c_int32)]
-        _lib = L
+        _lib = load(LIB)
     return _lib
 
 
@@ -198,9 +210,11 @@ def run_job(job, horizon: int, threads: int = 0) -> dict:
 
 
 def run_one(wl, seed: int, replica_id: int, horizon: int, btrace_cap: int = 0,
-            rlog_cap: int = 0) -> dict:
-    """One replica with optional per-batch trace and per-request log."""
-    L = lib()
+            rlog_cap: int = 0, evlog_cap: int = 0, library=None) -> dict:
+    """One replica with optional per-batch trace, per-request log and
+    eviction log (a list of (batch, request id, kind) in eviction order).
+    `library`: another build of the oracle (a handle from load())."""
+    L = library if library is not None else lib()
     pin = _Pinned(wl)
     res = _Result()
     nb = (len(wl.hist_edges) if wl.hist_edges is not None else 0) + 1
@@ -208,11 +222,15 @@ def run_one(wl, seed: int, replica_id: int, horizon: int, btrace_cap: int = 0,
     bt = (_BatchRec * max(btrace_cap, 1))()
     rl = None
     logs = None
-    if rlog_cap > 0:
-        logs = [np.full(rlog_cap, -2.0), np.full(rlog_cap, -2.0),
-                np.full(rlog_cap, -2.0)]
+    ev = None
+    if rlog_cap > 0 or evlog_cap > 0:
+        n = max(rlog_cap, 1)
+        logs = [np.full(n, -2.0), np.full(n, -2.0), np.full(n, -2.0)]
+        ev = [np.zeros(max(evlog_cap, 1), np.int64), np.zeros(max(evlog_cap, 1), np.int64),
+              np.zeros(max(evlog_cap, 1), np.int32)]
         rl = _ReqLog(logs[0].ctypes.data, logs[1].ctypes.data,
-                     logs[2].ctypes.data, rlog_cap)
+                     logs[2].ctypes.data, rlog_cap, ev[0].ctypes.data, ev[1].ctypes.data,
+                     ev[2].ctypes.data, evlog_cap, 0)
     L.oracle_run(C.byref(pin.cfg), C.c_uint64(seed), C.c_uint32(replica_id),
                  horizon, C.byref(res), hist.ctypes.data,
                  C.addressof(bt) if btrace_cap > 0 else None, btrace_cap,
@@ -225,8 +243,12 @@ def run_one(wl, seed: int, replica_id: int, horizon: int, btrace_cap: int = 0,
         out["batches_trace"] = [
             {f: getattr(bt[i], f) for f, _ in _BatchRec._fields_ if f != "pad"}
             for i in range(nbt)]
-    if logs is not None:
+    if rlog_cap > 0:
         out["req_arr"], out["req_done"], out["req_first"] = logs
+    if evlog_cap > 0:
+        n_ev = min(rl.n_ev, evlog_cap)
+        out["evictions_log"] = [(int(ev[1][i]), int(ev[0][i]), int(ev[2][i]))
+                                for i in range(n_ev)]
     return out
 
 

@@ -286,6 +286,8 @@ typedef struct {
   int64_t next_id;
   int64_t tmp_cap;
   int64_t *tmp;
+  int pre_launch;  /* evictions now are the pre-launch (Q+) repair's */
+  int64_t mplus;   /* Nested: M_res(Q+) after the pre-launch repair   */
 } sim_t;
 
 static int key_less(const req_t *x, const req_t *y) {
@@ -707,6 +709,7 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   }
 
   /* pre-launch repair: unselected boundary prompts, most recent first */
+  S->pre_launch = 1;
   while (mplus > c->C) {
     int64_t best = -1;
     for (int32_t k = 2; k <= c->nseg; k++)
@@ -731,6 +734,8 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
     mplus -= charge(S, &S->R[best]);
     evict(S, best, 1);
   }
+  S->pre_launch = 0;
+  S->mplus = mplus;
   if (mplus > c->C) S->out->flags |= OR_FLAG_OVERFLOW;
   return 1;
 }
@@ -775,6 +780,12 @@ static void evict(sim_t *S, int64_t r, int fallback) {
   S->out->evictions++;
   S->out->evicted_tokens += gen;
   if (fallback) S->out->fallback_evictions++;
+  if (S->rlog && S->rlog->ev_cap > 0 && S->rlog->n_ev < S->rlog->ev_cap) {
+    const int64_t e = S->rlog->n_ev++;
+    S->rlog->ev_id[e] = q->id;
+    S->rlog->ev_batch[e] = S->b;
+    S->rlog->ev_kind[e] = (S->pre_launch ? OR_EV_PRE : OR_EV_POST) + (fallback ? 1 : 0);
+  }
   q->s = 0;
   q->seg = 0;
   q->sel = 0;
@@ -952,6 +963,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
       }
       tokens = 0;
       prefill_l = 0;
+      S.mplus = 0;
       int got;
       if (is_wait(c))
         got = decide_wait(&S, &tokens, &prefill_l);
@@ -1029,6 +1041,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
       if (c->policy == OR_NESTED)
         for (int32_t k = 2; k <= c->nseg; k++) rr += S.bnd[k].len;
       br->resident_after = rr;
+      br->mplus = S.mplus;
     }
   }
 

@@ -74,19 +74,33 @@ typedef struct {
   uint32_t pad;
 } or_result;
 
-/* One record per batch, for hand-trace tests. */
+/* One record per batch, for hand-trace tests.  mplus: Nested WAIT's
+ * projected resident memory M_res(Q+) after the pre-launch repair (0 for
+ * the other policies). */
 typedef struct {
   double t_launch, tau;
   int64_t tokens, prefills, selected, completions, evict_pre, evict_post,
-      mem_after, waiting_after, resident_after, pad;
+      mem_after, waiting_after, resident_after, mplus;
 } or_batch_rec;
 
-/* Optional per-request log (request id = arrival order, 0-based). */
+/* Eviction kinds in the eviction log. */
+#define OR_EV_POST 0          /* after the completion update, boundary/LIFO */
+#define OR_EV_POST_FALLBACK 1 /* after the completion update, interior       */
+#define OR_EV_PRE 2           /* before launch (Nested Q+), boundary         */
+#define OR_EV_PRE_FALLBACK 3  /* before launch (Nested Q+), interior         */
+
+/* Optional per-request log (request id = arrival order, 0-based) and
+ * eviction log (one entry per eviction, in the order they happen). */
 typedef struct {
   double *arr;   /* arrival time            [cap] */
   double *done;  /* completion time or -1   [cap] */
   double *first; /* first-token time or -1  [cap] */
   int64_t cap;
+  int64_t *ev_id;    /* evicted request id            [ev_cap] */
+  int64_t *ev_batch; /* batch index of the eviction   [ev_cap] */
+  int32_t *ev_kind;  /* OR_EV_*                       [ev_cap] */
+  int64_t ev_cap;
+  int64_t n_ev;      /* evictions logged (written by the oracle) */
 } or_req_log;
 
 int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,

@@ -36,7 +36,7 @@ F64_FIELDS = ["t_end", "busy_time", "lat_area", "ttft_area",
 BATCH_REC = np.dtype([("t_launch", np.float64), ("tau", np.float64)] + [
     (f, np.int64) for f in ("tokens", "prefills", "selected", "completions", "evict_pre",
                             "evict_post", "mem_after", "waiting_after", "resident_after",
-                            "pad")])
+                            "mplus")])
 
 
 class WsConfig(C.Structure):

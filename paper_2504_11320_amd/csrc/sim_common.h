@@ -98,7 +98,7 @@ struct KArgs {
 struct BatchRec {
   double t_launch, tau;
   int64_t tokens, prefills, selected, completions, evict_pre, evict_post, mem_after,
-      waiting_after, resident_after, pad;
+      waiting_after, resident_after, mplus;
 };
 static_assert(sizeof(BatchRec) == 96, "ws_batch_rec layout");
 

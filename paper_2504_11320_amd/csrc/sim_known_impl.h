@@ -859,7 +859,7 @@ sim_known_kernel(KArgs A) {
         }
         br.waiting_after = w;
         br.resident_after = res;
-        br.pad = 0;
+        br.mplus = 0;
         ((BatchRec *)A.btrace)[r * A.btrace_cap + batches] = br;
       }
     }

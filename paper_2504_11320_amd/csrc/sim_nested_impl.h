@@ -967,7 +967,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           if (k > 0) res += s_vt[k][tx] - s_vh[k][tx];
         }
         br.resident_after = res;
-        br.pad = 0;
+        br.mplus = mplus;
         ((BatchRec *)A.btrace)[r * A.btrace_cap + batches] = br;
       }
     }

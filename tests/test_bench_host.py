@@ -40,7 +40,23 @@ def test_algorithmic_counts_are_linear_in_events():
     assert bench.algorithmic_ops(res, 3) == pytest.approx(want)
     # the benchmark's event mix gives about 241 lane-operations per batch
     assert 235 < want / 1000 < 245
-    assert bench.algorithmic_bytes(res) == 16 * 2 * (590 + 1780) + 16 * 550
+    # record traffic: 32 bytes per arrival and per completion
+    assert bench.algorithmic_bytes(res) == 32 * (590 + 550)
+
+
+def test_chunks_cover_the_horizon():
+    for h, k in ((1000000, 20), (1000000, 3), (10000, 7), (5, 5)):
+        c = bench.chunks(h, k)
+        assert len(c) == k and sum(c) == h and max(c) - min(c) <= 1
+
+
+def test_baseline_threads_follow_the_allotment(monkeypatch):
+    monkeypatch.setenv("OMP_NUM_THREADS", "3")
+    assert bench.baseline_threads() == min(3, bench.host_cpu()["allowed"])
+    monkeypatch.delenv("OMP_NUM_THREADS")
+    assert 1 <= bench.baseline_threads() <= 16
+    cpu = bench.host_cpu()
+    assert cpu["nproc"] >= cpu["allowed"] >= 1
 
 
 def test_candidates_per_arrival():
@@ -52,19 +68,19 @@ def test_candidates_per_arrival():
 
 
 def test_profile_summary_lookup(monkeypatch):
-    path = os.path.join(ROOT, "profiles", bench.PROFILES["wait-llama"][0] + "_hbm.md")
+    path = os.path.join(ROOT, "profiles", bench.PROFILES["nested-heavytail"][0] + "_hbm.md")
     txt = open(path).read()
     h = re.search(r"source_sha256_16:\s*([0-9a-f]+)", txt).group(1)
-    b = float(re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt).group(1))
-    got = bench.traffic_from_profile("wait-llama")
-    if h == bench.source_hash("wait-llama"):
-        assert got == b
+    b = float(re.search(r"hbm_bytes_per_replica_iteration:\s*([0-9.eE+]+)", txt).group(1))
+    got = bench.traffic_from_profile("nested-heavytail", 1000.0)
+    if h == bench.source_hash("nested-heavytail"):
+        assert got == pytest.approx(1000.0 * b)
     else:
         assert got is None
     # a summary taken on other sources is not used
     monkeypatch.setattr(bench, "source_hash", lambda workload="wait-llama": "0" * 16)
-    assert bench.traffic_from_profile("wait-llama") is None
-    assert bench.traffic_from_profile("no-such-workload") is None
+    assert bench.traffic_from_profile("nested-heavytail", 1.0) is None
+    assert bench.traffic_from_profile("no-such-workload", 1.0) is None
 
 
 def test_more_than_one_gpu_is_refused():
@@ -81,8 +97,9 @@ def test_every_workload_runs_on_the_oracle(oracle_lib):
     each sampled job runs 50 batches on the oracle without a flag."""
     from oracle import oracle as O
     table = bench._workloads()
-    assert next(iter(table)) == "wait-llama"
-    for name, (desc, build, horizon, policy, picks) in table.items():
+    assert next(iter(table)) == "nested-heavytail"
+    for name, (desc, build, horizon, policy, picks, cpu_reps) in table.items():
+        assert cpu_reps >= 1, name
         jobs = build(4)
         assert desc and horizon > 0, name
         assert all(0 <= p < len(jobs) for p in picks), name

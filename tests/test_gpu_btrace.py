@@ -13,7 +13,7 @@ from tests.gpu_util import sim_module
 pytestmark = pytest.mark.gpu
 
 INT_F = ("tokens", "prefills", "selected", "completions", "evict_pre", "evict_post",
-         "mem_after", "waiting_after", "resident_after")
+         "mem_after", "waiting_after", "resident_after", "mplus")
 
 
 @pytest.fixture(scope="module")
@@ -95,3 +95,40 @@ def test_trace_across_resume(B):
     r1 = one.results()
     for k in plain:
         assert np.array_equal(plain[k], r1[k]), k
+
+
+def test_prelaunch_repair_hand_traces(B):
+    """The hand-traced instances of Nested WAIT's pre-launch repair
+    (golden/nested_prelaunch_repair.json: Q+ before and after the repair,
+    boundary LIFO across queues, interior fallback, OVERFLOW) replayed on
+    the GPU: every batch record equals the hand trace, and the results
+    equal the oracle's."""
+    from oracle import oracle as O
+    from tests.test_oracle_nested_prelaunch import _instances, _workload
+    inst = _instances()
+    names = sorted(inst)
+    jobs = [W.Job(_workload(inst[n]), 0, W.ids(3)) for n in names]
+    H = max(g["horizon"] for g in inst.values()) + 2
+    sim = B.Simulation(jobs)
+    sim.prepare()
+    tr = sim.advance_traced(H, H)
+    res = sim.results()
+    start = 0
+    for n, job in zip(names, jobs):
+        g = inst[n]
+        h = g["horizon"]
+        o = O.run_one(job.wl, 0, 0, H, btrace_cap=H)
+        for x in range(job.n):
+            r = start + x
+            nb = int(res["batches"][r])
+            assert nb == o["batches"], (n, x)
+            _compare(tr[r], o["batches_trace"], nb, f"{n} replica {x}")
+            for b, want in enumerate(g["batches"][:h]):
+                for f in INT_F[:-1]:
+                    assert tr[r][b][f] == want[f], (n, b, f)
+                assert tr[r][b]["mplus"] == want["mplus_after"], (n, b)
+            assert bool(res["flags"][r] & B.WS_FLAG_OVERFLOW) == g["final"]["overflow"], n
+            for f in ("evictions", "fallback_evictions", "evicted_tokens"):
+                assert res[f][r] == o[f], (n, f)
+        start += job.n
+    print(f"[gpu] pre-launch repair hand traces: {len(names)} instances match", flush=True)
