@@ -53,6 +53,10 @@
  * Errors: functions return a ws_status.  Validation failures return
  * WS_EINVAL before anything is launched; wait_sim_last_error() then holds a
  * message (thread-local, valid until the next call on the same thread).
+ * No C++ exception crosses this interface: a failed host allocation returns
+ * WS_ENOMEM, any other exception WS_EINTERNAL.  A call that fails after
+ * launching work on the library's side streams still orders that work
+ * before the caller's stream (or waits for it) before returning.
  * Conditions met by individual replicas at run time are reported in that
  * replica's flags word, never by aborting the launch.
  */
@@ -74,7 +78,9 @@ typedef enum {
   WS_ENOMEM = -2,      /* host allocation failed                          */
   WS_EDEVICE = -3,     /* HIP runtime error                               */
   WS_EWORKSPACE = -4,  /* workspace or result buffer too small            */
-  WS_EUNSUPPORTED = -5 /* valid model, but outside the library's limits  */
+  WS_EUNSUPPORTED = -5, /* valid model, but outside the library's limits */
+  WS_EINTERNAL = -6     /* unexpected internal failure (a C++ exception
+                           caught at the ABI boundary)                   */
 } ws_status;
 
 typedef enum {

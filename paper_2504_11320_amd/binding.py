@@ -17,6 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libwait_sim.so")
 
 WS_OK, WS_EINVAL, WS_ENOMEM, WS_EDEVICE, WS_EWORKSPACE, WS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+WS_EINTERNAL = -6
 WS_WAIT, WS_NESTED_WAIT, WS_FCFS, WS_WAIT_NOWAIT = 0, 1, 2, 3
 WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW, WS_FLAG_THIN_LIMIT = 1, 2, 4, 8
 WS_ABI_VERSION = 2

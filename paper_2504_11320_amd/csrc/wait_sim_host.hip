@@ -53,9 +53,41 @@ __global__ void __launch_bounds__(256) export_kernel(KArgs A, uint8_t *out) {
 
 thread_local std::string g_err;
 
-int fail(int code, const std::string &msg) {
-  g_err = msg;
+// Record the message of a failure and return its code.  Never throws: if the
+// message cannot be stored the previous one is cleared instead.
+int fail(int code, const char *msg) noexcept {
+  try {
+    g_err = msg;
+  } catch (...) {
+    g_err.clear();
+  }
   return code;
+}
+int fail(int code, const std::string &msg) noexcept { return fail(code, msg.c_str()); }
+
+// A failure of job `idx`; the message is only built on this (failure) path.
+int fail_job(int code, int idx, const char *what) noexcept {
+  try {
+    g_err = "job " + std::to_string(idx) + ": " + what;
+  } catch (...) {
+    g_err.clear();
+  }
+  return code;
+}
+int fail_job(int code, int idx, const std::string &what) noexcept {
+  return fail_job(code, idx, what.c_str());
+}
+
+// Body of an extern "C" entry point: no C++ exception crosses the C ABI.
+template <class F>
+int guarded(F &&body) noexcept {
+  try {
+    return body();
+  } catch (const std::bad_alloc &) {
+    return fail(WS_ENOMEM, "host memory allocation failed");
+  } catch (...) {
+    return fail(WS_EINTERNAL, "internal error (unexpected C++ exception)");
+  }
 }
 
 // Replicas per 64-lane wavefront.  A replica is a serial chain of events, so
@@ -90,12 +122,18 @@ struct JobHost {
 };
 
 struct Layout {
+  Layout() = default;
+  Layout(Layout &&) = default;
+  Layout &operator=(Layout &&) = default;
+  Layout(const Layout &) = delete;
+  Layout &operator=(const Layout &) = delete;
   int64_t R = 0;
   int32_t hist_stride = 1;
   uint64_t off_jobs = 0, off_seed = 0, off_rid = 0, off_job_of = 0,
            off_list = 0, off_tables = 0, off_state = 0, off_hist = 0,
            off_rings = 0, total = 0;
-  std::vector<JobHost> jobs;
+  JobHost *jobs = nullptr;     // [n_jobs]: `own`, or storage of the caller
+  std::vector<JobHost> own;
   int32_t list_count[3] = {0, 0, 0};
   int32_t lanes[3] = {64, 64, 64};  // replicas per wavefront, per launch
   uint64_t list_off[3] = {0, 0, 0};
@@ -109,137 +147,136 @@ int launch_kind(const ws_policy *p) {
 }
 
 int validate_job(const ws_job &jb, int idx, JobHost &H) {
-  const std::string at = "job " + std::to_string(idx) + ": ";
-  if (!jb.cfg || !jb.pol) return fail(WS_EINVAL, at + "cfg and pol must be non-NULL");
-  if (jb.n < 0) return fail(WS_EINVAL, at + "negative replica count");
-  if (jb.n > 0 && !jb.streams) return fail(WS_EINVAL, at + "streams must be non-NULL");
+  if (!jb.cfg || !jb.pol) return fail_job(WS_EINVAL, idx, "cfg and pol must be non-NULL");
+  if (jb.n < 0) return fail_job(WS_EINVAL, idx, "negative replica count");
+  if (jb.n > 0 && !jb.streams) return fail_job(WS_EINVAL, idx, "streams must be non-NULL");
   const ws_config &c = *jb.cfg;
   const ws_policy &p = *jb.pol;
   // WAIT-no-wait runs on the WAIT kernel with a flag
   const int kind = p.kind == WS_WAIT_NOWAIT ? (int)WS_WAIT : (int)p.kind;
   if (c.m < 1 || c.m > WS_MAX_TYPES)
-    return fail(WS_EINVAL, at + "m must be in 1.." + std::to_string(WS_MAX_TYPES));
-  if (!c.prompt_len || !c.lambda) return fail(WS_EINVAL, at + "prompt_len and lambda required");
+    return fail_job(WS_EINVAL, idx, std::string("m must be in 1..") + std::to_string(WS_MAX_TYPES));
+  if (!c.prompt_len || !c.lambda) return fail_job(WS_EINVAL, idx, "prompt_len and lambda required");
   for (int j = 0; j < c.m; ++j) {
-    if (c.prompt_len[j] < 1) return fail(WS_EINVAL, at + "prompt lengths must be >= 1");
+    if (c.prompt_len[j] < 1) return fail_job(WS_EINVAL, idx, "prompt lengths must be >= 1");
     if (!(c.lambda[j] >= 0.0) || !std::isfinite(c.lambda[j]))
-      return fail(WS_EINVAL, at + "rates must be finite and >= 0");
+      return fail_job(WS_EINVAL, idx, "rates must be finite and >= 0");
   }
-  if (!(c.d0 > 0.0) || !std::isfinite(c.d0)) return fail(WS_EINVAL, at + "d0 must be > 0");
-  if (!(c.d1 >= 0.0) || !std::isfinite(c.d1)) return fail(WS_EINVAL, at + "d1 must be >= 0");
-  if (c.C < 1 || c.C > (int64_t(1) << 30)) return fail(WS_EINVAL, at + "C must be in 1..2^30");
+  if (!(c.d0 > 0.0) || !std::isfinite(c.d0)) return fail_job(WS_EINVAL, idx, "d0 must be > 0");
+  if (!(c.d1 >= 0.0) || !std::isfinite(c.d1)) return fail_job(WS_EINVAL, idx, "d1 must be >= 0");
+  if (c.C < 1 || c.C > (int64_t(1) << 30)) return fail_job(WS_EINVAL, idx, "C must be in 1..2^30");
   const bool known = c.out_len != nullptr;
   int64_t maxL = 0;
   if (known) {
     for (int j = 0; j < c.m; ++j) {
-      if (c.out_len[j] < 1) return fail(WS_EINVAL, at + "output lengths must be >= 1");
+      if (c.out_len[j] < 1) return fail_job(WS_EINVAL, idx, "output lengths must be >= 1");
       maxL = std::max<int64_t>(maxL, c.out_len[j]);
     }
   } else {
-    if (c.out_cap < 1) return fail(WS_EINVAL, at + "out_cap must be >= 1 without out_len");
+    if (c.out_cap < 1) return fail_job(WS_EINVAL, idx, "out_cap must be >= 1 without out_len");
     maxL = c.out_cap;
     if (c.n_trace == 0) {
-      if (c.out_cap > 1 && !c.out_cdf_u32) return fail(WS_EINVAL, at + "out_cdf_u32 required");
+      if (c.out_cap > 1 && !c.out_cdf_u32) return fail_job(WS_EINVAL, idx, "out_cdf_u32 required");
       for (int j = 0; j < c.m; ++j)
         for (int s = 1; s + 1 < c.out_cap; ++s)
           if (c.out_cdf_u32[(size_t)j * (c.out_cap - 1) + s] <
               c.out_cdf_u32[(size_t)j * (c.out_cap - 1) + s - 1])
-            return fail(WS_EINVAL, at + "CDF table rows must be nondecreasing");
+            return fail_job(WS_EINVAL, idx, "CDF table rows must be nondecreasing");
     }
   }
   if (c.n_hist < 0 || c.n_hist > WS_MAX_HIST_EDGES)
-    return fail(WS_EINVAL, at + "n_hist out of range");
+    return fail_job(WS_EINVAL, idx, "n_hist out of range");
   if (c.n_hist > 0) {
-    if (!c.hist_edges) return fail(WS_EINVAL, at + "hist_edges required");
+    if (!c.hist_edges) return fail_job(WS_EINVAL, idx, "hist_edges required");
     for (int b = 0; b < c.n_hist; ++b) {
-      if (!std::isfinite(c.hist_edges[b])) return fail(WS_EINVAL, at + "edges must be finite");
+      if (!std::isfinite(c.hist_edges[b])) return fail_job(WS_EINVAL, idx, "edges must be finite");
       if (b > 0 && !(c.hist_edges[b] > c.hist_edges[b - 1]))
-        return fail(WS_EINVAL, at + "edges must be strictly increasing");
+        return fail_job(WS_EINVAL, idx, "edges must be strictly increasing");
     }
   }
   if (c.record_capacity < 16 || c.record_capacity > (1 << 26) ||
       (c.record_capacity & (c.record_capacity - 1)) != 0)
-    return fail(WS_EINVAL, at + "record_capacity must be a power of two in 16..2^26");
-  if (c.n_trace < 0) return fail(WS_EINVAL, at + "n_trace must be >= 0");
+    return fail_job(WS_EINVAL, idx, "record_capacity must be a power of two in 16..2^26");
+  if (c.n_trace < 0) return fail_job(WS_EINVAL, idx, "n_trace must be >= 0");
   if (c.n_trace > 0) {
-    if (!c.trace_time || !c.trace_type) return fail(WS_EINVAL, at + "trace arrays required");
-    if (!known && !c.trace_out_len) return fail(WS_EINVAL, at + "trace_out_len required");
+    if (!c.trace_time || !c.trace_type) return fail_job(WS_EINVAL, idx, "trace arrays required");
+    if (!known && !c.trace_out_len) return fail_job(WS_EINVAL, idx, "trace_out_len required");
     for (int64_t i = 0; i < c.n_trace; ++i) {
       if (!(c.trace_time[i] >= 0.0) || !std::isfinite(c.trace_time[i]))
-        return fail(WS_EINVAL, at + "trace times must be finite and >= 0");
+        return fail_job(WS_EINVAL, idx, "trace times must be finite and >= 0");
       if (i > 0 && c.trace_time[i] < c.trace_time[i - 1])
-        return fail(WS_EINVAL, at + "trace times must be nondecreasing");
+        return fail_job(WS_EINVAL, idx, "trace times must be nondecreasing");
       if (c.trace_type[i] < 0 || c.trace_type[i] >= c.m)
-        return fail(WS_EINVAL, at + "trace type out of range");
+        return fail_job(WS_EINVAL, idx, "trace type out of range");
       if (!known && (c.trace_out_len[i] < 1 || c.trace_out_len[i] > c.out_cap))
-        return fail(WS_EINVAL, at + "trace output length out of range");
+        return fail_job(WS_EINVAL, idx, "trace output length out of range");
     }
   }
   double fmax[WS_MAX_TYPES] = {};
   if (c.n_rate_pts != 0) {
     if (c.n_rate_pts < 0 || c.n_rate_pts > WS_MAX_RATE_PTS)
-      return fail(WS_EINVAL, at + "n_rate_pts must be in 0.." + std::to_string(WS_MAX_RATE_PTS));
-    if (c.n_trace > 0) return fail(WS_EINVAL, at + "a rate profile and a trace are exclusive");
-    if (!c.rate_t || !c.rate_f) return fail(WS_EINVAL, at + "rate_t and rate_f required");
+      return fail_job(WS_EINVAL, idx, std::string("n_rate_pts must be in 0..") + std::to_string(WS_MAX_RATE_PTS));
+    if (c.n_trace > 0) return fail_job(WS_EINVAL, idx, "a rate profile and a trace are exclusive");
+    if (!c.rate_t || !c.rate_f) return fail_job(WS_EINVAL, idx, "rate_t and rate_f required");
     const int P = c.n_rate_pts;
     for (int i = 0; i < P; ++i) {
-      if (!std::isfinite(c.rate_t[i])) return fail(WS_EINVAL, at + "rate_t must be finite");
+      if (!std::isfinite(c.rate_t[i])) return fail_job(WS_EINVAL, idx, "rate_t must be finite");
       if (i > 0 && !(c.rate_t[i] > c.rate_t[i - 1]))
-        return fail(WS_EINVAL, at + "rate_t must be strictly increasing");
+        return fail_job(WS_EINVAL, idx, "rate_t must be strictly increasing");
     }
     for (int j = 0; j < c.m; ++j) {
       for (int i = 0; i < P; ++i) {
         const double f = c.rate_f[(size_t)j * P + i];
         if (!(f >= 0.0) || !std::isfinite(f))
-          return fail(WS_EINVAL, at + "rate_f must be finite and >= 0");
+          return fail_job(WS_EINVAL, idx, "rate_f must be finite and >= 0");
         fmax[j] = std::max(fmax[j], f);
       }
       if (!std::isfinite(c.lambda[j] * fmax[j]))
-        return fail(WS_EINVAL, at + "lambda_j * max f_j must be finite");
+        return fail_job(WS_EINVAL, idx, "lambda_j * max f_j must be finite");
     }
   }
   int64_t reserve_tok = 0;
   if (kind != WS_FCFS && p.fcfs_chunk != 0)
-    return fail(WS_EINVAL, at + "fcfs_chunk applies to FCFS only");
+    return fail_job(WS_EINVAL, idx, "fcfs_chunk applies to FCFS only");
   if (kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
-    return fail(WS_EUNSUPPORTED, at + "WAIT and FCFS take at most " +
-                                     std::to_string(WS_MAX_TYPES_KNOWN) + " request types");
+    return fail_job(WS_EUNSUPPORTED, idx, std::string("WAIT and FCFS take at most ") +
+                                              std::to_string(WS_MAX_TYPES_KNOWN) + " request types");
   if (kind == WS_WAIT) {
-    if (!known) return fail(WS_EINVAL, at + "WAIT needs known output lengths");
-    if (!p.n) return fail(WS_EINVAL, at + "thresholds required");
+    if (!known) return fail_job(WS_EINVAL, idx, "WAIT needs known output lengths");
+    if (!p.n) return fail_job(WS_EINVAL, idx, "thresholds required");
     int64_t fresh = 0;  // memory one batch can admit
     for (int j = 0; j < c.m; ++j) {
-      if (p.n[j] < 1) return fail(WS_EINVAL, at + "thresholds must be >= 1");
+      if (p.n[j] < 1) return fail_job(WS_EINVAL, idx, "thresholds must be >= 1");
       fresh += (int64_t)p.n[j] * (c.prompt_len[j] + 1);
     }
     if (fresh >= (int64_t(1) << 29))
-      return fail(WS_EUNSUPPORTED, at + "sum_j n_j (l_j + 1) must stay below 2^29");
+      return fail_job(WS_EUNSUPPORTED, idx, "sum_j n_j (l_j + 1) must stay below 2^29");
   } else if (kind == WS_FCFS) {
     if (!(p.fcfs_reserve >= 0.0 && p.fcfs_reserve < 1.0))
-      return fail(WS_EINVAL, at + "fcfs_reserve must be in [0,1)");
+      return fail_job(WS_EINVAL, idx, "fcfs_reserve must be in [0,1)");
     reserve_tok = (int64_t)std::ceil(p.fcfs_reserve * (double)c.C);
-    if (p.fcfs_chunk < 0) return fail(WS_EINVAL, at + "fcfs_chunk must be >= 0");
+    if (p.fcfs_chunk < 0) return fail_job(WS_EINVAL, idx, "fcfs_chunk must be >= 0");
     for (int j = 0; j < c.m; ++j)
       if (c.prompt_len[j] > c.C - reserve_tok)
-        return fail(WS_EINVAL, at + "a prompt does not fit below the FCFS reserve");
-    if (!known) return fail(WS_EUNSUPPORTED, at + "FCFS with unknown lengths is not supported");
+        return fail_job(WS_EINVAL, idx, "a prompt does not fit below the FCFS reserve");
+    if (!known) return fail_job(WS_EUNSUPPORTED, idx, "FCFS with unknown lengths is not supported");
   } else if (kind == WS_NESTED_WAIT) {
-    if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail(WS_EINVAL, at + "L out of range");
-    if (!p.n || !p.seg_end) return fail(WS_EINVAL, at + "thresholds and seg_end required");
+    if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail_job(WS_EINVAL, idx, "L out of range");
+    if (!p.n || !p.seg_end) return fail_job(WS_EINVAL, idx, "thresholds and seg_end required");
     for (int k = 0; k < p.L; ++k) {
-      if (p.n[k] < 1) return fail(WS_EINVAL, at + "thresholds must be >= 1");
+      if (p.n[k] < 1) return fail_job(WS_EINVAL, idx, "thresholds must be >= 1");
       if (p.seg_end[k] < 1 || (k > 0 && p.seg_end[k] <= p.seg_end[k - 1]))
-        return fail(WS_EINVAL, at + "seg_end must be strictly increasing and >= 1");
+        return fail_job(WS_EINVAL, idx, "seg_end must be strictly increasing and >= 1");
     }
     if (p.seg_end[p.L - 1] != maxL)
-      return fail(WS_EINVAL, at + "last segment must end at the largest output length");
+      return fail_job(WS_EINVAL, idx, "last segment must end at the largest output length");
   } else {
-    return fail(WS_EINVAL, at + "unknown policy kind");
+    return fail_job(WS_EINVAL, idx, "unknown policy kind");
   }
   for (int j = 0; j < c.m; ++j) {
     const int64_t Lj = known ? c.out_len[j] : c.out_cap;
     if (c.prompt_len[j] + Lj > c.C)
-      return fail(WS_EINVAL, at + "a single prompt does not fit in C (atomic feasibility)");
+      return fail_job(WS_EINVAL, idx, "a single prompt does not fit in C (atomic feasibility)");
   }
 
   JobDev &d = H.d;
@@ -327,14 +364,21 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   }
   d.ring_stride = off;
   // ring offsets inside a replica block are kept as 32-bit values on the device
-  if (off >= (1ull << 32)) return fail(WS_EUNSUPPORTED, at + "record rings exceed 4 GiB per replica");
+  if (off >= (1ull << 32)) return fail_job(WS_EUNSUPPORTED, idx, "record rings exceed 4 GiB per replica");
   return WS_OK;
 }
 
-int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo) {
+// Validate the jobs and lay out the workspace.  `storage`: room for n_jobs
+// job descriptors supplied by the caller (no host allocation), or null.
+int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage = nullptr) {
   if (n_jobs < 1 || !jobs) return fail(WS_EINVAL, "need at least one job");
   Lo = Layout();
-  Lo.jobs.resize(n_jobs);
+  if (storage) {
+    Lo.jobs = storage;
+  } else {
+    Lo.own.resize(n_jobs);
+    Lo.jobs = Lo.own.data();
+  }
   int64_t R = 0;
   int32_t hmax = 0;
   for (int i = 0; i < n_jobs; ++i) {
@@ -490,113 +534,98 @@ KArgs base_args(const Layout &Lo, void *d_ws) {
   return A;
 }
 
-}  // namespace
-
-// ---------------------------------------------------------------- C ABI --
-
-extern "C" {
-
-const char *wait_sim_last_error(void) { return g_err.c_str(); }
-
-int wait_sim_abi_version(void) { return WS_ABI_VERSION; }
-
-int wait_sim_workspace_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes) {
-  g_err.clear();
-  if (!bytes) return fail(WS_EINVAL, "bytes must be non-NULL");
-  Layout Lo;
-  int rc = make_layout(jobs, n_jobs, Lo);
-  if (rc != WS_OK) return rc;
-  *bytes = (size_t)Lo.total;
-  return WS_OK;
-}
-
-int wait_sim_results_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes,
-                           int32_t *hist_stride) {
-  g_err.clear();
-  if (!bytes) return fail(WS_EINVAL, "bytes must be non-NULL");
-  Layout Lo;
-  int rc = make_layout(jobs, n_jobs, Lo);
-  if (rc != WS_OK) return rc;
-  *bytes = (size_t)results_size(Lo);
-  if (hist_stride) *hist_stride = Lo.hist_stride;
-  return WS_OK;
-}
-
-int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
-                     size_t ws_bytes, void *hip_stream) {
-  g_err.clear();
-  Layout Lo;
-  int rc = make_layout(jobs, n_jobs, Lo);
-  if (rc != WS_OK) return rc;
-  if (!d_workspace) return fail(WS_EINVAL, "workspace must be non-NULL");
-  if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
-  hipStream_t s = (hipStream_t)hip_stream;
-  // host image of everything up to the state region
-  std::vector<uint8_t> img(Lo.off_state, 0);
+// Write the table image (everything in front of the state region: job
+// descriptors, streams, replica lists and per-job tables) into `img`
+// (Lo.off_state bytes), copy it to the workspace on stream s and wait for the
+// copy.  Allocates nothing.
+int prepare_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *img,
+                  void *d_workspace, hipStream_t s) {
+  std::memset(img, 0, Lo.off_state);
   for (int i = 0; i < n_jobs; ++i)
-    std::memcpy(img.data() + Lo.off_jobs + sizeof(JobDev) * i, &Lo.jobs[i].d, sizeof(JobDev));
+    std::memcpy(img + Lo.off_jobs + sizeof(JobDev) * i, &Lo.jobs[i].d, sizeof(JobDev));
+  // replica lists per launch kind: each job starts a new wavefront, whose
+  // lanes beyond the launch's width are padding (-1)
+  int64_t pos[3] = {0, 0, 0};
+  auto put = [&](int pk, int32_t v) {
+    std::memcpy(img + Lo.list_off[pk] + 4 * pos[pk], &v, 4);
+    pos[pk]++;
+  };
   int64_t r = 0;
-  std::vector<int32_t> lists[3];
   for (int i = 0; i < n_jobs; ++i) {
     const ws_job &jb = jobs[i];
-    std::vector<int32_t> &list = lists[launch_kind(jb.pol)];
+    const int pk = launch_kind(jb.pol);
     for (int x = 0; x < jb.n; ++x, ++r) {
-      std::memcpy(img.data() + Lo.off_seed + 8 * r, &jb.streams[x].seed, 8);
-      std::memcpy(img.data() + Lo.off_rid + 4 * r, &jb.streams[x].replica_id, 4);
+      std::memcpy(img + Lo.off_seed + 8 * r, &jb.streams[x].seed, 8);
+      std::memcpy(img + Lo.off_rid + 4 * r, &jb.streams[x].replica_id, 4);
       const uint32_t ji = (uint32_t)i;
-      std::memcpy(img.data() + Lo.off_job_of + 4 * r, &ji, 4);
-      list.push_back((int32_t)r);
-      if (list.size() % 64 == (size_t)Lo.lanes[launch_kind(jb.pol)])
-        while (list.size() % 64 != 0) list.push_back(-1);
+      std::memcpy(img + Lo.off_job_of + 4 * r, &ji, 4);
+      put(pk, (int32_t)r);
+      if (pos[pk] % 64 == Lo.lanes[pk])
+        while (pos[pk] % 64 != 0) put(pk, -1);
     }
-    while (list.size() % 64 != 0) list.push_back(-1);
+    while (pos[pk] % 64 != 0) put(pk, -1);
     const ws_config &c = *jb.cfg;
     const JobDev &d = Lo.jobs[i].d;
-    if (c.n_hist > 0) std::memcpy(img.data() + d.off_edges, c.hist_edges, 8ull * c.n_hist);
+    if (c.n_hist > 0) std::memcpy(img + d.off_edges, c.hist_edges, 8ull * c.n_hist);
     if (Lo.jobs[i].cdf_bytes)
-      std::memcpy(img.data() + d.off_cdf, c.out_cdf_u32, 4ull * c.m * (c.out_cap - 1));
+      std::memcpy(img + d.off_cdf, c.out_cdf_u32, 4ull * c.m * (c.out_cap - 1));
     if (c.n_trace > 0) {
-      std::memcpy(img.data() + d.off_tr_time, c.trace_time, 8ull * c.n_trace);
-      std::memcpy(img.data() + d.off_tr_type, c.trace_type, 4ull * c.n_trace);
-      if (c.trace_out_len)
-        std::memcpy(img.data() + d.off_tr_len, c.trace_out_len, 4ull * c.n_trace);
+      std::memcpy(img + d.off_tr_time, c.trace_time, 8ull * c.n_trace);
+      std::memcpy(img + d.off_tr_type, c.trace_type, 4ull * c.n_trace);
+      if (c.trace_out_len) std::memcpy(img + d.off_tr_len, c.trace_out_len, 4ull * c.n_trace);
     }
     if (c.n_rate_pts > 0) {  // rate_t [P], then rate_f [m][P]
-      std::memcpy(img.data() + d.off_rate, c.rate_t, 8ull * c.n_rate_pts);
-      std::memcpy(img.data() + d.off_rate + 8ull * c.n_rate_pts, c.rate_f,
-                  8ull * c.n_rate_pts * c.m);
+      std::memcpy(img + d.off_rate, c.rate_t, 8ull * c.n_rate_pts);
+      std::memcpy(img + d.off_rate + 8ull * c.n_rate_pts, c.rate_f, 8ull * c.n_rate_pts * c.m);
     }
   }
-  for (int pk = 0; pk < 3; ++pk)
-    if (!lists[pk].empty())
-      std::memcpy(img.data() + Lo.list_off[pk], lists[pk].data(), 4 * lists[pk].size());
-  HIP_TRY(hipMemcpyAsync(d_workspace, img.data(), img.size(), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemcpyAsync(d_workspace, img, Lo.off_state, hipMemcpyHostToDevice, s));
   HIP_TRY(hipStreamSynchronize(s));
   return WS_OK;
 }
 
-int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
-                     int32_t resume, void *d_workspace, size_t ws_bytes,
-                     void *d_results, size_t results_bytes, void *hip_stream) {
-  return wait_sim_advance_traced(jobs, n_jobs, horizon, resume, d_workspace, ws_bytes,
-                                 d_results, results_bytes, nullptr, 0, hip_stream);
-}
+// Orders the launches a call puts on the library's side streams before the
+// caller's stream: every side stream that received work is joined back into
+// it (an event recorded there, waited for by the caller's stream), also when
+// the call fails part-way; if even that fails the side stream is
+// synchronised, so no launch of the call outlives its return unordered.
+struct SideJoin {
+  hipStream_t main = nullptr;
+  hipEvent_t fork = nullptr;
+  hipStream_t pending[2] = {nullptr, nullptr};
+  int n_pending = 0;
 
-int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
-                            int32_t resume, void *d_workspace, size_t ws_bytes,
-                            void *d_results, size_t results_bytes, void *d_btrace,
-                            int64_t btrace_cap, void *hip_stream) {
-  g_err.clear();
-  Layout Lo;
-  int rc = make_layout(jobs, n_jobs, Lo);
-  if (rc != WS_OK) return rc;
-  if (horizon < 0) return fail(WS_EINVAL, "horizon must be >= 0");
-  if (!d_workspace || !d_results) return fail(WS_EINVAL, "device buffers must be non-NULL");
-  if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
-  if (results_bytes < results_size(Lo)) return fail(WS_EWORKSPACE, "result buffer too small");
-  if (btrace_cap < 0) return fail(WS_EINVAL, "btrace_cap must be >= 0");
-  if (btrace_cap > 0 && !d_btrace) return fail(WS_EINVAL, "d_btrace must be non-NULL");
-  hipStream_t s = (hipStream_t)hip_stream;
+  static hipError_t join_one(hipStream_t main, hipStream_t side) {
+    hipEvent_t ev = nullptr;
+    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(ev, side);
+    if (e == hipSuccess) e = hipStreamWaitEvent(main, ev, 0);
+    if (ev != nullptr) (void)hipEventDestroy(ev);  // released once it has completed
+    if (e != hipSuccess) (void)hipStreamSynchronize(side);
+    return e;
+  }
+  // Join every pending side stream; returns the first error.
+  hipError_t join_all() {
+    hipError_t first = hipSuccess;
+    for (int i = 0; i < n_pending; ++i) {
+      const hipError_t e = join_one(main, pending[i]);
+      if (first == hipSuccess) first = e;
+    }
+    n_pending = 0;
+    return first;
+  }
+  ~SideJoin() {
+    (void)join_all();
+    if (fork != nullptr) (void)hipEventDestroy(fork);
+  }
+};
+
+// Launch the simulation kernels of every policy kind, then the export of the
+// results.  Allocates no device memory; a call with one policy kind creates
+// no stream or event.
+int advance_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, int64_t horizon,
+                 int32_t resume, void *d_workspace, void *d_results, void *d_btrace,
+                 int64_t btrace_cap, hipStream_t s) {
   KArgs A = base_args(Lo, d_workspace);
   A.horizon = horizon;
   A.resume = resume ? 1 : 0;
@@ -607,11 +636,12 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
   int kinds = 0;
   for (int pk = 0; pk < 3; ++pk) kinds += Lo.list_count[pk] > 0 ? 1 : 0;
   hipStream_t side[2] = {nullptr, nullptr};
-  hipEvent_t fork = nullptr;
+  SideJoin sj;
+  sj.main = s;
   if (kinds > 1) {
     HIP_TRY(side_streams(side));
-    HIP_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
-    HIP_TRY(hipEventRecord(fork, s));
+    HIP_TRY(hipEventCreateWithFlags(&sj.fork, hipEventDisableTiming));
+    HIP_TRY(hipEventRecord(sj.fork, s));
   }
   int launched = 0;
   for (int pk = 0; pk < 3; ++pk) {
@@ -619,7 +649,7 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
     hipStream_t ls = s;
     if (launched > 0) {
       ls = side[launched - 1];
-      HIP_TRY(hipStreamWaitEvent(ls, fork, 0));
+      HIP_TRY(hipStreamWaitEvent(ls, sj.fork, 0));
     }
     KArgs B = A;
     B.off_list = Lo.list_off[pk];
@@ -635,6 +665,7 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
         for (int j = 0; j < jobs[i].cfg->m; ++j)
           if (jobs[i].pol->n[j] != 1) B.unit_n = 0;
     }
+    if (launched > 0) sj.pending[sj.n_pending++] = ls;  // joined even if the launch fails
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)
       e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, ls);
@@ -642,16 +673,9 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
       e = pk == WS_WAIT ? launch_known_wait(Lo.max_m[pk], B, ls)
                         : launch_known_fcfs(Lo.max_m[pk], B, ls);
     if (e != hipSuccess) return fail(WS_EDEVICE, std::string("launch: ") + hipGetErrorString(e));
-    if (launched > 0) {  // join: the caller's stream waits for this kind
-      hipEvent_t join = nullptr;
-      HIP_TRY(hipEventCreateWithFlags(&join, hipEventDisableTiming));
-      HIP_TRY(hipEventRecord(join, ls));
-      HIP_TRY(hipStreamWaitEvent(s, join, 0));
-      HIP_TRY(hipEventDestroy(join));  // released once it has completed
-    }
     launched++;
   }
-  if (fork != nullptr) HIP_TRY(hipEventDestroy(fork));
+  HIP_TRY(sj.join_all());  // the caller's stream waits for every kind
   const int tb = 256;
   hipLaunchKernelGGL(export_kernel, dim3((unsigned)((Lo.R + tb - 1) / tb)), dim3(tb), 0, s, A,
                      (uint8_t *)d_results);
@@ -661,6 +685,91 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                          4ull * (uint64_t)Lo.hist_stride * (uint64_t)Lo.R,
                          hipMemcpyDeviceToDevice, s));
   return WS_OK;
+}
+
+// Checks shared by the entry points that advance a workspace.
+int check_advance(const Layout &Lo, int64_t horizon, const void *d_workspace, size_t ws_bytes,
+                  const void *d_results, size_t results_bytes) {
+  if (horizon < 0) return fail(WS_EINVAL, "horizon must be >= 0");
+  if (!d_workspace || !d_results) return fail(WS_EINVAL, "device buffers must be non-NULL");
+  if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
+  if (results_bytes < results_size(Lo)) return fail(WS_EWORKSPACE, "result buffer too small");
+  return WS_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- C ABI --
+
+extern "C" {
+
+const char *wait_sim_last_error(void) { return g_err.c_str(); }
+
+int wait_sim_abi_version(void) { return WS_ABI_VERSION; }
+
+int wait_sim_workspace_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    if (!bytes) return fail(WS_EINVAL, "bytes must be non-NULL");
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    *bytes = (size_t)Lo.total;
+    return WS_OK;
+  });
+}
+
+int wait_sim_results_bytes(const ws_job *jobs, int32_t n_jobs, size_t *bytes,
+                           int32_t *hist_stride) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    if (!bytes) return fail(WS_EINVAL, "bytes must be non-NULL");
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    *bytes = (size_t)results_size(Lo);
+    if (hist_stride) *hist_stride = Lo.hist_stride;
+    return WS_OK;
+  });
+}
+
+int wait_sim_prepare(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
+                     size_t ws_bytes, void *hip_stream) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    if (!d_workspace) return fail(WS_EINVAL, "workspace must be non-NULL");
+    if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
+    std::vector<uint8_t> img(Lo.off_state);
+    return prepare_image(jobs, n_jobs, Lo, img.data(), d_workspace, (hipStream_t)hip_stream);
+  });
+}
+
+int wait_sim_advance(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                     int32_t resume, void *d_workspace, size_t ws_bytes,
+                     void *d_results, size_t results_bytes, void *hip_stream) {
+  return wait_sim_advance_traced(jobs, n_jobs, horizon, resume, d_workspace, ws_bytes,
+                                 d_results, results_bytes, nullptr, 0, hip_stream);
+}
+
+int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                            int32_t resume, void *d_workspace, size_t ws_bytes,
+                            void *d_results, size_t results_bytes, void *d_btrace,
+                            int64_t btrace_cap, void *hip_stream) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    rc = check_advance(Lo, horizon, d_workspace, ws_bytes, d_results, results_bytes);
+    if (rc != WS_OK) return rc;
+    if (btrace_cap < 0) return fail(WS_EINVAL, "btrace_cap must be >= 0");
+    if (btrace_cap > 0 && !d_btrace) return fail(WS_EINVAL, "d_btrace must be non-NULL");
+    return advance_impl(jobs, n_jobs, Lo, horizon, resume, d_workspace, d_results, d_btrace,
+                        btrace_cap, (hipStream_t)hip_stream);
+  });
 }
 
 int wait_sim_run_batch(const ws_job *jobs, int32_t n_jobs, int64_t horizon,

@@ -136,3 +136,21 @@ def test_wait_admission_bound():
     from paper_2504_11320_amd import binding as B
     assert _err(_job(n=[1 << 22, 1, 1])).code == B.WS_EUNSUPPORTED   # 2^22 x 129
     assert B.workspace_bytes(B.JobArray(_job(n=[1000, 1, 1]))) > 0
+
+
+def test_host_allocation_failure_is_an_error_code():
+    """No C++ exception crosses the C ABI: a job count whose host-side
+    descriptors cannot be allocated returns WS_ENOMEM."""
+    from paper_2504_11320_amd import binding as B
+    try:
+        overcommit = open("/proc/sys/vm/overcommit_memory").read().strip()
+    except OSError:
+        overcommit = "?"
+    if overcommit != "0" and overcommit != "2":
+        pytest.skip("the kernel may grant any allocation (overcommit_memory != 0, 2)")
+    L = B.lib()
+    ja = B.JobArray(_job())
+    size = ctypes.c_size_t()
+    rc = L.wait_sim_workspace_bytes(ja.ptr, (1 << 31) - 1, ctypes.byref(size))
+    assert rc == B.WS_ENOMEM
+    assert b"allocation" in L.wait_sim_last_error()
