@@ -107,6 +107,9 @@ typedef enum {
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255
 #define WS_MAX_RATE_PTS 32
+/* Workspace of wait_sim_run_static: a device array of this many bytes that
+   every GPU the library runs on holds until the process ends. */
+#define WS_STATIC_WORKSPACE_BYTES (64u << 20)
 
 /* The model (Section 2). */
 typedef struct {
@@ -264,6 +267,26 @@ int wait_sim_run(const ws_config *cfg, const ws_policy *pol,
 int wait_sim_run_batch(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                        void *d_workspace, size_t ws_bytes, void *d_results,
                        size_t results_bytes, void *hip_stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * as wait_sim_run, with the workspace taken from a static device array of
+ * WS_STATIC_WORKSPACE_BYTES (64 MiB) instead of the caller.  The caller
+ * still passes the host structs and the device result buffer (sized by
+ * wait_sim_results_bytes).  The call allocates no device memory and creates
+ * no stream or event; it blocks the host until the job tables have been
+ * copied (as wait_sim_prepare does), then launches asynchronously on
+ * hip_stream.  Jobs whose workspace (wait_sim_workspace_bytes) exceeds
+ * WS_STATIC_WORKSPACE_BYTES return WS_EWORKSPACE.  Every call on one GPU
+ * uses that GPU's one array: calls that overlap on the same GPU (other host
+ * threads, or a new call issued before an earlier call's kernels have
+ * finished on another stream) race and give undefined results; serialise
+ * them, e.g. on one stream.  The array is not cleared between calls (each
+ * call rebuilds what it reads). */
+int wait_sim_run_static(const ws_config *cfg, const ws_policy *pol,
+                        const ws_stream *streams, int32_t n_replicas,
+                        int64_t horizon, void *d_results, size_t results_bytes,
+                        void *hip_stream);
 
 /* Message of the last failure on this thread ("" if none). */
 const char *wait_sim_last_error(void);

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(PKG, "libwait_sim.so")
 
 WS_OK, WS_EINVAL, WS_ENOMEM, WS_EDEVICE, WS_EWORKSPACE, WS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 WS_EINTERNAL = -6
+WS_STATIC_WORKSPACE_BYTES = 64 << 20
 WS_WAIT, WS_NESTED_WAIT, WS_FCFS, WS_WAIT_NOWAIT = 0, 1, 2, 3
 WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW, WS_FLAG_THIN_LIMIT = 1, 2, 4, 8
 WS_ABI_VERSION = 2
@@ -101,6 +102,9 @@ def lib():
         L.wait_sim_advance_traced.argtypes = [jp, C.c_int32, C.c_int64, C.c_int32,
                                               C.c_void_p, C.c_size_t, C.c_void_p,
                                               C.c_size_t, C.c_void_p, C.c_int64, C.c_void_p]
+        L.wait_sim_run_static.argtypes = [C.POINTER(WsConfig), C.POINTER(WsPolicy), C.c_void_p,
+                                          C.c_int32, C.c_int64, C.c_void_p, C.c_size_t,
+                                          C.c_void_p]
         L.wait_sim_last_error.restype = C.c_char_p
         L.wait_sim_abi_version.restype = C.c_int
         if L.wait_sim_abi_version() != WS_ABI_VERSION:
@@ -293,6 +297,25 @@ def run_batch(jobs: Sequence, horizon: int, device: str = "cuda:0") -> dict:
     sim = Simulation(jobs, device)
     sim.prepare()
     sim.advance(horizon, resume=False)
+    return sim.results()
+
+
+def run_static(job, horizon: int, device: str = "cuda:0") -> dict:
+    """One job through wait_sim_run_static (the library's static workspace,
+    no device allocation inside the call); the result buffer is allocated
+    here, before the call."""
+    import torch
+    ja = JobArray([job])
+    nbytes, _ = results_bytes(ja)
+    dev = torch.device(device)
+    res = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    sim = Simulation.__new__(Simulation)
+    sim.torch, sim.device, sim.ja, sim.res, sim.R = torch, dev, ja, res, ja.replicas
+    sim.res_bytes, sim.hist_stride = results_bytes(ja)
+    with torch.cuda.device(dev):
+        _check(lib().wait_sim_run_static(ja.arr[0].cfg, ja.arr[0].pol, ja.arr[0].streams,
+                                         ja.arr[0].n, int(horizon), res.data_ptr(), nbytes,
+                                         _stream_handle(torch, dev)))
     return sim.results()
 
 

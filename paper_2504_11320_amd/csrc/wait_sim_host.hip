@@ -697,6 +697,40 @@ int check_advance(const Layout &Lo, int64_t horizon, const void *d_workspace, si
   return WS_OK;
 }
 
+// ----------------------------------------------- workspace of run_static --
+
+// The workspace of wait_sim_run_static.  Every device the library runs on
+// holds its own copy until the process ends.  In host code this name is only
+// a stand-in for the symbol: its device address comes from
+// hipGetSymbolAddress, once per device (static_workspace()).
+__device__ __align__(256) uint8_t scratch[WS_STATIC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device, looked up on the first
+// call there.
+int static_workspace(void **out) {
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(WS_EDEVICE, "device index out of range");
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void *p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr) return fail(WS_EDEVICE, "no device address for the static workspace");
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return WS_OK;
+}
+
+// Host staging of the table image for wait_sim_run_static (its image is at
+// most the static workspace's size); used under static_mu.
+std::mutex static_mu;
+uint8_t static_img[WS_STATIC_WORKSPACE_BYTES];
+
 }  // namespace
 
 // ---------------------------------------------------------------- C ABI --
@@ -791,6 +825,37 @@ int wait_sim_run(const ws_config *cfg, const ws_policy *pol, const ws_stream *st
   jb.n = n_replicas;
   return wait_sim_run_batch(&jb, 1, horizon, d_workspace, ws_bytes, d_results, results_bytes,
                             hip_stream);
+}
+
+int wait_sim_run_static(const ws_config *cfg, const ws_policy *pol, const ws_stream *streams,
+                        int32_t n_replicas, int64_t horizon, void *d_results,
+                        size_t results_bytes, void *hip_stream) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    ws_job jb;
+    jb.cfg = cfg;
+    jb.pol = pol;
+    jb.streams = streams;
+    jb.n = n_replicas;
+    JobHost job;  // the layout's descriptor storage: no host allocation
+    Layout Lo;
+    int rc = make_layout(&jb, 1, Lo, &job);
+    if (rc != WS_OK) return rc;
+    if (Lo.total > WS_STATIC_WORKSPACE_BYTES)
+      return fail(WS_EWORKSPACE,
+                  "wait_sim_run_static: these replicas need more workspace than the "
+                  "static workspace of WS_STATIC_WORKSPACE_BYTES holds; use wait_sim_run");
+    void *ws = nullptr;
+    rc = static_workspace(&ws);
+    if (rc != WS_OK) return rc;
+    rc = check_advance(Lo, horizon, ws, WS_STATIC_WORKSPACE_BYTES, d_results, results_bytes);
+    if (rc != WS_OK) return rc;
+    hipStream_t s = (hipStream_t)hip_stream;
+    std::lock_guard<std::mutex> lock(static_mu);
+    rc = prepare_image(&jb, 1, Lo, static_img, ws, s);
+    if (rc != WS_OK) return rc;
+    return advance_impl(&jb, 1, Lo, horizon, 0, ws, d_results, nullptr, 0, s);
+  });
 }
 
 }  // extern "C"

@@ -138,6 +138,26 @@ def test_wait_admission_bound():
     assert B.workspace_bytes(B.JobArray(_job(n=[1000, 1, 1]))) > 0
 
 
+def test_static_entry_validates_on_the_host():
+    """wait_sim_run_static checks the model and the size of its static
+    workspace before touching the device: an invalid job gives WS_EINVAL, a
+    job whose workspace exceeds WS_STATIC_WORKSPACE_BYTES gives
+    WS_EWORKSPACE with a message naming the static workspace."""
+    from paper_2504_11320_amd import binding as B
+    L = B.lib()
+
+    def call(jobs):
+        ja = B.JobArray(jobs)
+        a = ja.arr[0]
+        return L.wait_sim_run_static(a.cfg, a.pol, a.streams, a.n, 10, None, 0, None)
+
+    assert call(_job(d0=0.0)) == B.WS_EINVAL
+    big = W.config2(replicas=1024, rate_index=[3])
+    assert B.workspace_bytes(B.JobArray(big)) > B.WS_STATIC_WORKSPACE_BYTES
+    assert call(big) == B.WS_EWORKSPACE
+    assert b"static workspace" in L.wait_sim_last_error()
+
+
 def test_host_allocation_failure_is_an_error_code():
     """No C++ exception crosses the C ABI: a job count whose host-side
     descriptors cannot be allocated returns WS_ENOMEM."""
