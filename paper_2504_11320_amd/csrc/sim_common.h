@@ -499,6 +499,13 @@ __device__ __forceinline__ void place_if(T (&a)[MT], int j, bool c, T v) {
   for (int i = 0; i < MT; ++i) a[i] = opaque((c && i == j) ? v : a[i]);
 }
 
+// Lanes per replica of the Nested WAIT kernel: the smallest of 4, 8, 16 that
+// covers the types and the segments (one type and one segment per lane).
+__host__ __device__ constexpr int nested_group_width(int max_m, int max_seg) {
+  return (max_m > max_seg ? max_m : max_seg) <= 4 ? 4
+         : (max_m > max_seg ? max_m : max_seg) <= 8 ? 8 : 16;
+}
+
 // Launchers, one per kernel family (defined next to their kernels).
 hipError_t launch_known_wait(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_known_fcfs(int max_m, const KArgs &A, hipStream_t s);

@@ -2,31 +2,50 @@
 // Algorithm 2, Section 5.1; event-driven form Algorithm 4, Appendix B.1;
 // coarse segments with heterogeneous prompts, Appendix A).
 //
-// One lane per replica.  Per-type arrival state and per-segment counters
-// live in the lane's own column of LDS; request records live in HBM:
-//   - the external queue Q_{1,0} (FIFO ring);
-//   - for segment k >= 2 the resident boundary queue (a ring kept in
-//     admission-key order, so FIFO selection pops the front and LIFO eviction
-//     pops the back);
+// A group of G lanes (G = 4, 8 or 16, a power of two >= the job's types and
+// segments) runs one replica; a 64-lane wavefront holds 64/G replicas.  Lane
+// g of a group owns request type g (its arrival clock, draw counter and the
+// length of its pending arrival) and segment g (its service count, interior
+// count and memory, calendar, cohort slots and the cache of its youngest
+// interior prompt).  What a batch does segment by segment -- the entering
+// cohorts, the calendar links, the projected state Q+ of the pre-launch
+// repair, the completion walk -- runs on the segment lanes at once; the sums
+// over segments and types (batch tokens, Q+, the earliest arrival, the prefix
+// of segments meeting their thresholds, the most recently admitted eviction
+// candidate) are group reductions with DPP lane permutations inside the
+// 16-lane rows, on the ALU.  Replica-wide scalars (clock, counters, censored
+// areas, resident memory) are kept identical in every lane of the group.
+//
+// Request records live in HBM, in the replica's block of the workspace:
+//   - the external queue Q_{1,0} (FIFO ring of 16-byte records);
+//   - for segment k >= 2 the resident boundary queue (a ring in
+//     admission-key order: FIFO selection pops the front, LIFO eviction pops
+//     the back);
 //   - for every segment a ring of cohort slots indexed by the segment's
-//     service number modulo delta_k (its number of processing stages).  All
-//     prompts that entered the segment at one service form one cohort of at
-//     most n_k prompts and share a stage, so each stage holds one cohort (the
-//     stage-cap invariant of the Nested WAIT analysis) and every interior
-//     prompt of a served segment is selected.
+//     service number modulo delta_k (its number of processing stages).  The
+//     prompts that entered the segment at one service form a cohort of at
+//     most n_k prompts and share a stage (the stage-cap invariant), so every
+//     interior prompt of a served segment is selected.
 // A prompt's exit from its segment (completion at its own output length, or
 // survival to the next boundary queue at r_k) happens at a known service, so
 // each segment keeps a calendar: bucket (service mod delta_k) heads a linked
 // list of the prompts that exit at that service.  Cohorts are linked in
 // reverse admission order, so a bucket is traversed youngest cohort first and
 // in admission order within a cohort: the same (stage, key) order as the
-// oracle's selection list, which fixes the order of floating-point sums and
-// of survivors joining the next boundary queue.
+// oracle's selection list.  The completion latencies a segment lane meets are
+// buffered in LDS and added to the replica's latency sum in segment order, so
+// the floating-point sum takes the oracle's order exactly.
 //
 // The projected state Q+ of the pre-launch repair (apply the selected moves
 // with no early completion) is computed from per-segment counts and the
 // prompts still live in the terminal cohort slot (a record with L = 0 has left
 // its segment).
+//
+// Memory handoffs between lanes of one wavefront (a survivor pushed by lane k
+// into the boundary queue of segment k+1, a record appended to Q_{1,0} by a
+// type lane and read by lane 0) need no hardware fence: the memory operations
+// of a wavefront are performed in order.  wave_lds_sync() keeps the compiler
+// from reordering them.
 #pragma once
 
 #include "sim_common.h"
@@ -34,9 +53,7 @@
 namespace wsim {
 namespace {
 
-// Per-segment constants, staged in LDS: a segment index is often
-// lane-dependent (it starts at a lane's own prefix length), and LDS serves
-// such reads without a round trip to the job table in memory.
+// Per-segment constants, staged in LDS.
 struct SegConst {
   uint64_t dmagic;  // fastmod multiplier for delta
   int32_t end;      // r_k
@@ -60,13 +77,6 @@ __device__ __forceinline__ NRec nrec_of(uint4 a, uint4 b) {
   r.next = b.w;
   return r;
 }
-__device__ __forceinline__ uint4 nrec_lo(const NRec &r) {
-  const uint64_t u = (uint64_t)__double_as_longlong(r.a_ft);
-  return make_uint4((uint32_t)u, (uint32_t)(u >> 32), r.kb, r.kp);
-}
-__device__ __forceinline__ uint4 nrec_hi(const NRec &r) {
-  return make_uint4((uint32_t)r.j, (uint32_t)r.L, r.c, r.next);
-}
 __device__ __forceinline__ QRec qrec_of(uint4 a) {
   QRec q;
   q.a_ft = __longlong_as_double((long long)(((uint64_t)a.y << 32) | a.x));
@@ -74,115 +84,139 @@ __device__ __forceinline__ QRec qrec_of(uint4 a) {
   q.L = (int32_t)a.w;
   return q;
 }
-__device__ __forceinline__ uint4 qrec_u4(const QRec &q) {
-  const uint64_t u = (uint64_t)__double_as_longlong(q.a_ft);
-  return make_uint4((uint32_t)u, (uint32_t)(u >> 32), (uint32_t)q.j, (uint32_t)q.L);
+// A 32-byte record in one round trip: both 16-byte halves issued together.
+__device__ __forceinline__ NRec load_nrec(const NRec *p) {
+  const uint4 lo = ((const uint4 *)p)[0], hi = ((const uint4 *)p)[1];
+  return nrec_of(lo, hi);
 }
-// Asynchronous copy of 4 or 16 bytes per lane from HBM into LDS: lane t
-// writes lds_base + t * size, so lds_base is the start of a per-lane array
-// (and must be the same for all lanes).
-__device__ __forceinline__ void copy4_to_lds(const void *src, void *lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 4, 0,
-                                   0);
+__device__ __forceinline__ uint64_t nrec_key(const NRec &r) {
+  return ((uint64_t)r.kb << 32) | r.kp;
 }
-__device__ __forceinline__ void copy16_to_lds(const void *src, void *lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_base, 16, 0,
-                                   0);
+
+// ---------------------------------------------------------- group lanes --
+// DPP lane permutations inside 16-lane rows (gfx9 encodings): swap neighbours
+// (quad_perm [1,0,3,2]), swap pairs (quad_perm [2,3,0,1]), mirror each half
+// row (lane i <-> 7-i), mirror the row (i <-> 15-i).  After the first two a
+// lane holds its quad's reduction; the half-row mirror pairs each lane with
+// one of the other quad of its 8, the row mirror with one of the other 8 of
+// its 16: an all-reduce over groups of 4, 8 or 16 aligned lanes that reads
+// no lane outside the group.
+constexpr int kDppSwap1 = 0xB1;
+constexpr int kDppSwap2 = 0x4E;
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
-__device__ __forceinline__ uint4 opaque4(uint4 v) {
-  v.x = opaque(v.x);
-  v.y = opaque(v.y);
-  v.z = opaque(v.z);
-  v.w = opaque(v.w);
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  return ((uint64_t)dpp32<CTRL>((uint32_t)(v >> 32)) << 32) | dpp32<CTRL>((uint32_t)v);
+}
+
+template <int G, typename Op>
+__device__ __forceinline__ uint64_t group_reduce64(uint64_t v, Op op) {
+  v = op(v, dpp64<kDppSwap1>(v));
+  v = op(v, dpp64<kDppSwap2>(v));
+  if constexpr (G >= 8) v = op(v, dpp64<kDppHalfMirror>(v));
+  if constexpr (G >= 16) v = op(v, dpp64<kDppMirror>(v));
   return v;
 }
-// Wait for every outstanding memory operation of the wavefront (including the
-// asynchronous copies); also a compiler barrier for memory accesses.
+template <int G>
+__device__ __forceinline__ int64_t group_sum(int64_t v) {
+  return (int64_t)group_reduce64<G>((uint64_t)v, [](uint64_t a, uint64_t b) { return a + b; });
+}
+template <int G>
+__device__ __forceinline__ uint64_t group_max(uint64_t v) {
+  return group_reduce64<G>(v, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
+}
+template <int G>
+__device__ __forceinline__ uint32_t group_or(uint32_t v) {
+  return (uint32_t)group_reduce64<G>((uint64_t)v, [](uint64_t a, uint64_t b) { return a | b; });
+}
+template <int G>
+__device__ __forceinline__ double group_min(double v) {
+  const uint64_t r = group_reduce64<G>((uint64_t)__double_as_longlong(v), [](uint64_t a, uint64_t b) {
+    const double x = __longlong_as_double((long long)a), y = __longlong_as_double((long long)b);
+    return y < x ? b : a;
+  });
+  return __longlong_as_double((long long)r);
+}
+// The group's G bits of a wavefront ballot (bit g = group lane g).
+template <int G>
+__device__ __forceinline__ uint32_t group_bits(bool pred) {
+  const uint64_t b = __ballot(pred);
+  return (uint32_t)((b >> (threadIdx.x & (64 - G))) & ((1ull << G) - 1ull));
+}
+
+// Wait for every outstanding memory operation of the wavefront; also a
+// compiler barrier for memory accesses.
 __device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// MT: type slots (>= m); LT: segment slots (>= L); LN: replicas per
-// wavefront (lanes LN..63 are padding), which sizes the per-lane LDS columns;
-// TV: jobs with time-varying rates are supported (compiled out of the common
-// kernels).
-template <int MT, int LT, int LN, bool TV>
+// G: lanes per replica (types and segments per group); TV: jobs with
+// time-varying rates are supported (compiled out of the common kernels).
+template <int G, bool TV>
 __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
+  constexpr int NR = 64 / G;  // replicas per wavefront
+  constexpr int MT = G;       // type slots
+  constexpr int LT = G;       // segment slots
   // Inter-arrival gaps and output lengths are drawn ahead of use by the
-  // whole wavefront at once into a ring of GR draws per type and lane; a
-  // lane whose ring runs dry draws for itself.
+  // whole wavefront at once into a ring of GR draws per type and replica; a
+  // type lane whose ring runs dry draws for itself.
   constexpr int GR = 4;
   constexpr int GU = GR / 2;         // draws added per refill
-  constexpr uint32_t kLow = GU / 2;  // a lane below this triggers a refill
-  __shared__ double s_tnext[MT][LN];
-  __shared__ uint32_t s_k[MT][LN], s_gend[MT][LN];
-  __shared__ int32_t s_Ln[MT][LN];
-  // With time-varying rates the rings hold candidates of the thinning bound
-  // process with their fourth Philox words (the acceptance draws), and the
-  // rate profile sits in LDS beside them.
-  __shared__ double s_gap[MT][GR][LN];
-  __shared__ int32_t s_glen[MT][GR][LN];
+  constexpr uint32_t kLow = GU / 2;  // a ring below this triggers a refill
+  // completion latencies buffered per segment lane before they are summed
+  constexpr int KL = 8;
+  __shared__ double s_gap[MT][GR][NR];
+  __shared__ int32_t s_glen[MT][GR][NR];
   constexpr int NP = TV ? kMaxRatePts : 1;
-  __shared__ uint32_t s_w3[TV ? MT : 1][TV ? GR : 1][TV ? LN : 1];
+  __shared__ uint32_t s_w3[TV ? MT : 1][TV ? GR : 1][TV ? NR : 1];
   __shared__ RateProfLds<MT, NP> s_prof;
-  __shared__ int8_t s_cur[TV ? MT : 1][TV ? LN : 1];  // profile piece per type
   double(&s_rt)[NP] = s_prof.t;
   double(&s_rf)[MT][NP] = s_prof.f;
   double(&s_fmax)[MT] = s_prof.fmax;
-  __shared__ uint64_t s_seed[LN];
-  __shared__ uint32_t s_rid[LN];
-  // refill requests of one pass, all types together: lane, type, first draw
-  __shared__ uint8_t s_req_lane[MT * LN], s_req_j[MT * LN];
-  __shared__ uint32_t s_req_k[MT * LN];
+  __shared__ uint64_t s_seed[NR];
+  __shared__ uint32_t s_rid[NR];
+  // refill requests of one pass: requesting lane, first draw
+  __shared__ uint8_t s_req_ln[64];
+  __shared__ uint32_t s_req_k[64];
   __shared__ double s_lam[MT];
-  __shared__ uint32_t s_svc[LT][LN], s_I[LT][LN], s_vh[LT][LN], s_vt[LT][LN];
-  __shared__ int64_t s_M[LT][LN], s_B[LT][LN];
   __shared__ int32_t s_l[MT], s_lp[MT];
   __shared__ SegConst s_seg[LT];
-  // Per lane: the back record of each boundary queue, and the youngest live
-  // interior record of each segment with its index (kNil: not known; found by
-  // a scan when next needed).  LIFO selections then read no HBM.
-  __shared__ NRec s_vb[LT][LN], s_yi[LT][LN];
-  __shared__ uint32_t s_yidx[LT][LN];
-  // Per lane and segment: the index of the last youngest interior record that
-  // left the segment (kNil: none known).  Every record entered after it has
-  // left too, so the scan for the next youngest starts just below it; s_yi
-  // still holds it while s_yidx is kNil.
-  __shared__ uint32_t s_ydead[LT][LN];
-  // per type: the guide of its output-length CDF row (kCdfGuide + 1 entries)
+  // per segment and replica: boundary-queue ring ends, boundary memory and
+  // back record (survivors of segment k-1 are pushed by lane k-1)
+  __shared__ uint32_t s_vh[LT][NR], s_vt[LT][NR];
+  __shared__ int64_t s_B[LT][NR];
+  __shared__ NRec s_vb[LT][NR];
+  // completion latencies of one batch, per segment, in traversal order
+  __shared__ double s_lat[LT][KL][NR];
+  __shared__ int32_t s_latn[LT][NR];
+  __shared__ int32_t s_latdone[LT][NR];
   __shared__ uint16_t s_cdfg[MT][kCdfGuide + 1];
-  // Prefetch landing slots, one per lane, filled by asynchronous copies from
-  // HBM (global_load_lds) issued at the end of an iteration and waited for at
-  // the start of the next: the head of Q_{1,0}; per segment that can launch
-  // next, the front of its boundary queue, the first record of the next
-  // launch's terminal cohort slot and the head of the calendar bucket served
-  // next.  32-byte records land as two 16-byte halves.
-  __shared__ uint4 s_q0[LN];
-  __shared__ uint4 s_vfa[LT][LN], s_vfb[LT][LN];
-  __shared__ uint4 s_tra[LT][LN], s_trb[LT][LN];
-  __shared__ uint32_t s_bh[LT][LN];
-  // per lane and segment: the entering cohort's accounting, formed at launch
-  __shared__ int32_t s_eB[LT][LN], s_eM[LT][LN];
-  __shared__ uint32_t s_eI[LT][LN];
   __shared__ double s_edges[WS_MAX_HIST_EDGES + 1];
   __shared__ uint8_t s_htab[kHistTab];
   __shared__ int s_hsteps;
 
   const int tx = threadIdx.x;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + tx;
-  // replica of this lane, or -1 for padding (padding only ends a job's
-  // wavefront, so lane 0 of every wavefront holds a replica)
-  const int32_t r32 = gid < A.n_list ? ((const int32_t *)(A.ws + A.off_list))[gid] : -1;
+  const int gl = tx & (G - 1);  // lane in the group: type gl, segment gl
+  const int q = tx / G;         // replica slot of the wavefront
+  // replica of this group, or -1 for padding (padding only ends a job's
+  // wavefront, so group 0 of every wavefront holds a replica)
+  const int32_t r32 =
+      q < A.lanes ? ((const int32_t *)(A.ws + A.off_list))[(int64_t)blockIdx.x * 64 + q] : -1;
   const int64_t r = r32 < 0 ? 0 : r32;
-  // every lane of a wavefront belongs to the same job: its constants are
+  // every replica of a wavefront belongs to the same job: its constants are
   // wavefront-uniform
   const uint32_t jix =
       __builtin_amdgcn_readfirstlane(((const uint32_t *)(A.ws + A.off_job_of))[r]);
   const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
   const int m = J.m;
+  const int L = J.nseg;
   const int n_hist = J.n_hist;
   const int P = TV ? J.n_rate : 0;  // rate-profile points, 0 for constant rates
   const bool tv = TV && P > 0;
-  // per-type prompt lengths (indexed by a lane's request type) and the
-  // histogram edges with their bucket index, staged in LDS by the block
   {
     const double *edges_g = (const double *)(A.ws + J.off_edges);
     for (int b = tx; b <= n_hist; b += 64) s_edges[b] = b < n_hist ? edges_g[b] : INFINITY;
@@ -193,7 +227,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
     for (int k = tx; k < LT; k += 64) {
       SegConst c;
-      const bool on = k < J.nseg;
+      const bool on = k < L;
       c.end = on ? J.seg_end[k] : 0;
       c.n = on ? J.seg_n[k] : 0;
       c.delta = on ? J.seg_delta[k] : 1;
@@ -227,13 +261,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   }
   const HistIdx hidx = hist_index_build(s_edges, n_hist, s_htab, &s_hsteps);
   const double *edges = s_edges;
-  if (r32 < 0 || tx >= LN) return;  // padding lane: uses only its own LDS columns
+  if (r32 < 0) return;  // padding group: uses nothing of the others
   const uint64_t seed = ((const uint64_t *)(A.ws + A.off_seed))[r];
   const uint32_t rid = ((const uint32_t *)(A.ws + A.off_rid))[r];
-  s_seed[tx] = seed;
-  s_rid[tx] = rid;
+  if (gl == 0) {
+    s_seed[q] = seed;
+    s_rid[q] = rid;
+  }
 
-  const int L = J.nseg;
   const double d0 = J.d0, d1 = J.d1;
   const int64_t C = J.C;
   const bool trace = J.n_trace > 0;
@@ -249,10 +284,26 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   QRec *q10 = (QRec *)(blk + J.off_q[0]);
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
 
-  auto recs = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + s_seg[k].off_rec); };
-  auto bkts = [&](int k) __attribute__((always_inline)) { return (uint32_t *)(blk + s_seg[k].off_bkt); };
-  auto vring = [&](int k) __attribute__((always_inline)) { return (NRec *)(blk + s_seg[k].off_v); };
-  auto vmask = [&](int k) __attribute__((always_inline)) { return s_seg[k].vmask; };
+  // this lane's type and segment
+  const bool is_t = gl < m;
+  const bool is_s = gl < L;
+  const int k = gl;
+  const SegConst sc = s_seg[gl];
+  const int32_t rk = sc.end, nk = sc.n, delta = sc.delta, ent = sc.entry;
+  const int32_t rprev = k >= 1 ? ent - 1 : 0;  // r_{k-1}
+  const uint64_t dmg = sc.dmagic;
+  NRec *rc = (NRec *)(blk + sc.off_rec);
+  uint32_t *bk = (uint32_t *)(blk + sc.off_bkt);
+  NRec *vr = (NRec *)(blk + sc.off_v);
+  const uint32_t vmask = sc.vmask;
+  const int32_t n0 = s_seg[0].n;
+  // the next segment (survivors of this one join its boundary queue)
+  const bool has_next = is_s && k + 1 < L;
+  const int kn = has_next ? k + 1 : gl;
+  const SegConst scn = s_seg[kn];
+  NRec *vrn = (NRec *)(blk + scn.off_v);
+  const uint32_t vmaskn = scn.vmask;
+
   auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
     return (known || cap <= 1) ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
   };
@@ -261,10 +312,20 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return use_guide ? s_cdfg[j] : nullptr;
   };
 
+  // replica-wide scalars, identical in every lane of the group (lat_sum:
+  // group lane 0 only)
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
   int64_t batches, arrivals, comps, ctok, evicts, etok, fallback, btok, peak, idle, N, U,
       Mres, tridx, pendft;
   uint32_t flags, qh, qt;
+  // type lane: next arrival time, its counter and output length, ring end
+  double tn = INFINITY;
+  uint32_t kj = 0, gend = 0;
+  int32_t Lnj = 1;
+  int cur = -1;  // time-varying rates: profile piece of the type's clock
+  // segment lane: services, interior prompts and their memory
+  uint32_t svc = 0, I = 0;
+  int64_t M = 0;
 
   if (!A.resume) {
     t = lat_area = ttft_area = lat_sum = mem_area = busy = 0.0;
@@ -272,35 +333,33 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     N = U = Mres = tridx = pendft = 0;
     flags = 0;
     qh = qt = 0;
-    for (int j = 0; j < MT; ++j) {
-      s_k[j][tx] = 0;
-      s_tnext[j][tx] = INFINITY;
-      s_Ln[j][tx] = 1;
-      if (j < m && !trace) {
-        int32_t Lj = 1;
-        if (tv) {
-          uint32_t k0 = 0;
-          int cur = -1;
-          s_tnext[j][tx] = draw_thinned(seed, rid, (uint32_t)j, k0, 0.0, J.lambda[j], s_fmax[j],
-                                        s_rt, s_rf[j], P, row_of(j), cap, &Lj, cur, flags);
-          s_k[j][tx] = k0;
-        } else {
-          const double g = draw_gap(seed, rid, (uint32_t)j, 0u, J.lambda[j], row_of(j), cap, &Lj,
-                                    nullptr, guide_of(j));
-          s_tnext[j][tx] = 0.0 + g;
-        }
-        s_Ln[j][tx] = known ? J.lp[j] : (cap <= 1 ? 1 : Lj);
+    if (is_t && !trace) {
+      int32_t Lj = 1;
+      if (tv) {
+        uint32_t k0 = 0;
+        uint32_t fl = 0;
+        tn = draw_thinned(seed, rid, (uint32_t)gl, k0, 0.0, J.lambda[gl], s_fmax[gl], s_rt,
+                          s_rf[gl], P, row_of(gl), cap, &Lj, cur, fl);
+        kj = k0;
+        flags |= fl;
+      } else {
+        tn = 0.0 + draw_gap(seed, rid, (uint32_t)gl, 0u, J.lambda[gl], row_of(gl), cap, &Lj,
+                            nullptr, guide_of(gl));
       }
+      Lnj = known ? J.lp[gl] : (cap <= 1 ? 1 : Lj);
     }
-    for (int k = 0; k < LT; ++k) {
-      s_svc[k][tx] = s_I[k][tx] = s_vh[k][tx] = s_vt[k][tx] = 0;
-      s_M[k][tx] = s_B[k][tx] = 0;
-      if (k < L) {
-        uint32_t *bk = bkts(k);
-        for (int x = 0; x < s_seg[k].delta; ++x) bk[x] = kNil;
-      }
+    // flags are replica-wide
+    flags = group_or<G>(flags);
+    if (is_s) {
+      s_vh[k][q] = s_vt[k][q] = 0;
+      s_B[k][q] = 0;
     }
-    for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
+    // calendar buckets start empty: each segment's buckets by the whole group
+    for (int kk = 0; kk < L; ++kk) {
+      uint32_t *b = (uint32_t *)(blk + s_seg[kk].off_bkt);
+      for (int x = gl; x < s_seg[kk].delta; x += G) b[x] = kNil;
+    }
+    for (int b = gl; b < A.hist_stride; b += G) hist[b] = 0;  // whole row, padding included
   } else {
     t = slot_f(A, S_T, r);
     lat_area = slot_f(A, S_LAT, r);
@@ -326,33 +385,40 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     flags = (uint32_t)slot_i(A, S_FLAGS, r);
     qh = (uint32_t)slot_i(A, S_QH, r);
     qt = (uint32_t)slot_i(A, S_QT, r);
-    for (int j = 0; j < MT; ++j) {
-      s_tnext[j][tx] = slot_f(A, S_TNEXT + j, r);
-      s_k[j][tx] = (uint32_t)slot_i(A, S_K + j, r);
-      s_Ln[j][tx] = (int32_t)slot_i(A, S_LNEXT + j, r);
+    if (is_t) {
+      tn = slot_f(A, S_TNEXT + gl, r);
+      kj = (uint32_t)slot_i(A, S_K + gl, r);
+      Lnj = (int32_t)slot_i(A, S_LNEXT + gl, r);
     }
-    for (int k = 0; k < LT; ++k) {
-      s_svc[k][tx] = (uint32_t)slot_i(A, S_KSVC + k, r);
-      s_I[k][tx] = (uint32_t)slot_i(A, S_KI + k, r);
-      s_M[k][tx] = slot_i(A, S_KM + k, r);
-      s_B[k][tx] = slot_i(A, S_KB + k, r);
-      s_vh[k][tx] = (uint32_t)slot_i(A, S_KVH + k, r);
-      s_vt[k][tx] = (uint32_t)slot_i(A, S_KVT + k, r);
+    if (is_s) {
+      svc = (uint32_t)slot_i(A, S_KSVC + k, r);
+      I = (uint32_t)slot_i(A, S_KI + k, r);
+      M = slot_i(A, S_KM + k, r);
+      s_B[k][q] = slot_i(A, S_KB + k, r);
+      s_vh[k][q] = (uint32_t)slot_i(A, S_KVH + k, r);
+      s_vt[k][q] = (uint32_t)slot_i(A, S_KVT + k, r);
     }
   }
+  gend = kj + 1u;  // draw rings start empty
+  // youngest live interior record of this segment and its index (kNil: not
+  // known, found by a scan when next needed); ydead: the index of the last
+  // youngest that left (every record entered after it has left too, so the
+  // scan for the next one starts just below it; yi still holds it while yidx
+  // is kNil)
+  uint32_t yidx = kNil, ydead = kNil;
+  NRec yi;
+  yi.a_ft = 0.0;
+  yi.kb = yi.kp = 0;
+  yi.j = 0;
+  yi.L = 0;
+  yi.c = 0;
+  yi.next = kNil;
+  if (is_s && k >= 1 && s_vt[k][q] != s_vh[k][q])
+    s_vb[k][q] = load_nrec(vr + ((s_vt[k][q] - 1u) & vmask));
+  wave_lds_sync();
 
-  for (int j = 0; j < MT; ++j) {
-    s_gend[j][tx] = s_k[j][tx] + 1u;  // gap rings start empty
-    if constexpr (TV) s_cur[j][tx] = -1;  // profile cursors before the first piece
-  }
-  for (int k = 0; k < LT; ++k) {
-    s_yidx[k][tx] = kNil;
-    s_ydead[k][tx] = kNil;
-    if (k >= 1 && k < L && s_vt[k][tx] != s_vh[k][tx])
-      s_vb[k][tx] = vring(k)[(s_vt[k][tx] - 1u) & vmask(k)];
-  }
-
-  // ---- arrivals ------------------------------------------------------------
+  // ---- arrivals --------------------------------------------------------------
+  // The group's next arrival: its time, and its type (ties: the lowest type).
   auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
     if (trace) {
       if (tridx >= J.n_trace) {
@@ -362,127 +428,104 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       jn = tr_type[tridx];
       return tr_time[tridx];
     }
-    double best = s_tnext[0][tx];
-    jn = 0;
-    for (int j = 1; j < m; ++j) {
-      const double v = s_tnext[j][tx];
-      if (v < best) {
-        best = v;
-        jn = j;
-      }
-    }
-    return best;
+    const double v = is_t ? tn : INFINITY;
+    const double mn = group_min<G>(v);
+    const uint32_t b = group_bits<G>(is_t && v == mn);
+    jn = b != 0 ? __builtin_ctz(b) : 0;
+    return mn;
   };
 
-  auto push_q10 = [&](double a_ft, int32_t j, int32_t Lr) __attribute__((always_inline)) {
+  // Append a record to Q_{1,0}: the counters in every lane, the record by the
+  // lane given.
+  auto push_q10 = [&](bool writer, double a_ft, int32_t j, int32_t Lr)
+                      __attribute__((always_inline)) {
     if (qt - qh >= rec_cap) {
       flags |= kFlagCap;
-    } else {
+    } else if (writer) {
       QRec rec;
       rec.a_ft = a_ft;
       rec.j = j;
       rec.L = Lr;
       q10[qt & qmask] = rec;
-      if (qt == qh) s_q0[tx] = qrec_u4(rec);  // the new head
     }
     qt++;
   };
 
+  // Take the group's pending arrival of type jn at time a.
   auto take = [&](int jn, double a) __attribute__((always_inline)) {
-    int32_t Lr;
+    int32_t Lr = 0;
+    bool writer;
     if (trace) {
       Lr = known ? s_lp[jn] : tr_len[tridx];
       tridx++;
-    } else if (tv) {
-      if constexpr (TV) {  // thinning over the candidates in the ring
-        Lr = s_Ln[jn][tx];
-        uint32_t k = s_k[jn][tx] + 1u;
-        uint32_t ge = s_gend[jn][tx];
-        int32_t Lj = 1;
-        int cur = s_cur[jn][tx];
-        const double tn = next_thinned(k, s_tnext[jn][tx], s_fmax[jn], s_rt, s_rf[jn], P, cur, flags,
-                                       [&](uint32_t kc, double &g, uint32_t &w3) {
-                                         if (kc < ge) {
-                                           g = s_gap[jn][kc % GR][tx];
-                                           w3 = s_w3[jn][kc % GR][tx];
-                                           Lj = s_glen[jn][kc % GR][tx];
-                                         } else {
-                                           g = draw_gap(seed, rid, (uint32_t)jn, kc, J.lambda[jn],
-                                                        row_of(jn), cap, &Lj, &w3);
-                                           ge = kc + 1u;
-                                         }
-                                       });
-        s_cur[jn][tx] = (int8_t)cur;
-        s_gend[jn][tx] = ge;
-        s_k[jn][tx] = k;
-        s_tnext[jn][tx] = tn;
-        s_Ln[jn][tx] = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
-      }
+      writer = gl == 0;
     } else {
-      Lr = s_Ln[jn][tx];
-      const uint32_t k = s_k[jn][tx] + 1u;
-      s_k[jn][tx] = k;
-      int32_t Lj = 1;
-      double g;
-      if (k < s_gend[jn][tx]) {
-        g = s_gap[jn][k % GR][tx];
-        Lj = s_glen[jn][k % GR][tx];
-      } else {
-        g = draw_gap(seed, rid, (uint32_t)jn, k, J.lambda[jn], row_of(jn), cap, &Lj, nullptr,
-                     guide_of(jn));
-        s_gend[jn][tx] = k + 1u;
+      writer = gl == jn;
+      if (writer) {
+        Lr = Lnj;
+        if (tv) {
+          if constexpr (TV) {  // thinning over the candidates in the ring
+            uint32_t kk = kj + 1u;
+            uint32_t ge = gend;
+            int32_t Lj = 1;
+            uint32_t fl = 0;
+            tn = next_thinned(kk, tn, s_fmax[jn], s_rt, s_rf[jn], P, cur, fl,
+                              [&](uint32_t kc, double &g, uint32_t &w3) {
+                                if (kc < ge) {
+                                  g = s_gap[jn][kc % GR][q];
+                                  w3 = s_w3[jn][kc % GR][q];
+                                  Lj = s_glen[jn][kc % GR][q];
+                                } else {
+                                  g = draw_gap(seed, rid, (uint32_t)jn, kc, J.lambda[jn],
+                                               row_of(jn), cap, &Lj, &w3);
+                                  ge = kc + 1u;
+                                }
+                              });
+            gend = ge;
+            kj = kk;
+            flags |= fl;
+            Lnj = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
+          }
+        } else {
+          const uint32_t kk = kj + 1u;
+          kj = kk;
+          int32_t Lj = 1;
+          double g;
+          if (kk < gend) {
+            g = s_gap[jn][kk % GR][q];
+            Lj = s_glen[jn][kk % GR][q];
+          } else {
+            g = draw_gap(seed, rid, (uint32_t)jn, kk, J.lambda[jn], row_of(jn), cap, &Lj,
+                         nullptr, guide_of(jn));
+            gend = kk + 1u;
+          }
+          tn = tn + g;
+          Lnj = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
+        }
       }
-      s_tnext[jn][tx] = s_tnext[jn][tx] + g;
-      s_Ln[jn][tx] = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
+      if constexpr (TV) flags = group_or<G>(flags);  // thinning limit
     }
     arrivals++;
     N++;
     U++;
-    push_q10(a, jn, Lr);
+    push_q10(writer, a, jn, Lr);
   };
 
   // ---- evictions -------------------------------------------------------------
-  // Evict the back (most recently admitted) prompt of boundary queue h >= 1.
-  auto evict_boundary = [&](int h) __attribute__((always_inline)) -> int64_t {
-    const uint32_t vt = s_vt[h][tx] - 1u;
-    const NRec rec = s_vb[h][tx];
-    s_vt[h][tx] = vt;
-    if (vt != s_vh[h][tx]) s_vb[h][tx] = vring(h)[(vt - 1u) & vmask(h)];  // the new back
-    const int32_t rprev = s_seg[h - 1].end;
-    const int64_t ch = (int64_t)s_l[rec.j] + rprev;
-    s_B[h][tx] -= ch;
-    Mres -= ch;
-    evicts++;
-    etok += rprev;
-    push_q10(with_ft(rec.a_ft), rec.j, rec.L);  // it has produced r_{h-1} >= 1 tokens
-    return ch;
-  };
-
-  // Most recently admitted live interior prompt of segment k: the newest
-  // non-empty cohort slot, its highest live index.  Returns the record index
-  // or kNil.
-  auto youngest_interior = [&](int k, uint32_t &kb, uint32_t &kp) __attribute__((always_inline)) -> uint32_t {
-    if (s_I[k][tx] == 0) return kNil;
-    const uint32_t y = s_yidx[k][tx];
-    if (y != kNil) {
-      kb = s_yi[k][tx].kb;
-      kp = s_yi[k][tx].kp;
-      return y;
-    }
-    const int32_t delta = s_seg[k].delta;
-    const int32_t nk = s_seg[k].n;
-    const uint64_t dmg = s_seg[k].dmagic;
-    const uint32_t svc = s_svc[k][tx];
-    const NRec *rc = recs(k);
+  // Most recently admitted live interior prompt of this lane's segment: the
+  // newest non-empty cohort slot, its highest live index.  Lane-local;
+  // returns the record index or kNil (and caches the record in yi).
+  auto youngest_interior = [&]() __attribute__((always_inline)) -> uint32_t {
+    if (!is_s || I == 0) return kNil;
+    if (yidx != kNil) return yidx;
     // start just below the youngest that left last (its cohort entered at
-    // service c, no later cohort has entered since: an entering cohort sets
-    // the cache), else at the newest cohort slot
+    // service yi.c, no later cohort has entered since: an entering cohort
+    // sets the cache), else at the newest cohort slot
     int32_t back = 0, ifrom = nk - 1;
-    const uint32_t dead = s_ydead[k][tx];
-    if (dead != kNil) {
-      const uint32_t c0 = s_yi[k][tx].c;
+    if (ydead != kNil) {
+      const uint32_t c0 = yi.c;
       back = (int32_t)(svc - c0);
-      ifrom = (int32_t)(dead - fastmod(c0, dmg, (uint32_t)delta) * (uint32_t)nk) - 1;
+      ifrom = (int32_t)(ydead - fastmod(c0, dmg, (uint32_t)delta) * (uint32_t)nk) - 1;
       ifrom = ifrom < nk - 1 ? ifrom : nk - 1;  // indices stay inside the cohort slot
     }
     for (; back < delta && (int64_t)svc - back >= 1; ++back, ifrom = nk - 1) {
@@ -490,16 +533,10 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       // a record with L = 0 has left the segment (exit or eviction)
       for (int32_t i = ifrom; i >= 0; --i) {
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
-        // the whole record in one round trip (both halves issued together)
-        uint4 lo = ((const uint4 *)(rc + idx))[0], hi = ((const uint4 *)(rc + idx))[1];
-        lo = opaque4(lo);
-        hi = opaque4(hi);
-        const NRec rec = nrec_of(lo, hi);
+        const NRec rec = load_nrec(rc + idx);
         if (rec.L != 0) {
-          kb = rec.kb;
-          kp = rec.kp;
-          s_yi[k][tx] = rec;
-          s_yidx[k][tx] = idx;
+          yi = rec;
+          yidx = idx;
           return idx;
         }
       }
@@ -507,102 +544,111 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return kNil;
   };
 
-  auto evict_interior = [&](int k, uint32_t idx) __attribute__((always_inline)) -> int64_t {
-    NRec *rc = recs(k);
-    NRec rec = s_yi[k][tx];  // idx is the segment's youngest live interior record
-    s_yidx[k][tx] = kNil;
-    s_ydead[k][tx] = idx;
-    const int32_t delta = s_seg[k].delta;
-    const int32_t nk = s_seg[k].n;
-    const int64_t stage = (int64_t)s_seg[k].entry + (int64_t)(s_svc[k][tx] - rec.c) + 1;
-    const int64_t ch = (int64_t)s_l[rec.j] + stage;
-    (void)delta;
-    (void)nk;
-    const int32_t Lr = rec.L;
-    rec.L = 0;  // leaves a hole; the calendar skips it
-    rc[idx] = rec;
-    s_I[k][tx] -= 1u;
-    s_M[k][tx] -= ch;
+  // Evict the most recently admitted prompt among the boundary queues and,
+  // if allow_interior is set and none holds a prompt, among the interior of
+  // segments [klo, L).  Group-uniform: returns the memory freed (0 if
+  // nothing was left).  `boundary` is cleared once the boundary queues are
+  // found empty: within one repair they stay empty (evicted prompts go back
+  // to the entry queue), so later calls skip that step.
+  auto evict_lifo = [&](int klo, bool allow_interior, bool &boundary)
+                        __attribute__((always_inline)) -> int64_t {
+    if (boundary) {
+      const bool cand = is_s && k >= 1 && s_vt[k][q] != s_vh[k][q];
+      const uint64_t key = cand ? nrec_key(s_vb[k][q]) : 0ull;
+      const uint32_t cb = group_bits<G>(cand);
+      if (cb != 0) {
+        const uint64_t mx = group_max<G>(key);
+        const uint32_t wb = group_bits<G>(cand && key == mx);
+        const bool me = gl == __builtin_ctz(wb);  // keys are unique: one lane
+        int64_t ch = 0, gen = 0;
+        NRec rec = yi;
+        if (me) {
+          rec = s_vb[k][q];
+          const uint32_t vt = s_vt[k][q] - 1u;
+          s_vt[k][q] = vt;
+          if (vt != s_vh[k][q]) s_vb[k][q] = load_nrec(vr + ((vt - 1u) & vmask));  // the new back
+          ch = (int64_t)s_l[rec.j] + rprev;
+          gen = rprev;
+          s_B[k][q] -= ch;
+        }
+        ch = group_sum<G>(ch);
+        gen = group_sum<G>(gen);
+        Mres -= ch;
+        evicts++;
+        etok += gen;
+        push_q10(me, with_ft(rec.a_ft), rec.j, rec.L);  // it has produced r_{h-1} >= 1 tokens
+        wave_lds_sync();
+        return ch;
+      }
+      boundary = false;
+    }
+    if (!allow_interior) return 0;
+    uint32_t idx = kNil;
+    if (k >= klo) idx = youngest_interior();
+    const bool cand = idx != kNil;
+    const uint64_t key = cand ? nrec_key(yi) : 0ull;
+    const uint32_t cb = group_bits<G>(cand);
+    if (cb == 0) return 0;
+    const uint64_t mx = group_max<G>(key);
+    const uint32_t wb = group_bits<G>(cand && key == mx);
+    const bool me = gl == __builtin_ctz(wb);
+    int64_t ch = 0, gen = 0, dpend = 0;
+    const NRec rec = yi;
+    bool ft = false;
+    if (me) {
+      // idx is the segment's youngest live interior record
+      yidx = kNil;
+      ydead = idx;
+      const int64_t stage = (int64_t)ent + (int64_t)(svc - rec.c) + 1;
+      ch = (int64_t)s_l[rec.j] + stage;
+      gen = stage - 1;
+      NRec hole = rec;
+      hole.L = 0;  // leaves a hole; the calendar skips it
+      rc[idx] = hole;
+      I -= 1u;
+      M -= ch;
+      ft = has_ft(rec.a_ft) || stage >= 2;
+      if (stage == 1 && !ft) dpend = 1;
+    }
+    ch = group_sum<G>(ch);
+    gen = group_sum<G>(gen);
+    dpend = group_sum<G>(dpend);
     Mres -= ch;
     evicts++;
     fallback++;
-    etok += stage - 1;
-    const bool ft = has_ft(rec.a_ft) || stage >= 2;
-    if (stage == 1 && !ft) pendft--;
-    push_q10(ft ? with_ft(rec.a_ft) : arrival_of(rec.a_ft), rec.j, Lr);
+    etok += gen;
+    pendft -= dpend;
+    push_q10(me, ft ? with_ft(rec.a_ft) : arrival_of(rec.a_ft), rec.j, rec.L);
+    wave_lds_sync();
     return ch;
   };
 
-  // Evict the most recently admitted prompt among the boundary queues and,
-  // if allow_interior is set and none holds a prompt, among the interior of
-  // segments [klo, L).  Returns the memory freed, 0 if nothing was left.
-  // `boundary` is cleared once the boundary queues are found empty: within
-  // one repair they stay empty (evicted prompts go back to the entry queue),
-  // so later calls skip that scan.
-  auto evict_lifo = [&](int klo, bool allow_interior, bool &boundary)
-                        __attribute__((always_inline)) -> int64_t {
-    int hb = -1;
-    uint32_t bkb = 0, bkp = 0;
-    for (int h = 1; boundary && h < L; ++h) {
-      if (s_vt[h][tx] == s_vh[h][tx]) continue;
-      const uint32_t rkb = s_vb[h][tx].kb, rkp = s_vb[h][tx].kp;
-      if (hb < 0 || rkb > bkb || (rkb == bkb && rkp > bkp)) {
-        hb = h;
-        bkb = rkb;
-        bkp = rkp;
-      }
-    }
-    if (hb >= 0) return evict_boundary(hb);
-    boundary = false;
-    if (!allow_interior) return 0;
-    int kbest = -1;
-    uint32_t ibest = kNil;
-    for (int k = klo; k < L; ++k) {
-      uint32_t kb = 0, kp = 0;
-      const uint32_t idx = youngest_interior(k, kb, kp);
-      if (idx == kNil) continue;
-      if (kbest < 0 || kb > bkb || (kb == bkb && kp > bkp)) {
-        kbest = k;
-        ibest = idx;
-        bkb = kb;
-        bkp = kp;
-      }
-    }
-    if (kbest < 0) return 0;
-    return evict_interior(kbest, ibest);
-  };
-
-  // Stage A of the prefetch (end of an iteration): everything the next
-  // launch and completion read first.  Slot indices are masked into their
-  // rings, so a slot past a queue's tail reads a stale record that is never
-  // used (a push into the empty queue writes the landing slot instead).
-  // A segment k >= 1 can be in the next launch only if its boundary queue
+  // Prefetch, at the end of an iteration, what the next launch reads first:
+  // the head of Q_{1,0}; per segment that can launch next, the head of the
+  // calendar bucket served next, the front of its boundary queue and the
+  // (type, length) words of the next launch's terminal cohort slot.  A
+  // segment k >= 2 can be in the next launch only if its boundary queue
   // already holds n_k prompts (boundary queues change only in the completion
-  // step); only those segments are prefetched.
-  auto may_launch = [&](int k) __attribute__((always_inline)) {
-    return k == 0 || (int32_t)(s_vt[k][tx] - s_vh[k][tx]) >= s_seg[k].n;
-  };
-  auto prefetch_a = [&]() __attribute__((always_inline)) {
-    copy16_to_lds(q10 + (qh & qmask), &s_q0[0]);
-    for (int k = 0; k < L; ++k) {
-      if (!may_launch(k)) continue;
-      const int32_t delta = s_seg[k].delta;
-      const uint32_t x = s_svc[k][tx] + 1u;  // the segment's next service
-      copy4_to_lds(bkts(k) + fastmod(x, s_seg[k].dmagic, (uint32_t)delta), &s_bh[k][0]);
-      if (k >= 1) {
-        const NRec *f = vring(k) + (s_vh[k][tx] & vmask(k));
-        copy16_to_lds(f, &s_vfa[k][0]);
-        copy16_to_lds((const uint8_t *)f + 16, &s_vfb[k][0]);
-      }
-      if (s_seg[k].n == 1) {
-        const NRec *tr = recs(k) + fastmod(x - (uint32_t)(delta - 1), s_seg[k].dmagic, (uint32_t)delta);
-        copy16_to_lds(tr, &s_tra[k][0]);
-        copy16_to_lds((const uint8_t *)tr + 16, &s_trb[k][0]);
-      }
+  // step and its repair, both before this point).
+  uint4 pf_q0 = make_uint4(0u, 0u, 0u, 0u);
+  bool pf_q0_ok = false;  // the head was prefetched (the queue was not empty)
+  uint32_t bh = kNil;     // head of the bucket served next
+  NRec pf_vf = yi;        // front of this segment's boundary queue
+  uint2 pf_tr = make_uint2(0u, 0u);  // (j, L) of the terminal slot's record (n_k = 1)
+  auto prefetch = [&]() __attribute__((always_inline)) {
+    pf_q0_ok = qt != qh;
+    if (gl == 0 && pf_q0_ok) pf_q0 = ((const uint4 *)q10)[qh & qmask];
+    if (is_s && (k == 0 || (int32_t)(s_vt[k][q] - s_vh[k][q]) >= nk)) {
+      const uint32_t x = svc + 1u;  // the segment's next service
+      bh = bk[fastmod(x, dmg, (uint32_t)delta)];
+      if (k >= 1) pf_vf = load_nrec(vr + (s_vh[k][q] & vmask));
+      if (nk == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1)
+        pf_tr = *(const uint2 *)((const uint8_t *)(rc + fastmod(x - (uint32_t)(delta - 1), dmg,
+                                                               (uint32_t)delta)) + 16);
     }
   };
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
-  if (!stopped) prefetch_a();
+  if (!stopped) prefetch();
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
     // ---- refill the draw rings, all active lanes together -----------------
@@ -611,49 +657,37 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       const int nact = __popcll(act);
       const int wrank = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(act >> 32),
                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)act, 0u));
-      // the requests of every type are gathered first and drawn in one pass,
-      // so the types' memory round trips (CDF searches) overlap
-      int nreq = 0;  // wavefront-uniform
-      for (int j = 0; j < m; ++j) {
-        const uint32_t ge = s_gend[j][tx];
-        const uint32_t avail = ge - s_k[j][tx] - 1u;
-        if (__ballot(avail < kLow) == 0) continue;
-        const bool room = avail <= (uint32_t)(GR - GU);
+      const uint32_t avail = gend - kj - 1u;
+      if (__ballot(is_t && avail < kLow) != 0) {
+        const bool room = is_t && avail <= (uint32_t)(GR - GU);
         const uint64_t need = __ballot(room);
         if (room) {
-          const int rk = nreq + (int)__builtin_amdgcn_mbcnt_hi(
-                                    (uint32_t)(need >> 32),
-                                    __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
-          s_req_lane[rk] = (uint8_t)tx;
-          s_req_j[rk] = (uint8_t)j;
-          s_req_k[rk] = ge;
-          s_gend[j][tx] = ge + GU;  // read again only after the pass
+          const int rq = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(need >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)need, 0u));
+          s_req_ln[rq] = (uint8_t)tx;
+          s_req_k[rq] = gend;
+          gend += GU;  // read again only after the pass
         }
-        nreq += __popcll(need);
-      }
-      if (nreq > 0) {
+        const int nreq = __popcll(need);
         wave_lds_sync();
         const int total = nreq * GU;
         for (int base = 0; base < total; base += nact) {
           const int w = base + wrank;
           if (w < total) {
-            const int ln = (int)s_req_lane[w / GU];
-            const int j = (int)s_req_j[w / GU];
-            const uint32_t k = s_req_k[w / GU] + (uint32_t)(w % GU);
+            const int ln = (int)s_req_ln[w / GU];
+            const int j = ln & (G - 1), qq = ln / G;
+            const uint32_t kk = s_req_k[w / GU] + (uint32_t)(w % GU);
             int32_t Lj = 1;
             uint32_t w3;
-            s_gap[j][k % GR][ln] = draw_gap(s_seed[ln], s_rid[ln], (uint32_t)j, k, s_lam[j],
-                                            row_of(j), cap, &Lj, TV ? &w3 : nullptr,
-                                            guide_of(j));
-            s_glen[j][k % GR][ln] = Lj;
-            if constexpr (TV) s_w3[j][k % GR][ln] = w3;
+            s_gap[j][kk % GR][qq] = draw_gap(s_seed[qq], s_rid[qq], (uint32_t)j, kk, s_lam[j],
+                                             row_of(j), cap, &Lj, TV ? &w3 : nullptr, guide_of(j));
+            s_glen[j][kk % GR][qq] = Lj;
+            if constexpr (TV) s_w3[j][kk % GR][qq] = w3;
           }
         }
         wave_lds_sync();
       }
     }
-
-    wait_memory();  // stage A has landed
 
     // ---- decision: largest prefix of segments meeting their thresholds -----
     int kmax = 0;
@@ -662,9 +696,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         stopped = true;
         break;
       }
-      if ((int64_t)(qt - qh) >= s_seg[0].n) {
-        kmax = 1;
-        while (kmax < L && (int64_t)(s_vt[kmax][tx] - s_vh[kmax][tx]) >= s_seg[kmax].n) kmax++;
+      const bool ok = gl == 0 ? (int64_t)(qt - qh) >= n0
+                              : (is_s && (int32_t)(s_vt[k][q] - s_vh[k][q]) >= nk);
+      const uint32_t okb = group_bits<G>(ok);
+      if (okb & 1u) {
+        kmax = __builtin_ctz(~okb);  // lanes >= L never meet it
         break;
       }
       int jn;
@@ -679,7 +715,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       ttft_area += (double)U * dtm;
       mem_area += (double)Mres * dtm;
       t = ta;
-      for (;;) {
+      for (;;) {  // every arrival at this instant joins before the next decision
         if (flags & kFlagCap) break;
         int j2;
         const double a2 = peek(j2);
@@ -687,133 +723,112 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         take(j2, a2);
       }
       idle++;
+      wave_lds_sync();
     }
     if (stopped) break;
 
-
     // ---- launch: entering cohorts, calendar links, batch tokens -----------
+    const bool served = is_s && k < kmax;
     const uint32_t bidx = (uint32_t)batches;
-    int64_t tokens = 0, prefill_l = 0, mplus = Mres;
-    int64_t pend_new = 0;
-    // per-batch trace: every interior prompt of a served segment and the
-    // entering cohorts are processed
-    int64_t bt_sel = 0;
-    const int64_t bt_ev0 = evicts;
-    if constexpr (TV)
-      for (int k = 0; k < kmax; ++k) bt_sel += (int64_t)s_I[k][tx] + s_seg[k].n;
-    for (int k = 0; k < kmax; ++k) {
-      const int32_t delta = s_seg[k].delta;
-      const int32_t nk = s_seg[k].n;
-      const int32_t rk = s_seg[k].end;
-      const int32_t ent = s_seg[k].entry;
-      const uint32_t x = s_svc[k][tx] + 1u;
-      const uint64_t dmg = s_seg[k].dmagic;
+    const uint32_t x = svc + 1u;
+    int64_t tok = 0, pre_l = 0, pend_new = 0, dplus = 0, sel = 0;
+    int32_t eB = 0, eM = 0;
+    uint32_t eI = 0;
+    if (served) {
       const uint32_t slot = fastmod(x, dmg, (uint32_t)delta);
-      NRec *rc = recs(k);
-      uint32_t *bk = bkts(k);
-      tokens += s_M[k][tx];
+      tok = M;  // every interior prompt is processed at its stage
+      sel = (int64_t)I + nk;
       uint32_t suml = 0;
-      int32_t eB = 0, eM = 0;
-      uint32_t eI = 0;
       // link in reverse selection order: traversal is then in key order
       for (int32_t i = nk - 1; i >= 0; --i) {
         NRec e;
         if (k == 0) {
           QRec qr;
-          if (i == 0) {
-            qr = qrec_of(s_q0[tx]);  // the head, prefetched
-          } else {
+          if (i == 0 && pf_q0_ok)
+            qr = qrec_of(pf_q0);  // the head, prefetched
+          else
             qr = q10[(qh + (uint32_t)i) & qmask];
-            qr.a_ft = opaque(qr.a_ft);  // waited for inside this branch
-            qr.j = opaque(qr.j);
-            qr.L = opaque(qr.L);
-          }
           e.a_ft = qr.a_ft;
           e.j = qr.j;
           e.L = qr.L;
           e.kb = bidx;
           e.kp = (uint32_t)i;
-          tokens += s_l[qr.j];
-          prefill_l += s_l[qr.j];
+          tok += s_l[qr.j];
+          pre_l += s_l[qr.j];
           if (!has_ft(qr.a_ft)) pend_new++;
         } else {
-          if (i == 0) {
-            e = nrec_of(s_vfa[k][tx], s_vfb[k][tx]);  // the front, prefetched
-          } else {
-            const NRec *src = vring(k) + ((s_vh[k][tx] + (uint32_t)i) & vmask(k));
-            uint4 lo = ((const uint4 *)src)[0], hi = ((const uint4 *)src)[1];
-            lo = opaque4(lo);  // both halves in flight before the wait
-            hi = opaque4(hi);
-            e = nrec_of(lo, hi);
-          }
-          tokens += (int64_t)s_l[e.j] + s_seg[k - 1].end + 1;
+          e = i == 0 ? pf_vf : load_nrec(vr + ((s_vh[k][q] + (uint32_t)i) & vmask));
+          tok += (int64_t)s_l[e.j] + ent;  // processed at stage r_{k-1} + 1
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
         const uint32_t b = fastmod(x + (uint32_t)(pexit - ent), dmg, (uint32_t)delta);
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
         if (b == slot) {  // exits at this very service: heads the bucket served now
-          e.next = s_bh[k][tx];
-          s_bh[k][tx] = idx;
+          e.next = bh;
+          bh = idx;
         } else {
           e.next = bk[b];
         }
         bk[b] = idx;
         rc[idx] = e;
         if (i == nk - 1) {  // the cohort's last record is the segment's youngest
-          s_yi[k][tx] = e;
-          s_yidx[k][tx] = idx;
+          yi = e;
+          yidx = idx;
         }
-        suml += (uint32_t)s_l[e.j];
-        // what the completion step does with the entering prompts
         const int32_t le = s_l[e.j];
-        if (k > 0) eB += le + s_seg[k - 1].end;
+        suml += (uint32_t)le;
+        // what the completion step does with the entering prompts
+        if (k > 0) eB += le + rprev;
         if (pexit > ent) {
           eI += 1u;
           eM += le + ent + 1;
         }
       }
-      s_eB[k][tx] = eB;
-      s_eI[k][tx] = eI;
-      s_eM[k][tx] = eM;
-      if (k == 0)
-        qh += (uint32_t)nk;
-      else
-        s_vh[k][tx] += (uint32_t)nk;  // still charged in s_B until the completion
+      if (k > 0) s_vh[k][q] += (uint32_t)nk;  // still charged in s_B until the completion
       // projected change of the segment's memory (no early completion)
       if (delta >= 2) {
         uint32_t T = 0, Tl = 0;
         if ((int64_t)x - (delta - 1) >= 1) {
           // the terminal cohort slot: its prompts still in the segment
-          const uint32_t ts = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
           if (nk == 1) {  // prefetched
-            const int32_t trL = (int32_t)s_trb[k][tx].y, trj = (int32_t)s_trb[k][tx].x;
+            const int32_t trL = (int32_t)pf_tr.y, trj = (int32_t)pf_tr.x;
             T = trL != 0 ? 1u : 0u;
             Tl = trL != 0 ? (uint32_t)s_l[trj] : 0u;
           } else {
+            const uint32_t ts = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
             for (int32_t i = 0; i < nk; ++i) {
               // j and L (the second half's first two words) in one load
-              const uint2 jl = opaque(*(const uint2 *)((const uint8_t *)(rc + ts * (uint32_t)nk +
-                                                                          (uint32_t)i) + 16));
+              const uint2 jl = *(const uint2 *)((const uint8_t *)(rc + ts * (uint32_t)nk +
+                                                                  (uint32_t)i) + 16);
               const bool live = (int32_t)jl.y != 0;
               T += live ? 1u : 0u;
               Tl += live ? (uint32_t)s_l[(int32_t)jl.x] : 0u;
             }
           }
         }
-        mplus += (int64_t)s_I[k][tx] - T;
-        if (k == L - 1) mplus -= (int64_t)Tl + (int64_t)T * rk;
+        dplus = (int64_t)I - T;
+        if (k == L - 1) dplus -= (int64_t)Tl + (int64_t)T * rk;
         if (k == 0)
-          mplus += (int64_t)suml + nk;  // prefills land at stage 1
+          dplus += (int64_t)suml + nk;  // prefills land at stage 1
         else
-          mplus += 2ll * nk;            // l + r_{k-1} -> l + r_{k-1} + 2
+          dplus += 2ll * nk;            // l + r_{k-1} -> l + r_{k-1} + 2
       } else {                          // entering prompts are processed at r_k
         if (k < L - 1)
-          mplus += nk;                  // l + r_{k-1} -> l + r_k
+          dplus = nk;                   // l + r_{k-1} -> l + r_k
         else
-          mplus -= (int64_t)suml + (int64_t)nk * s_seg[k - 1].end;
+          dplus = -((int64_t)suml + (int64_t)nk * rprev);
       }
     }
+    const int64_t tokens = group_sum<G>(tok);
+    const int64_t prefill_l = group_sum<G>(pre_l);
+    pend_new = group_sum<G>(pend_new);
+    int64_t mplus = Mres + group_sum<G>(dplus);
+    int64_t bt_sel = 0;
+    if constexpr (TV) bt_sel = group_sum<G>(sel);
+    qh += (uint32_t)n0;
+    const int64_t bt_ev0 = evicts;
+    wave_lds_sync();
 
     // ---- pre-launch repair on the projected state ----------------------------
     bool bnd_pre = true;
@@ -852,53 +867,51 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     mem_area += (double)m_launch * tau;
     busy += tau;
     t = t_end;
+    wave_lds_sync();
 
-    // ---- completion transition, segment by segment ---------------------------
-    for (int k = 0; k < kmax; ++k) {
-      const int32_t delta = s_seg[k].delta;
-      const int32_t rk = s_seg[k].end;
-      const uint32_t x = s_svc[k][tx] + 1u;
-      s_svc[k][tx] = x;
-      NRec *rc = recs(k);
-      if (k == 0) {  // the stage-1 cohort produces its first tokens
-        U -= pendft;
-        pendft = pend_new;
+    // ---- completion transition, every served segment at once ----------------
+    // the stage-1 cohort produces its first tokens
+    U -= pendft;
+    pendft = pend_new;
+    int64_t Mk = M, dM = 0, dcomp = 0, dctok = 0;
+    uint32_t Ik = I, lflags = 0;
+    uint32_t node = kNil;
+    if (served) {
+      svc = x;
+      Mk = M + (int64_t)I + eM;  // every interior prompt advances
+      Ik = I + eI;
+      if (k > 0) {  // entering prompts leave the boundary queue's charge
+        s_B[k][q] -= eB;
+        dM -= eB;
       }
-      int64_t Mk = s_M[k][tx] + (int64_t)s_I[k][tx];  // every interior prompt advances
-      uint32_t Ik = s_I[k][tx];
-      // entering prompts: leave the entry queue, stay unless they exit now
-      // (their sums were formed at launch)
-      if (k > 0) {
-        s_B[k][tx] -= s_eB[k][tx];
-        Mres -= s_eB[k][tx];
-      }
-      Ik += s_eI[k][tx];
-      Mk += s_eM[k][tx];
-      // prompts whose exit is at this service: the bucket's head was
-      // prefetched, the list's records are read on demand
-      uint32_t *bk = bkts(k);
-      const uint32_t b = fastmod(x, s_seg[k].dmagic, (uint32_t)delta);
-      uint32_t idx = s_bh[k][tx];
-      bk[b] = kNil;
-      // Each record is loaded whole (both 16-byte halves at once) one node
-      // ahead: the next record's load is issued before this node's stores,
-      // so waiting for it does not wait for them.
-      uint4 clo = make_uint4(0u, 0u, 0u, 0u), chi = make_uint4(0u, 0u, 0u, kNil);
-      if (idx != kNil) {
-        clo = ((const uint4 *)(rc + idx))[0];
-        chi = ((const uint4 *)(rc + idx))[1];
-      }
-      while (idx != kNil) {
-        const NRec rec = nrec_of(opaque4(clo), opaque4(chi));
-        const uint32_t nxt = rec.next;
-        if (nxt != kNil) {
-          clo = ((const uint4 *)(rc + nxt))[0];
-          chi = ((const uint4 *)(rc + nxt))[1];
+      node = bh;
+      bk[fastmod(x, dmg, (uint32_t)delta)] = kNil;
+    }
+    wave_lds_sync();
+    // Walk the buckets served now.  A lane stops after KL completions until
+    // the group's latency sum has taken them: the sum runs over segments in
+    // order, each segment's latencies in traversal order.
+    NRec crec = yi;
+    if (node != kNil) crec = load_nrec(rc + node);
+    int32_t nbuf = 0;
+    // a bucket lists at most the segment's delta_k * n_k records: a longer
+    // walk could only follow a corrupted link, so it stops the replica
+    uint32_t steps = 0;
+    const uint32_t max_steps = (uint32_t)delta * (uint32_t)nk;
+    for (;;) {
+      while (node != kNil && nbuf < KL) {
+        if (++steps > max_steps) {
+          lflags |= kFlagCap;
+          node = kNil;
+          break;
         }
+        const NRec rec = crec;
+        const uint32_t nxt = rec.next;
+        if (nxt != kNil) crec = load_nrec(rc + nxt);  // one node ahead
         if (rec.L != 0) {  // holes left by evictions are skipped
-          if (idx == s_yidx[k][tx]) {  // the youngest leaves
-            s_ydead[k][tx] = idx;
-            s_yidx[k][tx] = kNil;
+          if (node == yidx) {  // the youngest leaves
+            ydead = node;
+            yidx = kNil;
           }
           const int64_t le = s_l[rec.j];
           const int32_t p = rec.L < rk ? rec.L : rk;
@@ -908,40 +921,58 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           }
           if (rec.L == p) {  // completion at its own output length
             const double lat = t_end - arrival_of(rec.a_ft);
-            lat_sum += lat;
+            s_lat[k][nbuf][q] = lat;
+            nbuf++;
             __hip_atomic_fetch_add(&hist[hist_bin_idx(edges, s_htab, hidx, lat)], 1u,
                                    __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            comps++;
-            ctok += rec.L;
-            N--;
+            dcomp++;
+            dctok += rec.L;
           } else {  // survivor joins the boundary queue of segment k+1
-            const int h = k + 1;
             NRec v = rec;
             v.a_ft = with_ft(rec.a_ft);
-            const uint32_t vt = s_vt[h][tx];
-            if (vt - s_vh[h][tx] <= vmask(h)) {
-              vring(h)[vt & vmask(h)] = v;
-              if (vt == s_vh[h][tx]) {  // pushed into an empty queue: its front
-                s_vfa[h][tx] = nrec_lo(v);
-                s_vfb[h][tx] = nrec_hi(v);
-              }
-              s_vt[h][tx] = vt + 1u;
-              s_vb[h][tx] = v;
+            const uint32_t vt = s_vt[kn][q];
+            if (vt - s_vh[kn][q] <= vmaskn) {
+              vrn[vt & vmaskn] = v;
+              s_vt[kn][q] = vt + 1u;
+              s_vb[kn][q] = v;
             } else {
-              flags |= kFlagCap;  // bounded by construction; guards the ring
+              lflags |= kFlagCap;  // bounded by construction; guards the ring
             }
-            s_B[h][tx] += le + rk;
-            Mres += le + rk;
+            s_B[kn][q] += le + rk;
+            dM += le + rk;
           }
-          rc[idx].L = 0;  // no longer in the segment
+          rc[node].L = 0;  // no longer in the segment
         }
-        idx = nxt;
+        node = nxt;
       }
-      Mres += Mk - s_M[k][tx];
-      s_M[k][tx] = Mk;
-      s_I[k][tx] = Ik;
+      // the group's latency sum takes the buffered latencies in segment order,
+      // up to the first segment still walking
+      if (is_s) {
+        s_latn[k][q] = nbuf;
+        s_latdone[k][q] = node == kNil ? 1 : 0;
+      }
+      wave_lds_sync();
+      if (gl == 0) {
+        for (int kk = 0; kk < kmax; ++kk) {
+          const int32_t nb = s_latn[kk][q];
+          for (int32_t i = 0; i < nb; ++i) lat_sum += s_lat[kk][i][q];
+          s_latn[kk][q] = 0;
+          if (!s_latdone[kk][q]) break;
+        }
+      }
+      wave_lds_sync();
+      if (is_s) nbuf = s_latn[k][q];
+      if (group_bits<G>(node != kNil || nbuf != 0) == 0) break;
     }
+    Mres += group_sum<G>(Mk - M + dM);
+    comps += group_sum<G>(dcomp);
+    ctok += group_sum<G>(dctok);
+    N -= group_sum<G>(dcomp);
+    flags |= group_or<G>(lflags);
+    M = Mk;
+    I = Ik;
     if (Mres > peak) peak = Mres;
+    wave_lds_sync();
 
     // ---- repair: boundary prompts first, then interior prompts -------------
     bool bnd_post = true;
@@ -950,99 +981,85 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
     if constexpr (TV) {
       if (A.btrace != nullptr && batches < A.btrace_cap) {
-        BatchRec br;
-        br.t_launch = t_end - tau;
-        br.tau = tau;
-        br.tokens = tokens;
-        br.prefills = s_seg[0].n;
-        br.selected = bt_sel;
-        br.completions = comps - bt_comps0;
-        br.evict_pre = bt_ev1 - bt_ev0;
-        br.evict_post = evicts - bt_ev1;
-        br.mem_after = Mres;
-        br.waiting_after = qt - qh;
-        int64_t res = 0;
-        for (int k = 0; k < L; ++k) {
-          res += s_I[k][tx];
-          if (k > 0) res += s_vt[k][tx] - s_vh[k][tx];
+        const int64_t res = group_sum<G>(
+            is_s ? (int64_t)I + (k > 0 ? (int64_t)(s_vt[k][q] - s_vh[k][q]) : 0) : 0);
+        if (gl == 0) {
+          BatchRec br;
+          br.t_launch = t_end - tau;
+          br.tau = tau;
+          br.tokens = tokens;
+          br.prefills = n0;
+          br.selected = bt_sel;
+          br.completions = comps - bt_comps0;
+          br.evict_pre = bt_ev1 - bt_ev0;
+          br.evict_post = evicts - bt_ev1;
+          br.mem_after = Mres;
+          br.waiting_after = qt - qh;
+          br.resident_after = res;
+          br.mplus = mplus;
+          ((BatchRec *)A.btrace)[r * A.btrace_cap + batches] = br;
         }
-        br.resident_after = res;
-        br.mplus = mplus;
-        ((BatchRec *)A.btrace)[r * A.btrace_cap + batches] = br;
       }
     }
     batches++;
     btok += tokens;
-    prefetch_a();
+    wave_lds_sync();
+    prefetch();
   }
-  // no asynchronous copy may still target this workgroup's LDS when it ends
   wait_memory();
 
   // ---- save state ------------------------------------------------------------
-  put_f(A, S_T, r, t);
-  put_f(A, S_LAT, r, lat_area);
-  put_f(A, S_TTFT, r, ttft_area);
-  put_f(A, S_LATSUM, r, lat_sum);
-  put_f(A, S_MEM, r, mem_area);
-  put_f(A, S_BUSY, r, busy);
-  put_i(A, S_BATCHES, r, batches);
-  put_i(A, S_ARR, r, arrivals);
-  put_i(A, S_COMP, r, comps);
-  put_i(A, S_CTOK, r, ctok);
-  put_i(A, S_EVICT, r, evicts);
-  put_i(A, S_ETOK, r, etok);
-  put_i(A, S_FALLBACK, r, fallback);
-  put_i(A, S_BTOK, r, btok);
-  put_i(A, S_PEAK, r, peak);
-  put_i(A, S_IDLE, r, idle);
-  put_i(A, S_N, r, N);
-  put_i(A, S_U, r, U);
-  put_i(A, S_MRES, r, Mres);
-  put_i(A, S_TRIDX, r, tridx);
-  put_i(A, S_PENDFT, r, pendft);
-  put_i(A, S_FLAGS, r, (int64_t)flags);
-  put_i(A, S_QH, r, qh);
-  put_i(A, S_QT, r, qt);
-  for (int j = 0; j < MT; ++j) {
-    put_f(A, S_TNEXT + j, r, s_tnext[j][tx]);
-    put_i(A, S_K + j, r, s_k[j][tx]);
-    put_i(A, S_LNEXT + j, r, s_Ln[j][tx]);
+  if (gl == 0) {
+    put_f(A, S_T, r, t);
+    put_f(A, S_LAT, r, lat_area);
+    put_f(A, S_TTFT, r, ttft_area);
+    put_f(A, S_LATSUM, r, lat_sum);
+    put_f(A, S_MEM, r, mem_area);
+    put_f(A, S_BUSY, r, busy);
+    put_i(A, S_BATCHES, r, batches);
+    put_i(A, S_ARR, r, arrivals);
+    put_i(A, S_COMP, r, comps);
+    put_i(A, S_CTOK, r, ctok);
+    put_i(A, S_EVICT, r, evicts);
+    put_i(A, S_ETOK, r, etok);
+    put_i(A, S_FALLBACK, r, fallback);
+    put_i(A, S_BTOK, r, btok);
+    put_i(A, S_PEAK, r, peak);
+    put_i(A, S_IDLE, r, idle);
+    put_i(A, S_N, r, N);
+    put_i(A, S_U, r, U);
+    put_i(A, S_MRES, r, Mres);
+    put_i(A, S_TRIDX, r, tridx);
+    put_i(A, S_PENDFT, r, pendft);
+    put_i(A, S_FLAGS, r, (int64_t)flags);
+    put_i(A, S_QH, r, qh);
+    put_i(A, S_QT, r, qt);
   }
-  for (int k = 0; k < LT; ++k) {
-    put_i(A, S_KSVC + k, r, s_svc[k][tx]);
-    put_i(A, S_KI + k, r, s_I[k][tx]);
-    put_i(A, S_KM + k, r, s_M[k][tx]);
-    put_i(A, S_KB + k, r, s_B[k][tx]);
-    put_i(A, S_KVH + k, r, s_vh[k][tx]);
-    put_i(A, S_KVT + k, r, s_vt[k][tx]);
-  }
+  put_f(A, S_TNEXT + gl, r, is_t ? tn : INFINITY);
+  put_i(A, S_K + gl, r, kj);
+  put_i(A, S_LNEXT + gl, r, Lnj);
+  put_i(A, S_KSVC + k, r, svc);
+  put_i(A, S_KI + k, r, I);
+  put_i(A, S_KM + k, r, M);
+  put_i(A, S_KB + k, r, is_s ? s_B[k][q] : 0);
+  put_i(A, S_KVH + k, r, is_s ? s_vh[k][q] : 0);
+  put_i(A, S_KVT + k, r, is_s ? s_vt[k][q] : 0);
 }
 
-template <int MT, int LT, bool TV>
-hipError_t launch_ml(const KArgs &A, hipStream_t s) {
-  const dim3 g((A.n_list + 63) / 64), b(64);
-  if (A.lanes == 32)
-    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 32, TV>), g, b, 0, s, A);
-  else if (A.lanes == 16)
-    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 16, TV>), g, b, 0, s, A);
-  else if (A.lanes == 8)
-    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 8, TV>), g, b, 0, s, A);
-  else if (A.lanes == 4)
-    hipLaunchKernelGGL((sim_nested_kernel<MT, LT, 4, TV>), g, b, 0, s, A);
-  else
-    return hipErrorInvalidValue;
+template <int G, bool TV>
+hipError_t launch_g(const KArgs &A, hipStream_t s) {
+  hipLaunchKernelGGL((sim_nested_kernel<G, TV>), dim3(A.n_list / 64), dim3(64), 0, s, A);
   return hipGetLastError();
 }
 
 template <bool TV>
 hipError_t launch_nested_k(int max_m, int max_seg, const KArgs &A, hipStream_t s) {
-  if (max_m <= 4) {
-    if (max_seg <= 4) return launch_ml<4, 4, TV>(A, s);
-    if (max_seg <= 8) return launch_ml<4, 8, TV>(A, s);
-    return launch_ml<4, 16, TV>(A, s);
-  }
-  if (max_seg <= 8) return launch_ml<16, 8, TV>(A, s);
-  return launch_ml<16, 16, TV>(A, s);
+  const int G = nested_group_width(max_m, max_seg);
+  // the host's replica list holds 64 / G replicas per wavefront
+  if (A.lanes != 64 / G || A.n_list % 64 != 0) return hipErrorInvalidValue;
+  if (G == 4) return launch_g<4, TV>(A, s);
+  if (G == 8) return launch_g<8, TV>(A, s);
+  return launch_g<16, TV>(A, s);
 }
 
 }  // namespace

@@ -405,17 +405,19 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
     int32_t nmax = 0;  // largest job: no wavefront needs more lanes
     for (int i = 0; i < n_jobs; ++i)
       if (launch_kind(jobs[i].pol) == pk) nmax = std::max(nmax, jobs[i].n);
-    // the Nested WAIT kernel keeps more per-lane state in LDS: at most 32; so
-    // do the known-length kernels with up to 4 types (their 64-lane LDS
-    // footprint would leave half of a CU's SIMDs idle), except replays
-    int lanes = pk == WS_NESTED_WAIT ? 32 : (Lo.max_m[pk] <= 4 && !any_trace ? 32 : 64);
-    const int min_lanes = pk == WS_NESTED_WAIT ? 4 : 8;
+    // the known-length kernels with up to 4 types stop at 32 replicas per
+    // wavefront (their 64-lane LDS footprint would leave half of a CU's SIMDs
+    // idle), except replays
+    int lanes = Lo.max_m[pk] <= 4 && !any_trace ? 32 : 64;
+    const int min_lanes = 8;
     bool any_tv = false;
     for (int i = 0; i < n_jobs; ++i)
       any_tv |= launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_rate_pts > 0;
-    const int64_t target =
-        pk == WS_NESTED_WAIT || any_tv ? kTargetWavesNested : kTargetWaves;
-    if (!any_trace || pk == WS_NESTED_WAIT) {  // known-length replays keep 64
+    const int64_t target = any_tv ? kTargetWavesNested : kTargetWaves;
+    if (pk == WS_NESTED_WAIT) {
+      // a group of lanes per replica: 64 / G replicas per wavefront
+      lanes = 64 / nested_group_width(Lo.max_m[pk], Lo.max_seg);
+    } else if (!any_trace) {  // known-length replays keep 64
       while (lanes > min_lanes && lanes / 2 >= nmax) lanes /= 2;
       while (lanes > min_lanes && waves(lanes) < target) lanes /= 2;
     }
