@@ -127,13 +127,27 @@ template <int G>
 __device__ __forceinline__ int64_t group_sum(int64_t v) {
   return (int64_t)group_reduce64<G>((uint64_t)v, [](uint64_t a, uint64_t b) { return a + b; });
 }
+template <int G, typename Op>
+__device__ __forceinline__ uint32_t group_reduce32(uint32_t v, Op op) {
+  v = op(v, dpp32<kDppSwap1>(v));
+  v = op(v, dpp32<kDppSwap2>(v));
+  if constexpr (G >= 8) v = op(v, dpp32<kDppHalfMirror>(v));
+  if constexpr (G >= 16) v = op(v, dpp32<kDppMirror>(v));
+  return v;
+}
+// Sum of values whose group total fits in 32 bits (per-batch memory changes
+// and counts).
+template <int G>
+__device__ __forceinline__ int32_t group_sum32(int32_t v) {
+  return (int32_t)group_reduce32<G>((uint32_t)v, [](uint32_t a, uint32_t b) { return a + b; });
+}
 template <int G>
 __device__ __forceinline__ uint64_t group_max(uint64_t v) {
   return group_reduce64<G>(v, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
 }
 template <int G>
 __device__ __forceinline__ uint32_t group_or(uint32_t v) {
-  return (uint32_t)group_reduce64<G>((uint64_t)v, [](uint64_t a, uint64_t b) { return a | b; });
+  return group_reduce32<G>(v, [](uint32_t a, uint32_t b) { return a | b; });
 }
 template <int G>
 __device__ __forceinline__ double group_min(double v) {
@@ -417,6 +431,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     s_vb[k][q] = load_nrec(vr + ((s_vt[k][q] - 1u) & vmask));
   wave_lds_sync();
 
+  // What the next launch reads first, loaded ahead (see prefetch below).
+  uint4 pf_q0 = make_uint4(0u, 0u, 0u, 0u);
+  bool pf_q0_ok = false;  // the head was prefetched (the queue was not empty)
+  uint32_t bh = kNil;     // head of the bucket served next
+  NRec pf_vf = yi;        // front of this segment's boundary queue
+  uint2 pf_tr = make_uint2(0u, 0u);  // (j, L) of the terminal slot's record (n_k = 1)
+  uint32_t pf_ti = kNil;             // its index
+
   // ---- arrivals --------------------------------------------------------------
   // The group's next arrival: its time, and its type (ties: the lowest type).
   auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
@@ -559,20 +581,20 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       if (cb != 0) {
         const uint64_t mx = group_max<G>(key);
         const uint32_t wb = group_bits<G>(cand && key == mx);
-        const bool me = gl == __builtin_ctz(wb);  // keys are unique: one lane
-        int64_t ch = 0, gen = 0;
-        NRec rec = yi;
+        const int h = __builtin_ctz(wb);  // keys are unique: one lane
+        const bool me = gl == h;
+        // every lane reads the victim (the back of boundary queue h) and its
+        // charge l + r_{h-1} from LDS
+        const NRec rec = s_vb[h][q];
+        const int64_t gen = s_seg[h].entry - 1;
+        const int64_t ch = (int64_t)s_l[rec.j] + gen;
+        wave_lds_sync();
         if (me) {
-          rec = s_vb[k][q];
           const uint32_t vt = s_vt[k][q] - 1u;
           s_vt[k][q] = vt;
           if (vt != s_vh[k][q]) s_vb[k][q] = load_nrec(vr + ((vt - 1u) & vmask));  // the new back
-          ch = (int64_t)s_l[rec.j] + rprev;
-          gen = rprev;
           s_B[k][q] -= ch;
         }
-        ch = group_sum<G>(ch);
-        gen = group_sum<G>(gen);
         Mres -= ch;
         evicts++;
         etok += gen;
@@ -591,28 +613,32 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     if (cb == 0) return 0;
     const uint64_t mx = group_max<G>(key);
     const uint32_t wb = group_bits<G>(cand && key == mx);
-    const bool me = gl == __builtin_ctz(wb);
-    int64_t ch = 0, gen = 0, dpend = 0;
+    const int w = __builtin_ctz(wb);
+    const bool me = gl == w;
+    int32_t ch = 0, gen = 0, dpend = 0;
     const NRec rec = yi;
     bool ft = false;
     if (me) {
       // idx is the segment's youngest live interior record
       yidx = kNil;
       ydead = idx;
-      const int64_t stage = (int64_t)ent + (int64_t)(svc - rec.c) + 1;
-      ch = (int64_t)s_l[rec.j] + stage;
+      const int32_t stage = ent + (int32_t)(svc - rec.c) + 1;
+      ch = s_l[rec.j] + stage;
       gen = stage - 1;
       NRec hole = rec;
       hole.L = 0;  // leaves a hole; the calendar skips it
       rc[idx] = hole;
+      if (idx == pf_ti) pf_tr.y = 0u;  // the prefetched terminal record has left
       I -= 1u;
       M -= ch;
       ft = has_ft(rec.a_ft) || stage >= 2;
       if (stage == 1 && !ft) dpend = 1;
     }
-    ch = group_sum<G>(ch);
-    gen = group_sum<G>(gen);
-    dpend = group_sum<G>(dpend);
+    // the victim's charge, lost tokens and first-token state, from its lane
+    ch = __shfl(ch, w, G);
+    const int32_t gd = __shfl(gen * 2 + dpend, w, G);
+    gen = gd >> 1;
+    dpend = gd & 1;
     Mres -= ch;
     evicts++;
     fallback++;
@@ -623,18 +649,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     return ch;
   };
 
-  // Prefetch, at the end of an iteration, what the next launch reads first:
-  // the head of Q_{1,0}; per segment that can launch next, the head of the
-  // calendar bucket served next, the front of its boundary queue and the
+  // Prefetch, right after the completion walk, what the next launch reads
+  // first: the head of Q_{1,0}; per segment that can launch next, the head of
+  // the calendar bucket served next, the front of its boundary queue and the
   // (type, length) words of the next launch's terminal cohort slot.  A
   // segment k >= 2 can be in the next launch only if its boundary queue
-  // already holds n_k prompts (boundary queues change only in the completion
-  // step and its repair, both before this point).
-  uint4 pf_q0 = make_uint4(0u, 0u, 0u, 0u);
-  bool pf_q0_ok = false;  // the head was prefetched (the queue was not empty)
-  uint32_t bh = kNil;     // head of the bucket served next
-  NRec pf_vf = yi;        // front of this segment's boundary queue
-  uint2 pf_tr = make_uint2(0u, 0u);  // (j, L) of the terminal slot's record (n_k = 1)
+  // holds n_k prompts now (the repair that follows can only remove prompts;
+  // the front it keeps is the one loaded here, and an interior eviction that
+  // empties the terminal slot clears the prefetched length).
   auto prefetch = [&]() __attribute__((always_inline)) {
     pf_q0_ok = qt != qh;
     if (gl == 0 && pf_q0_ok) pf_q0 = ((const uint4 *)q10)[qh & qmask];
@@ -642,9 +664,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       const uint32_t x = svc + 1u;  // the segment's next service
       bh = bk[fastmod(x, dmg, (uint32_t)delta)];
       if (k >= 1) pf_vf = load_nrec(vr + (s_vh[k][q] & vmask));
-      if (nk == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1)
-        pf_tr = *(const uint2 *)((const uint8_t *)(rc + fastmod(x - (uint32_t)(delta - 1), dmg,
-                                                               (uint32_t)delta)) + 16);
+      pf_ti = kNil;
+      if (nk == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1) {
+        pf_ti = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
+        pf_tr = *(const uint2 *)((const uint8_t *)(rc + pf_ti) + 16);
+      }
     }
   };
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
@@ -731,9 +755,19 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     const bool served = is_s && k < kmax;
     const uint32_t bidx = (uint32_t)batches;
     const uint32_t x = svc + 1u;
-    int64_t tok = 0, pre_l = 0, pend_new = 0, dplus = 0, sel = 0;
+    int64_t tok = 0, sel = 0;
+    int32_t pre_l = 0, pend_new = 0, dplus = 0;
     int32_t eB = 0, eM = 0;
     uint32_t eI = 0;
+    // n_k = 1: the entering record is stored only at the completion step, so
+    // the launch never waits for the bucket head it links to; the walk's
+    // first record (the head prefetched for this service) is loaded now
+    NRec pend = yi;
+    uint32_t pend_idx = kNil;
+    const uint32_t bh0 = bh;
+    NRec crec0 = yi;
+    const bool pre_ok = served && nk == 1 && bh0 != kNil;
+    if (pre_ok) crec0 = load_nrec(rc + bh0);
     if (served) {
       const uint32_t slot = fastmod(x, dmg, (uint32_t)delta);
       tok = M;  // every interior prompt is processed at its stage
@@ -764,14 +798,16 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         const int32_t pexit = e.L < rk ? e.L : rk;
         const uint32_t b = fastmod(x + (uint32_t)(pexit - ent), dmg, (uint32_t)delta);
         const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
-        if (b == slot) {  // exits at this very service: heads the bucket served now
-          e.next = bh;
-          bh = idx;
-        } else {
-          e.next = bk[b];
-        }
+        // (the bucket served now was prefetched as bh: the same head)
+        e.next = b == slot ? bh : bk[b];
         bk[b] = idx;
-        rc[idx] = e;
+        if (b == slot) bh = idx;  // exits at this very service: heads the bucket served now
+        if (nk == 1) {
+          pend = e;
+          pend_idx = idx;
+        } else {
+          rc[idx] = e;
+        }
         if (i == nk - 1) {  // the cohort's last record is the segment's youngest
           yi = e;
           yidx = idx;
@@ -807,23 +843,23 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             }
           }
         }
-        dplus = (int64_t)I - T;
-        if (k == L - 1) dplus -= (int64_t)Tl + (int64_t)T * rk;
+        dplus = (int32_t)I - (int32_t)T;
+        if (k == L - 1) dplus -= (int32_t)Tl + (int32_t)T * rk;
         if (k == 0)
-          dplus += (int64_t)suml + nk;  // prefills land at stage 1
+          dplus += (int32_t)suml + nk;  // prefills land at stage 1
         else
-          dplus += 2ll * nk;            // l + r_{k-1} -> l + r_{k-1} + 2
+          dplus += 2 * nk;              // l + r_{k-1} -> l + r_{k-1} + 2
       } else {                          // entering prompts are processed at r_k
         if (k < L - 1)
           dplus = nk;                   // l + r_{k-1} -> l + r_k
         else
-          dplus = -((int64_t)suml + (int64_t)nk * rprev);
+          dplus = -((int32_t)suml + nk * rprev);
       }
     }
     const int64_t tokens = group_sum<G>(tok);
-    const int64_t prefill_l = group_sum<G>(pre_l);
-    pend_new = group_sum<G>(pend_new);
-    int64_t mplus = Mres + group_sum<G>(dplus);
+    const int64_t prefill_l = group_sum32<G>(pre_l);
+    pend_new = group_sum32<G>(pend_new);
+    int64_t mplus = Mres + group_sum32<G>(dplus);
     int64_t bt_sel = 0;
     if constexpr (TV) bt_sel = group_sum<G>(sel);
     qh += (uint32_t)n0;
@@ -873,9 +909,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     // the stage-1 cohort produces its first tokens
     U -= pendft;
     pendft = pend_new;
-    int64_t Mk = M, dM = 0, dcomp = 0, dctok = 0;
+    int64_t Mk = M, dctok = 0;
+    int32_t dM = 0, dcomp = 0;
     uint32_t Ik = I, lflags = 0;
     uint32_t node = kNil;
+    if (pend_idx != kNil) rc[pend_idx] = pend;  // the entering record (n_k = 1)
     if (served) {
       svc = x;
       Mk = M + (int64_t)I + eM;  // every interior prompt advances
@@ -892,7 +930,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     // the group's latency sum has taken them: the sum runs over segments in
     // order, each segment's latencies in traversal order.
     NRec crec = yi;
-    if (node != kNil) crec = load_nrec(rc + node);
+    if (node != kNil) {
+      if (node == pend_idx)
+        crec = pend;
+      else if (pre_ok && node == bh0)
+        crec = crec0;
+      else
+        crec = load_nrec(rc + node);
+    }
     int32_t nbuf = 0;
     // a bucket lists at most the segment's delta_k * n_k records: a longer
     // walk could only follow a corrupted link, so it stops the replica
@@ -907,7 +952,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         }
         const NRec rec = crec;
         const uint32_t nxt = rec.next;
-        if (nxt != kNil) crec = load_nrec(rc + nxt);  // one node ahead
+        if (nxt != kNil) {  // one node ahead
+          if (pre_ok && nxt == bh0)
+            crec = crec0;
+          else
+            crec = load_nrec(rc + nxt);
+        }
         if (rec.L != 0) {  // holes left by evictions are skipped
           if (node == yidx) {  // the youngest leaves
             ydead = node;
@@ -939,7 +989,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
               lflags |= kFlagCap;  // bounded by construction; guards the ring
             }
             s_B[kn][q] += le + rk;
-            dM += le + rk;
+            dM += (int32_t)(le + rk);
           }
           rc[node].L = 0;  // no longer in the segment
         }
@@ -947,32 +997,36 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       }
       // the group's latency sum takes the buffered latencies in segment order,
       // up to the first segment still walking
-      if (is_s) {
-        s_latn[k][q] = nbuf;
-        s_latdone[k][q] = node == kNil ? 1 : 0;
-      }
-      wave_lds_sync();
-      if (gl == 0) {
-        for (int kk = 0; kk < kmax; ++kk) {
-          const int32_t nb = s_latn[kk][q];
-          for (int32_t i = 0; i < nb; ++i) lat_sum += s_lat[kk][i][q];
-          s_latn[kk][q] = 0;
-          if (!s_latdone[kk][q]) break;
+      if (group_bits<G>(nbuf != 0) != 0) {
+        if (is_s) {
+          s_latn[k][q] = nbuf;
+          s_latdone[k][q] = node == kNil ? 1 : 0;
         }
+        wave_lds_sync();
+        if (gl == 0) {
+          for (int kk = 0; kk < kmax; ++kk) {
+            const int32_t nb = s_latn[kk][q];
+            for (int32_t i = 0; i < nb; ++i) lat_sum += s_lat[kk][i][q];
+            s_latn[kk][q] = 0;
+            if (!s_latdone[kk][q]) break;
+          }
+        }
+        wave_lds_sync();
+        if (is_s) nbuf = s_latn[k][q];
       }
-      wave_lds_sync();
-      if (is_s) nbuf = s_latn[k][q];
       if (group_bits<G>(node != kNil || nbuf != 0) == 0) break;
     }
-    Mres += group_sum<G>(Mk - M + dM);
-    comps += group_sum<G>(dcomp);
+    Mres += group_sum32<G>((int32_t)(Mk - M) + dM);
+    const int32_t nc = group_sum32<G>(dcomp);
+    comps += nc;
+    N -= nc;
     ctok += group_sum<G>(dctok);
-    N -= group_sum<G>(dcomp);
     flags |= group_or<G>(lflags);
     M = Mk;
     I = Ik;
     if (Mres > peak) peak = Mres;
     wave_lds_sync();
+    prefetch();
 
     // ---- repair: boundary prompts first, then interior prompts -------------
     bool bnd_post = true;
@@ -1004,7 +1058,6 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     batches++;
     btok += tokens;
     wave_lds_sync();
-    prefetch();
   }
   wait_memory();
 
