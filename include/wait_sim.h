@@ -103,7 +103,7 @@ typedef enum {
 
 /* Limits of the library. */
 #define WS_MAX_TYPES 16
-#define WS_MAX_TYPES_KNOWN 8  /* WAIT and FCFS: more types give WS_EUNSUPPORTED */
+#define WS_MAX_TYPES_KNOWN 16 /* WAIT and FCFS (the same as WS_MAX_TYPES)       */
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255
 #define WS_MAX_RATE_PTS 32

@@ -499,6 +499,29 @@ __device__ __forceinline__ void place_if(T (&a)[MT], int j, bool c, T v) {
   for (int i = 0; i < MT; ++i) a[i] = opaque((c && i == j) ? v : a[i]);
 }
 
+// Widest wavefront (replicas per wavefront) of the known-length kernel with
+// MT type slots: 64 replicas, 32 with 16 slots (see the note on 16 types in
+// the design notes).
+__host__ __device__ constexpr int known_max_lanes(int mt) { return mt > 8 ? 32 : 64; }
+
+// Launch a simulation kernel on g workgroups of one 64-lane wavefront, after
+// checking that its static LDS fits a workgroup on the current device (a
+// kernel declaring more would otherwise run with the excess unaddressable).
+template <typename Kernel>
+hipError_t launch_checked(Kernel kernel, dim3 g, hipStream_t s, const KArgs &A) {
+  hipFuncAttributes fa;
+  hipError_t e = hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel));
+  if (e != hipSuccess) return e;
+  int dev = 0, lim = 0;
+  e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  e = hipDeviceGetAttribute(&lim, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return e;
+  if (fa.sharedSizeBytes > (size_t)lim) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(kernel, g, dim3(64), 0, s, A);
+  return hipGetLastError();
+}
+
 // Lanes per replica of the Nested WAIT kernel: the smallest of 4, 8, 16 that
 // covers the types and the segments (one type and one segment per lane).
 __host__ __device__ constexpr int nested_group_width(int max_m, int max_seg) {

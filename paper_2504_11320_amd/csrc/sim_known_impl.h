@@ -37,7 +37,7 @@
 namespace wsim {
 namespace {
 
-// MT: type slots (>= m, at most 8); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
+// MT: type slots (>= m, at most 16); POL: WS_WAIT or WS_FCFS; TRACE: some job of the
 // launch replays an arrival list; LN: replicas per wavefront (lanes LN..63
 // are padding), which sizes the per-lane LDS arrays; TV: jobs with
 // time-varying rates are supported (compiled out of the common kernels);
@@ -908,27 +908,25 @@ sim_known_kernel(KArgs A) {
 
 template <int MT, int POL, bool TV, bool ONE>
 hipError_t launch_lanes(const KArgs &A, hipStream_t s) {
-  const int blocks = (A.n_list + 63) / 64;
-  const dim3 g(blocks), b(64);
-  if (A.any_trace) {  // arrival-list replay (tests, small jobs): 64 per wavefront
+  // the widest wavefront for this many type slots (known_max_lanes)
+  constexpr int kMax = known_max_lanes(MT);
+  const dim3 g((A.n_list + 63) / 64);
+  if (A.lanes > kMax) return hipErrorInvalidValue;
+  if (A.any_trace) {  // arrival-list replay (tests, small jobs): the widest wavefront
     if constexpr (TV) {
-      if (A.lanes != 64) return hipErrorInvalidValue;
-      hipLaunchKernelGGL((sim_known_kernel<MT, POL, true, 64, TV, ONE>), g, b, 0, s, A);
+      if (A.lanes != kMax) return hipErrorInvalidValue;
+      return launch_checked(sim_known_kernel<MT, POL, true, kMax, TV, ONE>, g, s, A);
     } else {
       return hipErrorInvalidValue;  // replays run on the TV kernels
     }
-  } else if (A.lanes == 64) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 64, TV, ONE>), g, b, 0, s, A);
-  } else if (A.lanes == 32) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 32, TV, ONE>), g, b, 0, s, A);
-  } else if (A.lanes == 16) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 16, TV, ONE>), g, b, 0, s, A);
-  } else if (A.lanes == 8) {
-    hipLaunchKernelGGL((sim_known_kernel<MT, POL, false, 8, TV, ONE>), g, b, 0, s, A);
-  } else {
-    return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+  if constexpr (kMax == 64) {
+    if (A.lanes == 64) return launch_checked(sim_known_kernel<MT, POL, false, 64, TV, ONE>, g, s, A);
+  }
+  if (A.lanes == 32) return launch_checked(sim_known_kernel<MT, POL, false, 32, TV, ONE>, g, s, A);
+  if (A.lanes == 16) return launch_checked(sim_known_kernel<MT, POL, false, 16, TV, ONE>, g, s, A);
+  if (A.lanes == 8) return launch_checked(sim_known_kernel<MT, POL, false, 8, TV, ONE>, g, s, A);
+  return hipErrorInvalidValue;
 }
 
 // The unit-threshold kernels exist for constant-rate WAIT only.
@@ -946,7 +944,8 @@ hipError_t launch_pol(int max_m, const KArgs &A, hipStream_t s) {
   if (max_m <= 3) return launch_mt<3, POL, TV>(A, s);
   if (max_m <= 4) return launch_mt<4, POL, TV>(A, s);
   if (max_m <= 8) return launch_mt<8, POL, TV>(A, s);
-  return hipErrorInvalidValue;  // the host admits at most WS_MAX_TYPES_KNOWN types
+  if (max_m <= 16) return launch_mt<16, POL, TV>(A, s);
+  return hipErrorInvalidValue;  // the host admits at most WS_MAX_TYPES types
 }
 
 }  // namespace

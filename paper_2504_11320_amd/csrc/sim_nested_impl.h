@@ -1101,8 +1101,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
 template <int G, bool TV>
 hipError_t launch_g(const KArgs &A, hipStream_t s) {
-  hipLaunchKernelGGL((sim_nested_kernel<G, TV>), dim3(A.n_list / 64), dim3(64), 0, s, A);
-  return hipGetLastError();
+  return launch_checked(sim_nested_kernel<G, TV>, dim3(A.n_list / 64), s, A);
 }
 
 template <bool TV>

@@ -238,9 +238,6 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   int64_t reserve_tok = 0;
   if (kind != WS_FCFS && p.fcfs_chunk != 0)
     return fail_job(WS_EINVAL, idx, "fcfs_chunk applies to FCFS only");
-  if (kind != WS_NESTED_WAIT && c.m > WS_MAX_TYPES_KNOWN)
-    return fail_job(WS_EUNSUPPORTED, idx, std::string("WAIT and FCFS take at most ") +
-                                              std::to_string(WS_MAX_TYPES_KNOWN) + " request types");
   if (kind == WS_WAIT) {
     if (!known) return fail_job(WS_EINVAL, idx, "WAIT needs known output lengths");
     if (!p.n) return fail_job(WS_EINVAL, idx, "thresholds required");
@@ -408,7 +405,7 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
     // the known-length kernels with up to 4 types stop at 32 replicas per
     // wavefront (their 64-lane LDS footprint would leave half of a CU's SIMDs
     // idle), except replays
-    int lanes = Lo.max_m[pk] <= 4 && !any_trace ? 32 : 64;
+    int lanes = Lo.max_m[pk] <= 4 && !any_trace ? 32 : known_max_lanes(Lo.max_m[pk]);
     const int min_lanes = 8;
     bool any_tv = false;
     for (int i = 0; i < n_jobs; ++i)
@@ -417,7 +414,7 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
     if (pk == WS_NESTED_WAIT) {
       // a group of lanes per replica: 64 / G replicas per wavefront
       lanes = 64 / nested_group_width(Lo.max_m[pk], Lo.max_seg);
-    } else if (!any_trace) {  // known-length replays keep 64
+    } else if (!any_trace) {  // known-length replays keep the widest
       while (lanes > min_lanes && lanes / 2 >= nmax) lanes /= 2;
       while (lanes > min_lanes && waves(lanes) < target) lanes /= 2;
     }

@@ -72,8 +72,7 @@ def test_fcfs_reserve_validation():
 
 
 def test_type_limits():
-    """WAIT and FCFS take at most 8 request types (more: WS_EUNSUPPORTED);
-    Nested WAIT takes up to 16; more than 16 is invalid everywhere."""
+    """Every policy takes up to 16 request types; more than 16 is invalid."""
     from paper_2504_11320_amd import binding as B
 
     def model(m, policy):
@@ -87,11 +86,9 @@ def test_type_limits():
             kw.update(out_len=[8] * m, n=[1] * m if policy == "wait" else [])
         return [W.Job(W.Workload(**kw), 0, W.ids(2))]
 
-    for policy in ("wait", "fcfs"):
-        assert B.workspace_bytes(B.JobArray(model(8, policy))) > 0
-        assert _err(model(9, policy)).code == B.WS_EUNSUPPORTED
-    assert B.workspace_bytes(B.JobArray(model(16, "nested"))) > 0
-    assert _err(model(17, "nested")).code == B.WS_EINVAL
+    for policy in ("wait", "fcfs", "nested"):
+        assert B.workspace_bytes(B.JobArray(model(16, policy))) > 0
+        assert _err(model(17, policy)).code == B.WS_EINVAL
 
 
 def test_rate_profile_validation():

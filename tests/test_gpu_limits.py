@@ -83,3 +83,21 @@ def test_nested_layouts_agree(B, reps):
     jobs = W.config3(replicas=reps)
     _subset_equal(B, jobs, 300, [(0, 0, 33), (20, reps - 40, reps)],
                   f"Nested WAIT, {32 * reps} replicas")
+
+
+def test_sixteen_types_wait_and_fcfs(B):
+    """16 request types under WAIT and FCFS (thresholds up to 3, 255 edges),
+    37 + 29 replicas: the 16-slot known-length kernel at 32 replicas per
+    wavefront, against the oracle."""
+    rng = np.random.default_rng(16)
+    l, lam = _types(rng, 16)
+    lp = [int(x) for x in rng.integers(1, 64, 16)]
+    C = 4 * max(a + b for a, b in zip(l, lp)) * 4
+    edges = W.default_edges(5.0, 255)
+    wait = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="wait",
+                      n=[int(x) for x in rng.integers(1, 4, 16)], out_len=lp,
+                      hist_edges=edges, record_capacity=1 << 12)
+    fcfs = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="fcfs", n=[],
+                      out_len=lp, reserve=0.01, hist_edges=edges, record_capacity=1 << 12)
+    jobs = [W.Job(wait, 11, W.ids(37)), W.Job(fcfs, 12, W.ids(29, start=500))]
+    check(B, jobs, 1200, "16 types, WAIT and FCFS, 255 edges")
