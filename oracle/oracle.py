@@ -17,6 +17,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "wait_oracle.c")
 HDR = os.path.join(HERE, "wait_oracle.h")
 LIB = os.path.join(HERE, "liboracle.so")
+# another build (e.g. the sanitizer build, build_sanitized()) may be named in
+# WAIT_ORACLE_LIB
+LIB_OVERRIDE = os.environ.get("WAIT_ORACLE_LIB")
 
 
 def _stale() -> bool:
@@ -112,9 +115,24 @@ def load(path: str):
     return L
 
 
+def build_sanitized(out: str) -> str:
+    """The oracle with AddressSanitizer and UndefinedBehaviorSanitizer (clang,
+    shared ASan runtime: preload libclang_rt.asan when loading it)."""
+    cc = "/opt/rocm/lib/llvm/bin/clang"
+    cmd = [cc, "-O1", "-g", "-std=gnu11", "-Wall", "-ffp-contract=off", "-fno-fast-math",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-fno-omit-frame-pointer", "-shared-libasan", "-fPIC", "-shared", "-o", out,
+           SRC, "-lpthread", "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
 def lib():
     global _lib
     if _lib is None:
+        if LIB_OVERRIDE:
+            _lib = load(LIB_OVERRIDE)
+            return _lib
         if _stale():
             build(force=True)
         _lib = load(LIB)

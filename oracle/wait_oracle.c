@@ -317,6 +317,12 @@ static int cmp_seg_stage_key(const void *pa, const void *pb) {
   return 0;
 }
 
+/* Sort n request indices (nothing to sort below two: the array may not
+ * exist yet). */
+static void sort_ids(int64_t *v, int64_t n, int (*cmp)(const void *, const void *)) {
+  if (n > 1) qsort(v, (size_t)n, sizeof(int64_t), cmp);
+}
+
 static int64_t new_req(sim_t *S) {
   if (S->freelist.len > 0) return S->freelist.v[--S->freelist.len];
   if (S->nR == S->capR) {
@@ -574,7 +580,7 @@ static int decide_wait(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
     for (int64_t i = 0; i < S->res.len; i++)
       if (S->R[S->res.v[i]].j == j) S->tmp[cnt++] = S->res.v[i];
     t_sort_R = S->R;
-    qsort(S->tmp, (size_t)cnt, sizeof(int64_t), cmp_stage_key);
+    sort_ids(S->tmp, cnt, cmp_stage_key);
     select_by_stage(S, 0, cnt, c->n[j], tokens);
   }
   return 1;
@@ -605,7 +611,7 @@ static int decide_fcfs(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
       S->tmp[cnt++] = S->res.v[i];
   }
   t_sort_R = S->R;
-  qsort(S->tmp, (size_t)cnt, sizeof(int64_t), cmp_stage_key);
+  sort_ids(S->tmp, cnt, cmp_stage_key);
   for (int64_t i = 0; i < cnt; i++) select_req(S, S->tmp[i], S->R[S->tmp[i]].s, tokens);
   /* prefill budget of this iteration */
   int64_t budget = c->chunk > 0 ? c->chunk : INT64_MAX;
@@ -662,7 +668,7 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   ensure_tmp(S, S->res.len);
   for (int64_t i = 0; i < S->res.len; i++) S->tmp[i] = S->res.v[i];
   t_sort_R = S->R;
-  qsort(S->tmp, (size_t)S->res.len, sizeof(int64_t), cmp_seg_stage_key);
+  sort_ids(S->tmp, S->res.len, cmp_seg_stage_key);
 
   int64_t p = 0;
   int64_t i = 0;

@@ -14,7 +14,9 @@ from typing import Sequence
 import numpy as np
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libwait_sim.so")
+# another build of the library (e.g. the sanitizer build) may be named in
+# WAIT_SIM_LIB
+LIB_PATH = os.environ.get("WAIT_SIM_LIB") or os.path.join(PKG, "libwait_sim.so")
 
 WS_OK, WS_EINVAL, WS_ENOMEM, WS_EDEVICE, WS_EWORKSPACE, WS_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 WS_EINTERNAL = -6

@@ -38,10 +38,18 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build(verbose: bool = False, defines=(), out: str = LIB) -> str:
+# Host-side AddressSanitizer and UndefinedBehaviorSanitizer (device code is
+# built as usual): each -fsanitize= goes right after -Xarch_host.
+SANITIZE_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                  "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
+
+
+def build(verbose: bool = False, defines=(), out: str = LIB, sanitize: bool = False) -> str:
     """Compile every source for gfx950 and link `out` (default: the in-tree
-    library).  `defines` are extra -D options."""
-    dflags = [f"-D{d}" for d in defines]
+    library).  `defines` are extra -D options; `sanitize` instruments the host
+    code with ASan and UBSan (load the result with the clang ASan runtime
+    preloaded)."""
+    dflags = [f"-D{d}" for d in defines] + (SANITIZE_FLAGS if sanitize else [])
     with tempfile.TemporaryDirectory(prefix="wait_sim_build_") as tmp:
         def compile_one(src: str):
             obj = os.path.join(tmp, os.path.basename(src) + ".o")
@@ -58,6 +66,8 @@ def build(verbose: bool = False, defines=(), out: str = LIB) -> str:
         with ThreadPoolExecutor(workers) as ex:
             objs = list(ex.map(compile_one, SRCS))
         cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", out + ".tmp"] + objs
+        if sanitize:
+            cmd += ["-fsanitize=address,undefined", "-shared-libasan"]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)

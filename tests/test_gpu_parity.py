@@ -67,7 +67,9 @@ def test_trace_wait_composition(sim):
 
 
 def test_config1_parity(sim):
-    _check(sim, W.config1(), 2000, "config1 64x2000")
+    # the configuration's full horizon: 64 replicas x 10^4 batches, no stop
+    res, _ = _check(sim, W.config1(), 10000, "config1 64x10000")
+    assert (res["batches"] == 10000).all() and not (res["flags"] & 3).any()
 
 
 def test_config2_parity_ragged(sim):
