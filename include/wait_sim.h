@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 2
+#define WS_ABI_VERSION 3
 
 typedef enum {
   WS_OK = 0,
@@ -256,6 +256,60 @@ int wait_sim_advance_traced(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
                             int32_t resume, void *d_workspace, size_t ws_bytes,
                             void *d_results, size_t results_bytes, void *d_btrace,
                             int64_t btrace_cap, void *hip_stream);
+
+/* Checkpoints of the live state (the simulation state carried from one
+ * batch to the next, Section 2; Nested WAIT's segments, cohorts and boundary
+ * queues, Algorithm 2).  A checkpoint is a device buffer holding a header,
+ * every replica's state slots and latency histogram (structure of arrays over
+ * the replicas), and per replica only the live records of its rings: the
+ * queued prompts between head and tail, the resident records, and for Nested
+ * WAIT every segment's cohort slots and calendar buckets and the boundary
+ * queues.  Its size therefore follows the current queue lengths, not the
+ * worst-case ring capacities of the workspace.  It is position-independent
+ * (it may be copied to the host and back, or to another device) and belongs
+ * to the jobs it was taken for: restoring checks a fingerprint of the jobs'
+ * tables, seeds, replica ids and layout and of this library's layout rules.
+ *
+ * wait_sim_save_state: write the checkpoint of the workspace's current state
+ * to d_state_out (DEVICE memory owned by the caller, state_out_bytes long).
+ * Blocks the host until the checkpoint's size is known (a few small kernels
+ * on hip_stream after its earlier work); the copies then run asynchronously
+ * on hip_stream.  *state_used (if non-NULL) receives the size in bytes.
+ * d_state_out = NULL only sizes the checkpoint.  A buffer smaller than the
+ * size returns WS_EWORKSPACE (with *state_used set) and writes nothing.  The
+ * workspace must not be advanced on another stream meanwhile. */
+int wait_sim_save_state(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
+                        size_t ws_bytes, void *d_state_out,
+                        size_t state_out_bytes, size_t *state_used,
+                        void *hip_stream);
+
+/* wait_sim_load_state: prepare the workspace for the jobs (as
+ * wait_sim_prepare) and restore the checkpoint d_state_in (DEVICE memory,
+ * state_in_bytes long, written by wait_sim_save_state or
+ * wait_sim_run_batch_ex for the same jobs) into it; wait_sim_advance with
+ * resume = 1 then continues exactly as the saved workspace would have.
+ * Blocks the host until the restore has been checked.  Returns WS_EINVAL for
+ * a buffer that is not a checkpoint of these jobs or whose records do not
+ * match its state (nothing outside the checkpoint's used bytes is read). */
+int wait_sim_load_state(const ws_job *jobs, int32_t n_jobs, void *d_workspace,
+                        size_t ws_bytes, const void *d_state_in,
+                        size_t state_in_bytes, void *hip_stream);
+
+/* prepare (or, with d_state_in, load_state) + advance + (with d_state_out or
+ * state_used) save_state, in one call: advance every replica by `horizon`
+ * batches from the empty system, or from the checkpoint d_state_in, and write
+ * the checkpoint of the state it leaves to d_state_out.  The results are
+ * cumulative from t = 0 as for wait_sim_advance.  When d_state_out is too
+ * small the call returns WS_EWORKSPACE after the advance (results written,
+ * *state_used = the size needed): wait_sim_save_state with a larger buffer
+ * then takes the same checkpoint.  A checkpoint buffer must not overlap the
+ * workspace. */
+int wait_sim_run_batch_ex(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                          void *d_workspace, size_t ws_bytes, void *d_results,
+                          size_t results_bytes, void *hip_stream,
+                          const void *d_state_in, size_t state_in_bytes,
+                          void *d_state_out, size_t state_out_bytes,
+                          size_t *state_used);
 
 /* prepare + advance(resume = 0) for one job. */
 int wait_sim_run(const ws_config *cfg, const ws_policy *pol,

@@ -23,7 +23,7 @@ WS_EINTERNAL = -6
 WS_STATIC_WORKSPACE_BYTES = 64 << 20
 WS_WAIT, WS_NESTED_WAIT, WS_FCFS, WS_WAIT_NOWAIT = 0, 1, 2, 3
 WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW, WS_FLAG_THIN_LIMIT = 1, 2, 4, 8
-WS_ABI_VERSION = 2
+WS_ABI_VERSION = 3
 WS_NI64, WS_NF64 = 12, 6
 POLICY = {"wait": WS_WAIT, "nested": WS_NESTED_WAIT, "fcfs": WS_FCFS,
           "wait-nowait": WS_WAIT_NOWAIT}
@@ -107,6 +107,14 @@ def lib():
         L.wait_sim_run_static.argtypes = [C.POINTER(WsConfig), C.POINTER(WsPolicy), C.c_void_p,
                                           C.c_int32, C.c_int64, C.c_void_p, C.c_size_t,
                                           C.c_void_p]
+        L.wait_sim_save_state.argtypes = [jp, C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p,
+                                          C.c_size_t, C.POINTER(C.c_size_t), C.c_void_p]
+        L.wait_sim_load_state.argtypes = [jp, C.c_int32, C.c_void_p, C.c_size_t, C.c_void_p,
+                                          C.c_size_t, C.c_void_p]
+        L.wait_sim_run_batch_ex.argtypes = [jp, C.c_int32, C.c_int64, C.c_void_p, C.c_size_t,
+                                            C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p,
+                                            C.c_size_t, C.c_void_p, C.c_size_t,
+                                            C.POINTER(C.c_size_t)]
         L.wait_sim_last_error.restype = C.c_char_p
         L.wait_sim_abi_version.restype = C.c_int
         if L.wait_sim_abi_version() != WS_ABI_VERSION:
@@ -243,19 +251,59 @@ class Simulation:
                                           self.ws_bytes, self.res.data_ptr(), self.res_bytes,
                                           _stream_handle(self.torch, self.device)))
 
+    def state_bytes(self) -> int:
+        """Size of the checkpoint of the current state (wait_sim_save_state
+        without a buffer)."""
+        used = C.c_size_t()
+        with self.torch.cuda.device(self.device):
+            _check(lib().wait_sim_save_state(self.ja.ptr, self.ja.n_jobs, self.ws.data_ptr(),
+                                             self.ws_bytes, None, 0, C.byref(used),
+                                             _stream_handle(self.torch, self.device)))
+        return int(used.value)
+
     def checkpoint(self, to_host: bool = False):
-        """A copy of the workspace (every replica's state) taken after the
-        calls issued so far: a device tensor, or host memory with to_host."""
-        self.torch.cuda.current_stream(self.device).synchronize()
-        return self.ws.cpu() if to_host else self.ws.clone()
+        """The checkpoint of every replica's live state after the calls issued
+        so far (wait_sim_save_state): a device uint8 tensor of exactly its
+        size, or a host copy with to_host."""
+        torch = self.torch
+        used = C.c_size_t(self.state_bytes())
+        buf = torch.empty(used.value, dtype=torch.uint8, device=self.device)
+        with torch.cuda.device(self.device):
+            _check(lib().wait_sim_save_state(self.ja.ptr, self.ja.n_jobs, self.ws.data_ptr(),
+                                             self.ws_bytes, buf.data_ptr(), used.value,
+                                             C.byref(used), _stream_handle(torch, self.device)))
+        return buf.cpu() if to_host else buf
 
     def restore(self, state) -> None:
-        """Load a checkpoint of a Simulation of the same jobs; continue with
-        advance(..., resume=True)."""
-        if state.numel() != self.ws.numel():
-            raise ValueError("checkpoint of a different workspace layout")
-        self.ws.copy_(state.to(self.device))
+        """Load a checkpoint of a Simulation of the same jobs
+        (wait_sim_load_state); continue with advance(..., resume=True)."""
+        torch = self.torch
+        d = state.to(self.device).contiguous()
+        with torch.cuda.device(self.device):
+            _check(lib().wait_sim_load_state(self.ja.ptr, self.ja.n_jobs, self.ws.data_ptr(),
+                                             self.ws_bytes, d.data_ptr(), d.numel(),
+                                             _stream_handle(torch, self.device)))
         self.prepared = True
+
+    def run_ex(self, horizon: int, state_in=None, state_out=None) -> int:
+        """wait_sim_run_batch_ex: advance by `horizon` batches from the empty
+        system or from the checkpoint `state_in` (a device uint8 tensor), and
+        write the checkpoint of the state it leaves into `state_out` (a device
+        uint8 tensor at least that large) if given.  Returns the checkpoint's
+        size in bytes."""
+        torch = self.torch
+        used = C.c_size_t()
+        sin = state_in.contiguous() if state_in is not None else None
+        with torch.cuda.device(self.device):
+            _check(lib().wait_sim_run_batch_ex(
+                self.ja.ptr, self.ja.n_jobs, int(horizon), self.ws.data_ptr(), self.ws_bytes,
+                self.res.data_ptr(), self.res_bytes, _stream_handle(torch, self.device),
+                sin.data_ptr() if sin is not None else None,
+                sin.numel() if sin is not None else 0,
+                state_out.data_ptr() if state_out is not None else None,
+                state_out.numel() if state_out is not None else 0, C.byref(used)))
+        self.prepared = True
+        return int(used.value)
 
     def advance_traced(self, horizon: int, btrace_cap: int, resume: bool = False) -> np.ndarray:
         """advance() that also returns the per-batch trace: a structured array

@@ -3,6 +3,7 @@
 // table upload, kernel launches and the C ABI declared in include/wait_sim.h.
 #include <algorithm>
 #include <cmath>
+#include <cstddef>
 #include <cstring>
 #include <map>
 #include <mutex>
@@ -47,6 +48,140 @@ __global__ void __launch_bounds__(256) export_kernel(KArgs A, uint8_t *out) {
   const int ff[WS_NF64] = {S_T, S_BUSY, S_LAT, S_TTFT, S_LATSUM, S_MEM};
   for (int f = 0; f < WS_NF64; ++f) of[f * R + r] = slot_f(A, ff[f], r);
   ofl[r] = (uint32_t)slot_i(A, S_FLAGS, r);
+}
+
+// ------------------------------------------------------- checkpoints -----
+// A checkpoint holds a workspace's live state: every replica's state slots
+// and histogram (copied whole, coalesced) and, per replica, the live part of
+// its record rings -- the queued records between head and tail, the resident
+// deques, and for Nested WAIT the cohort slots and calendar buckets of every
+// segment and the boundary queues -- packed back to back.  Ring positions
+// follow from the indices in the state slots, so a restore writes each
+// record back to its slot.  Layout (all offsets multiples of 256):
+//   [header][state slots S_COUNT x R x 8][histograms H x R x 4]
+//   [blob offsets R x 8][blobs]
+struct CkptHeader {
+  uint64_t magic;        // kCkptMagic
+  uint64_t fingerprint;  // of the jobs' workspace layout
+  uint64_t used;         // bytes of the checkpoint in use (header included)
+  uint64_t R;            // replicas
+  uint64_t state_off, hist_off, dir_off, blob_off;
+  uint64_t pad[24];
+};
+static_assert(sizeof(CkptHeader) == 256, "checkpoint header layout");
+constexpr uint64_t kCkptMagic = 0x31504B434D495357ull;  // "WSIMCKP1"
+
+// The live ring segments of replica r, in a fixed order: f(ring base, index
+// mask, log2 of the 4-byte words per record, first index, records).  A ring
+// holds at most its capacity (a full queue counts the pushes it could not
+// store and flags the replica).
+template <typename F>
+__device__ __forceinline__ void for_each_segment(const KArgs &A, int64_t r, F f) {
+  const uint32_t jix = ((const uint32_t *)(A.ws + A.off_job_of))[r];
+  const JobDev &J = ((const JobDev *)(A.ws + A.off_jobs))[jix];
+  uint8_t *blk = A.ws + J.off_ring + (uint64_t)(r - J.replica_begin) * J.ring_stride;
+  auto hd = [&](int s) { return (uint32_t)slot_i(A, s, r); };
+  auto ring = [&](uint8_t *base, int cap_log2, int wl, int sh, int st) {
+    const uint32_t cap = 1u << cap_log2, h = hd(sh), n = hd(st) - h;
+    f(base, cap - 1u, wl, h, n < cap ? n : cap);
+  };
+  if (J.policy == WS_NESTED_WAIT) {
+    ring(blk + J.off_q[0], J.qcap_log2, 2, S_QH, S_QT);
+    for (int k = 0; k < J.nseg; ++k) {
+      const uint32_t cells = (uint32_t)J.seg_delta[k] * (uint32_t)J.seg_n[k];
+      f(blk + J.off_rec[k], ~0u, 3, 0u, cells);
+      f(blk + J.off_bkt[k], ~0u, 0, 0u, (uint32_t)J.seg_delta[k]);
+      if (k >= 1) ring(blk + J.off_v[k], J.vcap_log2[k], 3, S_KVH + k, S_KVT + k);
+    }
+    return;
+  }
+  const bool wait = J.policy == WS_WAIT;
+  for (int j = 0; j < (wait ? J.m : 1); ++j)
+    ring(blk + J.off_q[j], J.qcap_log2, wait ? 1 : 2, S_QH + j, S_QT + j);
+  for (int j = 0; j < J.m; ++j) ring(blk + J.off_d[j], J.dcap_log2[j], 2, S_DH + j, S_DT + j);
+}
+
+__device__ __forceinline__ uint64_t packed_bytes(const KArgs &A, int64_t r) {
+  uint64_t words = 0;
+  for_each_segment(A, r, [&](uint8_t *, uint32_t, int wl, uint32_t, uint32_t n) {
+    words += (uint64_t)n << wl;
+  });
+  return 4ull * words;
+}
+
+// Bytes of each replica's packed rings.
+__global__ void __launch_bounds__(256) ckpt_size_kernel(KArgs A, uint64_t *bytes) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < A.R) bytes[r] = packed_bytes(A, r);
+}
+
+// Exclusive prefix sum of the blob sizes in place (one workgroup of 1024
+// threads, each over a contiguous chunk); writes the header with the total.
+__global__ void __launch_bounds__(1024) ckpt_scan_kernel(uint64_t *dir, int64_t R, CkptHeader hdr,
+                                                         CkptHeader *out) {
+  __shared__ uint64_t part[1024];
+  const int tid = threadIdx.x;
+  const int64_t chunk = (R + 1023) / 1024;
+  const int64_t lo = tid * chunk < R ? tid * chunk : R;
+  const int64_t hi = lo + chunk < R ? lo + chunk : R;
+  uint64_t sum = 0;
+  for (int64_t i = lo; i < hi; ++i) sum += dir[i];
+  part[tid] = sum;
+  __syncthreads();
+  if (tid == 0) {
+    uint64_t run = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const uint64_t v = part[i];
+      part[i] = run;
+      run += v;
+    }
+    hdr.used = hdr.blob_off + run;
+    *out = hdr;
+  }
+  __syncthreads();
+  uint64_t run = part[tid];
+  for (int64_t i = lo; i < hi; ++i) {
+    const uint64_t v = dir[i];
+    dir[i] = run;
+    run += v;
+  }
+}
+
+// Copy every replica's live ring segments into its blob (to_ckpt) or back
+// into the workspace: one wavefront per replica, lanes over 4-byte words.  A
+// blob that would end beyond `limit` bytes of blob space is not copied and
+// sets *bad (a checkpoint whose blobs do not match its state slots).
+__global__ void __launch_bounds__(64) ckpt_copy_kernel(KArgs A, uint8_t *ckpt, const uint64_t *dir,
+                                                       uint64_t blob_off, uint64_t limit,
+                                                       int to_ckpt, uint32_t *bad) {
+  const int64_t r = blockIdx.x;
+  if (r >= A.R) return;
+  const uint64_t start = dir[r], bytes = packed_bytes(A, r);
+  if (start > limit || bytes > limit - start) {
+    if (threadIdx.x == 0) atomicOr(bad, 1u);
+    return;
+  }
+  uint32_t *blob = (uint32_t *)(ckpt + blob_off + start);
+  uint64_t pos = 0;
+  for_each_segment(A, r, [&](uint8_t *base, uint32_t mask, int wl, uint32_t lo, uint32_t n) {
+    uint32_t *ring = (uint32_t *)base;
+    const uint64_t total = (uint64_t)n << wl;
+    const uint32_t wmask = (1u << wl) - 1u;
+    for (uint64_t x = threadIdx.x; x < total; x += 64) {
+      const uint32_t rec = (uint32_t)(x >> wl), word = (uint32_t)x & wmask;
+      uint32_t *cell = ring + ((uint64_t)((lo + rec) & mask) << wl) + word;
+      if (to_ckpt)
+        blob[pos + x] = *cell;
+      else
+        *cell = blob[pos + x];
+    }
+    pos += total;
+  });
+}
+
+// Write the finished header (after every copy on the stream).
+__global__ void ckpt_seal_kernel(CkptHeader hdr, CkptHeader *out) {
+  if (threadIdx.x == 0) *out = hdr;
 }
 
 // ------------------------------------------------------------- host -----
@@ -131,7 +266,7 @@ struct Layout {
   int32_t hist_stride = 1;
   uint64_t off_jobs = 0, off_seed = 0, off_rid = 0, off_job_of = 0,
            off_list = 0, off_tables = 0, off_state = 0, off_hist = 0,
-           off_rings = 0, total = 0;
+           off_dir = 0, off_rings = 0, total = 0;
   JobHost *jobs = nullptr;     // [n_jobs]: `own`, or storage of the caller
   std::vector<JobHost> own;
   int32_t list_count[3] = {0, 0, 0};
@@ -427,7 +562,7 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
   if (R > (int64_t(1) << 30)) return fail(WS_EINVAL, "too many replicas");
   Lo.R = R;
   Lo.hist_stride = hmax;
-  uint64_t off = 256;
+  uint64_t off = 256;  // [0, 256): control block (checkpoint header, status)
   Lo.off_jobs = off;
   off = align_up(off + sizeof(JobDev) * (uint64_t)n_jobs, 256);
   Lo.off_seed = off;
@@ -460,6 +595,8 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
   off = align_up(off + 8ull * S_COUNT * (uint64_t)R, 256);
   Lo.off_hist = off;
   off = align_up(off + 4ull * (uint64_t)hmax * (uint64_t)R, 256);
+  Lo.off_dir = off;  // checkpoints: per-replica blob offsets
+  off = align_up(off + 8ull * (uint64_t)R, 256);
   Lo.off_rings = off;
   for (int i = 0; i < n_jobs; ++i) {
     JobHost &H = Lo.jobs[i];
@@ -533,12 +670,10 @@ KArgs base_args(const Layout &Lo, void *d_ws) {
   return A;
 }
 
-// Write the table image (everything in front of the state region: job
-// descriptors, streams, replica lists and per-job tables) into `img`
-// (Lo.off_state bytes), copy it to the workspace on stream s and wait for the
-// copy.  Allocates nothing.
-int prepare_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *img,
-                  void *d_workspace, hipStream_t s) {
+// Write the table image (everything in front of the state region: the
+// control block, job descriptors, streams, replica lists and per-job tables)
+// into `img` (Lo.off_state bytes).
+void build_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *img) {
   std::memset(img, 0, Lo.off_state);
   for (int i = 0; i < n_jobs; ++i)
     std::memcpy(img + Lo.off_jobs + sizeof(JobDev) * i, &Lo.jobs[i].d, sizeof(JobDev));
@@ -578,6 +713,13 @@ int prepare_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t 
       std::memcpy(img + d.off_rate + 8ull * c.n_rate_pts, c.rate_f, 8ull * c.n_rate_pts * c.m);
     }
   }
+}
+
+// build_image, then copy the image to the workspace on stream s and wait for
+// the copy.  Allocates nothing.
+int prepare_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *img,
+                  void *d_workspace, hipStream_t s) {
+  build_image(jobs, n_jobs, Lo, img);
   HIP_TRY(hipMemcpyAsync(d_workspace, img, Lo.off_state, hipMemcpyHostToDevice, s));
   HIP_TRY(hipStreamSynchronize(s));
   return WS_OK;
@@ -693,6 +835,124 @@ int check_advance(const Layout &Lo, int64_t horizon, const void *d_workspace, si
   if (!d_workspace || !d_results) return fail(WS_EINVAL, "device buffers must be non-NULL");
   if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
   if (results_bytes < results_size(Lo)) return fail(WS_EWORKSPACE, "result buffer too small");
+  return WS_OK;
+}
+
+// ---------------------------------------------------- checkpoint host --
+
+// Fingerprint of the jobs a checkpoint belongs to: a 64-bit hash of the
+// table image (job descriptors with every workspace offset, seeds, replica
+// ids, replica lists, tables) and of the layout's sizes.
+uint64_t fingerprint(const Layout &Lo, const uint8_t *img) {
+  uint64_t h = 0x9E3779B97F4A7C15ull;
+  auto mix = [&](uint64_t w) {
+    h ^= w;
+    h *= 0xBF58476D1CE4E5B9ull;
+    h ^= h >> 31;
+  };
+  for (uint64_t i = 0; i + 8 <= Lo.off_state; i += 8) {
+    uint64_t w;
+    std::memcpy(&w, img + i, 8);
+    mix(w);
+  }
+  mix((uint64_t)Lo.R);
+  mix((uint64_t)Lo.hist_stride);
+  mix(Lo.total);
+  return h;
+}
+
+// The checkpoint's header as the jobs lay it out (used = 0, magic = 0).
+CkptHeader ckpt_geometry(const Layout &Lo, uint64_t fp) {
+  CkptHeader h;
+  std::memset(&h, 0, sizeof(h));
+  const uint64_t R = (uint64_t)Lo.R;
+  h.fingerprint = fp;
+  h.R = R;
+  h.state_off = sizeof(CkptHeader);
+  h.hist_off = align_up(h.state_off + 8ull * S_COUNT * R, 256);
+  h.dir_off = align_up(h.hist_off + 4ull * (uint64_t)Lo.hist_stride * R, 256);
+  h.blob_off = align_up(h.dir_off + 8ull * R, 256);
+  return h;
+}
+
+// Size the checkpoint of the workspace's current state (blocks until known)
+// and, when d_out holds it, write it on stream s.
+int save_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, void *d_ws, void *d_out,
+              size_t out_bytes, size_t *used, hipStream_t s) {
+  std::vector<uint8_t> img(Lo.off_state);
+  build_image(jobs, n_jobs, Lo, img.data());
+  CkptHeader hdr = ckpt_geometry(Lo, fingerprint(Lo, img.data()));
+  KArgs A = base_args(Lo, d_ws);
+  uint8_t *ws = (uint8_t *)d_ws;
+  uint64_t *dir = (uint64_t *)(ws + Lo.off_dir);
+  CkptHeader *ctl = (CkptHeader *)ws;  // control block
+  const int tb = 256;
+  hipLaunchKernelGGL(ckpt_size_kernel, dim3((unsigned)((Lo.R + tb - 1) / tb)), dim3(tb), 0, s, A,
+                     dir);
+  HIP_TRY(hipGetLastError());
+  hipLaunchKernelGGL(ckpt_scan_kernel, dim3(1), dim3(1024), 0, s, dir, (int64_t)Lo.R, hdr, ctl);
+  HIP_TRY(hipGetLastError());
+  CkptHeader got;
+  HIP_TRY(hipMemcpyAsync(&got, ctl, sizeof(got), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (used) *used = (size_t)got.used;
+  if (!d_out) return WS_OK;
+  if (out_bytes < got.used)
+    return fail(WS_EWORKSPACE, "checkpoint buffer too small: the state needs " +
+                                   std::to_string(got.used) + " bytes");
+  uint8_t *out = (uint8_t *)d_out;
+  const uint64_t R = (uint64_t)Lo.R;
+  HIP_TRY(hipMemcpyAsync(out + hdr.state_off, ws + Lo.off_state, 8ull * S_COUNT * R,
+                         hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipMemcpyAsync(out + hdr.hist_off, ws + Lo.off_hist,
+                         4ull * (uint64_t)Lo.hist_stride * R, hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipMemcpyAsync(out + hdr.dir_off, dir, 8ull * R, hipMemcpyDeviceToDevice, s));
+  uint32_t *bad = (uint32_t *)(ws + offsetof(CkptHeader, pad));
+  hipLaunchKernelGGL(ckpt_copy_kernel, dim3((unsigned)R), dim3(64), 0, s, A, out,
+                     (const uint64_t *)dir, hdr.blob_off, got.used - hdr.blob_off, 1, bad);
+  HIP_TRY(hipGetLastError());
+  got.magic = kCkptMagic;
+  hipLaunchKernelGGL(ckpt_seal_kernel, dim3(1), dim3(64), 0, s, got, (CkptHeader *)out);
+  HIP_TRY(hipGetLastError());
+  return WS_OK;
+}
+
+// Prepare the workspace for the jobs and restore the checkpoint d_in into it
+// on stream s (blocks until the checks are done).
+int load_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, void *d_ws, const void *d_in,
+              size_t in_bytes, hipStream_t s) {
+  if (in_bytes < sizeof(CkptHeader)) return fail(WS_EINVAL, "checkpoint smaller than its header");
+  std::vector<uint8_t> img(Lo.off_state);
+  int rc = prepare_image(jobs, n_jobs, Lo, img.data(), d_ws, s);
+  if (rc != WS_OK) return rc;
+  const CkptHeader want = ckpt_geometry(Lo, fingerprint(Lo, img.data()));
+  CkptHeader got;
+  HIP_TRY(hipMemcpyAsync(&got, d_in, sizeof(got), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (got.magic != kCkptMagic) return fail(WS_EINVAL, "not a checkpoint (bad magic)");
+  if (got.fingerprint != want.fingerprint || got.R != want.R || got.state_off != want.state_off ||
+      got.hist_off != want.hist_off || got.dir_off != want.dir_off ||
+      got.blob_off != want.blob_off)
+    return fail(WS_EINVAL, "checkpoint taken for other jobs (fingerprint or layout differs)");
+  if (got.used < got.blob_off || got.used > in_bytes)
+    return fail(WS_EINVAL, "checkpoint size does not match its header");
+  const uint8_t *in = (const uint8_t *)d_in;
+  uint8_t *ws = (uint8_t *)d_ws;
+  const uint64_t R = (uint64_t)Lo.R;
+  HIP_TRY(hipMemcpyAsync(ws + Lo.off_state, in + got.state_off, 8ull * S_COUNT * R,
+                         hipMemcpyDeviceToDevice, s));
+  HIP_TRY(hipMemcpyAsync(ws + Lo.off_hist, in + got.hist_off,
+                         4ull * (uint64_t)Lo.hist_stride * R, hipMemcpyDeviceToDevice, s));
+  KArgs A = base_args(Lo, d_ws);
+  uint32_t *bad = (uint32_t *)(ws + offsetof(CkptHeader, pad));  // zeroed by the image
+  hipLaunchKernelGGL(ckpt_copy_kernel, dim3((unsigned)R), dim3(64), 0, s, A,
+                     const_cast<uint8_t *>(in), (const uint64_t *)(in + got.dir_off),
+                     got.blob_off, got.used - got.blob_off, 0, bad);
+  HIP_TRY(hipGetLastError());
+  uint32_t status = 0;
+  HIP_TRY(hipMemcpyAsync(&status, bad, 4, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  if (status != 0) return fail(WS_EINVAL, "checkpoint blobs do not match its state slots");
   return WS_OK;
 }
 
@@ -812,6 +1072,65 @@ int wait_sim_run_batch(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
   if (rc != WS_OK) return rc;
   return wait_sim_advance(jobs, n_jobs, horizon, 0, d_workspace, ws_bytes, d_results,
                           results_bytes, hip_stream);
+}
+
+int wait_sim_save_state(const ws_job *jobs, int32_t n_jobs, void *d_workspace, size_t ws_bytes,
+                        void *d_state_out, size_t state_out_bytes, size_t *state_used,
+                        void *hip_stream) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    if (!d_workspace) return fail(WS_EINVAL, "workspace must be non-NULL");
+    if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
+    if (!d_state_out && !state_used)
+      return fail(WS_EINVAL, "need a checkpoint buffer or state_used");
+    return save_impl(jobs, n_jobs, Lo, d_workspace, d_state_out, state_out_bytes, state_used,
+                     (hipStream_t)hip_stream);
+  });
+}
+
+int wait_sim_load_state(const ws_job *jobs, int32_t n_jobs, void *d_workspace, size_t ws_bytes,
+                        const void *d_state_in, size_t state_in_bytes, void *hip_stream) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    if (!d_workspace || !d_state_in) return fail(WS_EINVAL, "device buffers must be non-NULL");
+    if (ws_bytes < Lo.total) return fail(WS_EWORKSPACE, "workspace too small");
+    return load_impl(jobs, n_jobs, Lo, d_workspace, d_state_in, state_in_bytes,
+                     (hipStream_t)hip_stream);
+  });
+}
+
+int wait_sim_run_batch_ex(const ws_job *jobs, int32_t n_jobs, int64_t horizon,
+                          void *d_workspace, size_t ws_bytes, void *d_results,
+                          size_t results_bytes, void *hip_stream, const void *d_state_in,
+                          size_t state_in_bytes, void *d_state_out, size_t state_out_bytes,
+                          size_t *state_used) {
+  return guarded([&]() -> int {
+    g_err.clear();
+    Layout Lo;
+    int rc = make_layout(jobs, n_jobs, Lo);
+    if (rc != WS_OK) return rc;
+    rc = check_advance(Lo, horizon, d_workspace, ws_bytes, d_results, results_bytes);
+    if (rc != WS_OK) return rc;
+    hipStream_t s = (hipStream_t)hip_stream;
+    if (d_state_in) {
+      rc = load_impl(jobs, n_jobs, Lo, d_workspace, d_state_in, state_in_bytes, s);
+    } else {
+      std::vector<uint8_t> img(Lo.off_state);
+      rc = prepare_image(jobs, n_jobs, Lo, img.data(), d_workspace, s);
+    }
+    if (rc != WS_OK) return rc;
+    rc = advance_impl(jobs, n_jobs, Lo, horizon, d_state_in ? 1 : 0, d_workspace, d_results,
+                      nullptr, 0, s);
+    if (rc != WS_OK) return rc;
+    if (!d_state_out && !state_used) return WS_OK;
+    return save_impl(jobs, n_jobs, Lo, d_workspace, d_state_out, state_out_bytes, state_used, s);
+  });
 }
 
 int wait_sim_run(const ws_config *cfg, const ws_policy *pol, const ws_stream *streams,

@@ -25,7 +25,7 @@ def test_library_exports_header_symbols():
     assert "wait_sim_run" in names and "wait_sim_advance" in names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.wait_sim_abi_version() == B.WS_ABI_VERSION == 2
+    assert lib.wait_sim_abi_version() == B.WS_ABI_VERSION == 3
 
 
 def _err(jobs):
@@ -153,6 +153,38 @@ def test_static_entry_validates_on_the_host():
     assert B.workspace_bytes(B.JobArray(big)) > B.WS_STATIC_WORKSPACE_BYTES
     assert call(big) == B.WS_EWORKSPACE
     assert b"static workspace" in L.wait_sim_last_error()
+
+
+def test_checkpoint_entries_validate_on_the_host():
+    """The checkpoint entry points reject bad arguments before any device
+    call: NULL workspace or checkpoint buffers, a workspace smaller than the
+    jobs need, a save with neither a buffer nor a size out-parameter, an
+    invalid job."""
+    from paper_2504_11320_amd import binding as B
+    L = B.lib()
+    ja = B.JobArray(_job())
+    need = B.workspace_bytes(ja)
+    used = ctypes.c_size_t()
+    fake = ctypes.c_void_p(1 << 40)  # never dereferenced: the checks come first
+    assert L.wait_sim_save_state(ja.ptr, ja.n_jobs, None, need, None, 0, ctypes.byref(used),
+                                 None) == B.WS_EINVAL
+    assert L.wait_sim_save_state(ja.ptr, ja.n_jobs, fake, need - 1, None, 0,
+                                 ctypes.byref(used), None) == B.WS_EWORKSPACE
+    assert L.wait_sim_save_state(ja.ptr, ja.n_jobs, fake, need, None, 0, None,
+                                 None) == B.WS_EINVAL
+    assert L.wait_sim_load_state(ja.ptr, ja.n_jobs, fake, need, None, 0, None) == B.WS_EINVAL
+    assert L.wait_sim_load_state(ja.ptr, ja.n_jobs, None, need, fake, 1 << 20,
+                                 None) == B.WS_EINVAL
+    assert L.wait_sim_load_state(ja.ptr, ja.n_jobs, fake, need - 1, fake, 1 << 20,
+                                 None) == B.WS_EWORKSPACE
+    res, _ = B.results_bytes(ja)
+    assert L.wait_sim_run_batch_ex(ja.ptr, ja.n_jobs, 10, fake, need - 1, fake, res, None,
+                                   None, 0, None, 0, None) == B.WS_EWORKSPACE
+    assert L.wait_sim_run_batch_ex(ja.ptr, ja.n_jobs, -1, fake, need, fake, res, None,
+                                   None, 0, None, 0, None) == B.WS_EINVAL
+    bad = B.JobArray(_job(d0=0.0))
+    assert L.wait_sim_run_batch_ex(bad.ptr, bad.n_jobs, 10, fake, need, fake, res, None,
+                                   None, 0, None, 0, None) == B.WS_EINVAL
 
 
 def test_host_allocation_failure_is_an_error_code():
