@@ -48,7 +48,7 @@ class _Config(C.Structure):
         ("policy", C.c_int32), ("n", C.c_void_p), ("nseg", C.c_int32),
         ("seg_end", C.c_void_p), ("reserve", C.c_double),
         ("n_rate_pts", C.c_int32), ("rate_t", C.c_void_p), ("rate_f", C.c_void_p),
-        ("chunk", C.c_int32),
+        ("chunk", C.c_int32), ("stage_caps", C.c_void_p),
     ]
 
 
@@ -186,6 +186,8 @@ class _Pinned:
             c.seg_end, c.nseg = None, 0
         c.reserve = float(wl.reserve)
         c.chunk = int(getattr(wl, "chunk", 0) or 0)
+        caps = getattr(wl, "stage_caps", None)
+        c.stage_caps = None if caps is None else _ptr(arr(caps, np.int32))
         if getattr(wl, "rate_t", None) is not None:
             rt = arr(wl.rate_t, np.float64)
             rf = arr(np.asarray(wl.rate_f, dtype=np.float64).reshape(wl.m, len(rt)),

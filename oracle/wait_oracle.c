@@ -254,6 +254,7 @@ typedef struct {
   int64_t kb;   /* admission key: batch of last prefill          */
   int64_t kp;   /* admission key: position within that batch    */
   int64_t id;   /* request id (arrival order)                    */
+  int32_t cap_in; /* Nested: size of the cohort it entered its segment with */
 } req_t;
 
 typedef struct {
@@ -288,6 +289,7 @@ typedef struct {
   int64_t *tmp;
   int pre_launch;  /* evictions now are the pre-launch (Q+) repair's */
   int64_t mplus;   /* Nested: M_res(Q+) after the pre-launch repair   */
+  int64_t *nsvc;   /* Nested: services of segment k so far, k = 1..nseg */
 } sim_t;
 
 static int key_less(const req_t *x, const req_t *y) {
@@ -539,7 +541,10 @@ static void select_by_stage(sim_t *S, int64_t lo, int64_t hi, int32_t cap,
     int32_t s = S->R[S->tmp[i]].s;
     int64_t g = i;
     while (g < hi && S->R[S->tmp[g]].s == s) g++;
-    int64_t take = g - i < cap ? g - i : cap;
+    /* cap < 0 (Nested WAIT): a cell holds the cohort that entered the
+     * segment together, selected up to the size it entered with */
+    const int64_t lim = cap >= 0 ? cap : S->R[S->tmp[i]].cap_in;
+    int64_t take = g - i < lim ? g - i : lim;
     for (int64_t k = 0; k < take; k++) select_req(S, S->tmp[i + k], s, tokens);
     i = g;
   }
@@ -654,15 +659,28 @@ static int64_t projected_charge(const or_config *c, int64_t l, int32_t k,
 
 static void evict(sim_t *S, int64_t r, int fallback);
 
+/* Threshold of segment k (1-based) at its next service: n_k, or with
+ * per-stage caps (Section 6: the segment cap B_k spread over the segment's
+ * decode stages) the cap of the segment's stages taken in turn, the x-th
+ * service (x = 1, 2, ...) taking the cap of stage r_{k-1} + 1 + (x-1) mod
+ * (r_k - r_{k-1}).  The entering cohort has that size. */
+static int32_t entry_cap(const sim_t *S, int32_t k) {
+  const or_config *c = S->cfg;
+  if (!c->stage_caps) return c->n[k - 1];
+  const int32_t lo = seg_start(c, k);
+  const int32_t width = c->seg_end[k - 1] - lo;
+  return c->stage_caps[lo + (int32_t)(S->nsvc[k] % width)];
+}
+
 /* Algorithm 2 / Algorithm 4: largest prefix of segments whose entry queues
  * meet their thresholds; select up to n_k per cell of every prefix segment;
  * then evict unselected boundary prompts (LIFO) until the projected state
  * fits in C, falling back to unselected interior prompts. */
 static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   const or_config *c = S->cfg;
-  if (S->q[0].len < c->n[0]) return 0;
+  if (S->q[0].len < entry_cap(S, 1)) return 0;
   int32_t kmax = 1;
-  while (kmax < c->nseg && S->bnd[kmax + 1].len >= c->n[kmax]) kmax++;
+  while (kmax < c->nseg && S->bnd[kmax + 1].len >= entry_cap(S, kmax + 1)) kmax++;
 
   /* interior residents sorted by (segment, stage, key) */
   ensure_tmp(S, S->res.len);
@@ -673,7 +691,7 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   int64_t p = 0;
   int64_t i = 0;
   for (int32_t k = 1; k <= kmax; k++) {
-    int32_t nk = c->n[k - 1];
+    int32_t nk = entry_cap(S, k);
     if (k == 1) {
       for (int32_t x = 0; x < nk; x++) {
         int64_t r = dq_pop_front(&S->q[0]);
@@ -681,19 +699,22 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
         S->R[r].kp = p++;
         S->R[r].s = 0;
         S->R[r].seg = 1;
+        S->R[r].cap_in = nk;
         select_req(S, r, 0, tokens);
         *prefill_l += c->l[S->R[r].j];
       }
     } else {
       for (int32_t x = 0; x < nk; x++) {
         int64_t r = dq_at(&S->bnd[k], x);
+        S->R[r].cap_in = nk;
         select_req(S, r, seg_start(c, k) + 1, tokens);
       }
     }
     while (i < S->res.len && S->R[S->tmp[i]].seg < k) i++;
     int64_t lo = i;
     while (i < S->res.len && S->R[S->tmp[i]].seg == k) i++;
-    select_by_stage(S, lo, i, nk, tokens);
+    select_by_stage(S, lo, i, -1, tokens);
+    S->nsvc[k]++;
   }
 
   /* M_res(Q+) */
@@ -946,6 +967,8 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
   S.q = (dq_t *)calloc((size_t)S.nq, sizeof(dq_t));
   S.bnd = (dq_t *)calloc((size_t)(c->policy == OR_NESTED ? c->nseg + 2 : 1),
                          sizeof(dq_t));
+  S.nsvc = (int64_t *)calloc((size_t)(c->policy == OR_NESTED ? c->nseg + 2 : 1),
+                             sizeof(int64_t));
   S.t_next = (double *)calloc((size_t)c->m, sizeof(double));
   S.L_next = (int32_t *)calloc((size_t)c->m, sizeof(int32_t));
   S.k_next = (uint32_t *)calloc((size_t)c->m, sizeof(uint32_t));
@@ -1065,6 +1088,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
     for (int32_t k = 0; k < c->nseg + 2; k++) dq_free(&S.bnd[k]);
   free(S.q);
   free(S.bnd);
+  free(S.nsvc);
   free(S.res.v);
   free(S.sel.v);
   free(S.freelist.v);

@@ -47,6 +47,10 @@ class Workload:
     # linear through (rate_t[i], rate_f[j][i]) and constant outside
     rate_t: Optional[np.ndarray] = None      # f64 [P], strictly increasing
     rate_f: Optional[np.ndarray] = None      # f64 [m, P], >= 0
+    # Nested WAIT per-stage caps: cap of decode stage s at index s - 1
+    # (seg_end[-1] entries); segment k's caps are taken in turn, one per
+    # service, as the size of its entering cohort; n[k] is the largest
+    stage_caps: Optional[List[int]] = None
 
     @property
     def m(self) -> int:
@@ -259,6 +263,38 @@ def config_p512d20(replicas: int = 2048, record_capacity: int = 1 << 16) -> List
     return jobs
 
 
+# ------------------------------- two-type p512 mix under per-stage caps ----
+
+# The paper's two-type workload (0.7 p512d20, 0.3 p512d50; prompt 512, outputs
+# 20 or 50) under Nested WAIT with segments 1-20 and 21-50 and the per-stage
+# caps that the batch-size cap tl = 30 gives (Section 6): continuation ratio
+# 0.3, n_1 = 30 / (20 + 30 * 0.3), segment caps round(20 n_1) = 21 and
+# round(9.31) = 9, spread as evenly as possible over the segments' 20 and 30
+# decode stages (the first stages take one more).  A CPU test recomputes
+# these caps from tl.  Time model and budget as p512d20.
+P512MIX_SEG_END = [20, 50]
+P512MIX_CAPS_TL30 = [2] + [1] * 19 + [1] * 9 + [0] * 21
+P512MIX_RATES = [0.014, 0.018, 0.022]     # per ms
+
+
+def config_p512_mix(replicas: int = 1024, rates=None, stage_caps=None,
+                    record_capacity: int = 1 << 14) -> List[Job]:
+    """The two-type p512 mix (outputs 20 or 50, unknown to the scheduler)
+    under Nested WAIT with per-stage caps (default: those of tl = 30), one job
+    per rate."""
+    caps = list(P512MIX_CAPS_TL30 if stage_caps is None else stage_caps)
+    cdf = _cdf_table([0.0] * 19 + [0.7] * 30)[None, :]
+    n = [max(caps[:P512MIX_SEG_END[0]]), max(caps[P512MIX_SEG_END[0]:])]
+    jobs = []
+    for lam in (P512MIX_RATES if rates is None else rates):
+        wl = Workload(prompt_len=[512], lam=[lam], d0=10.0, d1=P512_D1, C=137000,
+                      policy="nested", n=n, out_cap=50, out_cdf=cdf,
+                      seg_end=list(P512MIX_SEG_END), hist_edges=default_edges(10.0),
+                      record_capacity=record_capacity, stage_caps=caps)
+        jobs.append(Job(wl, 0, ids(replicas)))
+    return jobs
+
+
 # ------------------------------------- decode-only (PD-disaggregated) ----
 
 # A decode server behind a separate prefill service receives each request with
@@ -334,7 +370,7 @@ def config_cyclic(replicas: int = 1024, n_rates: int = 32, rate_index=None,
 
 def trace_workload(policy: str, prompt_len, out_len, d0, d1, C, n, times, types,
                    lengths=None, seg_end=None, reserve=0.0, out_cap=0,
-                   record_capacity=1 << 12) -> Workload:
+                   record_capacity=1 << 12, stage_caps=None) -> Workload:
     """Workload whose arrivals are the given (time, type[, length]) list."""
     times = np.asarray(times, dtype=np.float64)
     types = np.asarray(types, dtype=np.int32)
@@ -347,4 +383,5 @@ def trace_workload(policy: str, prompt_len, out_len, d0, d1, C, n, times, types,
                     out_cap=out_cap, seg_end=seg_end, reserve=reserve,
                     hist_edges=default_edges(d0, 64),
                     record_capacity=record_capacity,
-                    trace=(times, types, lengths))
+                    trace=(times, types, lengths),
+                    stage_caps=None if stage_caps is None else list(stage_caps))
