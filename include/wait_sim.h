@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define WS_ABI_VERSION 3
+#define WS_ABI_VERSION 4
 
 typedef enum {
   WS_OK = 0,
@@ -161,6 +161,17 @@ typedef struct {
                             it; a partial prompt holds its cached tokens, is
                             evicted first and restarts.  0: whole prefills.
                             Must be 0 for the other policies.             */
+  const int32_t *stage_caps; /* NESTED, optional: per-stage caps (Section 6,
+                            the batch-size cap tl spread over segments and
+                            their decode stages).  stage_caps[s-1] >= 0 is
+                            the cap of decode stage s = 1..r_L; segment k
+                            takes the caps of its stages r_{k-1}+1..r_k in
+                            turn, one per service, as its threshold and the
+                            size of the cohort it admits; n[k] must be the
+                            largest cap of segment k and segment 1's caps
+                            must be >= 1.  NULL: every service of segment k
+                            admits n_k.  Must be NULL for the other
+                            policies.                                     */
 } ws_policy;
 
 /* One replica's random stream. */

@@ -23,7 +23,7 @@ WS_EINTERNAL = -6
 WS_STATIC_WORKSPACE_BYTES = 64 << 20
 WS_WAIT, WS_NESTED_WAIT, WS_FCFS, WS_WAIT_NOWAIT = 0, 1, 2, 3
 WS_FLAG_CAPACITY, WS_FLAG_STALL, WS_FLAG_OVERFLOW, WS_FLAG_THIN_LIMIT = 1, 2, 4, 8
-WS_ABI_VERSION = 3
+WS_ABI_VERSION = 4
 WS_NI64, WS_NF64 = 12, 6
 POLICY = {"wait": WS_WAIT, "nested": WS_NESTED_WAIT, "fcfs": WS_FCFS,
           "wait-nowait": WS_WAIT_NOWAIT}
@@ -59,7 +59,7 @@ class WsConfig(C.Structure):
 class WsPolicy(C.Structure):
     _fields_ = [("kind", C.c_int32), ("n", C.c_void_p), ("L", C.c_int32),
                 ("seg_end", C.c_void_p), ("fcfs_reserve", C.c_double),
-                ("fcfs_chunk", C.c_int32)]
+                ("fcfs_chunk", C.c_int32), ("stage_caps", C.c_void_p)]
 
 
 class WsStream(C.Structure):
@@ -179,6 +179,8 @@ class JobArray:
             pol.seg_end = None if wl.seg_end is None else self._a(wl.seg_end, np.int32)
             pol.fcfs_reserve = float(wl.reserve)
             pol.fcfs_chunk = int(getattr(wl, "chunk", 0) or 0)
+            caps = getattr(wl, "stage_caps", None)
+            pol.stage_caps = None if caps is None else self._a(caps, np.int32)
             ids = np.asarray(job.replica_ids, dtype=np.uint32)
             st = (WsStream * max(1, len(ids)))()
             for x, rid in enumerate(ids):

@@ -51,6 +51,8 @@ struct JobDev {
   uint64_t off_rec[kMaxSeg];    // Nested: interior records [delta][n]
   uint64_t off_bkt[kMaxSeg];    // Nested: calendar bucket heads [delta]
   uint64_t off_v[kMaxSeg];      // Nested: boundary-queue rings (k >= 1)
+  uint64_t off_caps;            // Nested per-stage caps: int32 [r_L]
+  int32_t has_caps, pad2_;
 };
 
 // Per-replica state slots (8 bytes each), stored [slot][R].
@@ -90,6 +92,7 @@ struct KArgs {
   int32_t any_tv;      // some job of this launch has time-varying rates
   int32_t lanes;       // replicas per wavefront (lanes >= this are padding)
   int32_t unit_n;      // WAIT launch whose jobs all have thresholds n_j = 1
+  int32_t any_caps;    // some Nested WAIT job of this launch has per-stage caps
   uint8_t *btrace;     // per-batch trace [R][btrace_cap] records, or null
   int64_t btrace_cap;
 };

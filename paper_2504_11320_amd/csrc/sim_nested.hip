@@ -5,7 +5,9 @@
 namespace wsim {
 
 hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s) {
-  if (A.any_tv || A.btrace != nullptr) return launch_nested_tv(max_m, max_seg, A, s);
+  // time-varying rates, per-batch traces and per-stage caps run in the
+  // general instantiation
+  if (A.any_tv || A.btrace != nullptr || A.any_caps) return launch_nested_tv(max_m, max_seg, A, s);
   return launch_nested_k<false>(max_m, max_seg, A, s);
 }
 

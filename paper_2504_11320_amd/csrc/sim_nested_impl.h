@@ -304,6 +304,17 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   const int k = gl;
   const SegConst sc = s_seg[gl];
   const int32_t rk = sc.end, nk = sc.n, delta = sc.delta, ent = sc.entry;
+  // per-stage caps (Section 6; general instantiation only): the segment's
+  // services take the caps of its decode stages r_{k-1}+1..r_k in turn as
+  // the size of the entering cohort; n_k, the largest, is the row width of
+  // the cohort slots
+  const bool capped = TV && J.has_caps != 0;
+  const int32_t nrow = nk;
+  const int32_t clo = k >= 1 ? ent - 1 : 0;  // r_{k-1}
+  const int32_t *capt = (const int32_t *)(A.ws + J.off_caps);
+  auto cap_at = [&](uint32_t services) __attribute__((always_inline)) -> int32_t {
+    return capped && is_s ? capt[clo + (int32_t)(services % (uint32_t)(rk - clo))] : nk;
+  };
   const int32_t rprev = k >= 1 ? ent - 1 : 0;  // r_{k-1}
   const uint64_t dmg = sc.dmagic;
   NRec *rc = (NRec *)(blk + sc.off_rec);
@@ -374,6 +385,13 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       for (int x = gl; x < s_seg[kk].delta; x += G) b[x] = kNil;
     }
     for (int b = gl; b < A.hist_stride; b += G) hist[b] = 0;  // whole row, padding included
+    if (capped) {  // a cohort smaller than the row leaves records unwritten: none is live
+      for (int kk = 0; kk < L; ++kk) {
+        NRec *rr = (NRec *)(blk + s_seg[kk].off_rec);
+        const int cells = s_seg[kk].delta * s_seg[kk].n;
+        for (int x = gl; x < cells; x += G) rr[x].L = 0;
+      }
+    }
   } else {
     t = slot_f(A, S_T, r);
     lat_area = slot_f(A, S_LAT, r);
@@ -414,6 +432,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
   }
   gend = kj + 1u;  // draw rings start empty
+  // size of the cohort this segment admits at its next service
+  int32_t ncap = cap_at(svc);
   // youngest live interior record of this segment and its index (kNil: not
   // known, found by a scan when next needed); ydead: the index of the last
   // youngest that left (every record entered after it has left too, so the
@@ -543,18 +563,18 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     // start just below the youngest that left last (its cohort entered at
     // service yi.c, no later cohort has entered since: an entering cohort
     // sets the cache), else at the newest cohort slot
-    int32_t back = 0, ifrom = nk - 1;
+    int32_t back = 0, ifrom = nrow - 1;
     if (ydead != kNil) {
       const uint32_t c0 = yi.c;
       back = (int32_t)(svc - c0);
-      ifrom = (int32_t)(ydead - fastmod(c0, dmg, (uint32_t)delta) * (uint32_t)nk) - 1;
-      ifrom = ifrom < nk - 1 ? ifrom : nk - 1;  // indices stay inside the cohort slot
+      ifrom = (int32_t)(ydead - fastmod(c0, dmg, (uint32_t)delta) * (uint32_t)nrow) - 1;
+      ifrom = ifrom < nrow - 1 ? ifrom : nrow - 1;  // indices stay inside the cohort slot
     }
-    for (; back < delta && (int64_t)svc - back >= 1; ++back, ifrom = nk - 1) {
+    for (; back < delta && (int64_t)svc - back >= 1; ++back, ifrom = nrow - 1) {
       const uint32_t slot = fastmod(svc - (uint32_t)back, dmg, (uint32_t)delta);
       // a record with L = 0 has left the segment (exit or eviction)
       for (int32_t i = ifrom; i >= 0; --i) {
-        const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
+        const uint32_t idx = slot * (uint32_t)nrow + (uint32_t)i;
         const NRec rec = load_nrec(rc + idx);
         if (rec.L != 0) {
           yi = rec;
@@ -660,12 +680,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   auto prefetch = [&]() __attribute__((always_inline)) {
     pf_q0_ok = qt != qh;
     if (gl == 0 && pf_q0_ok) pf_q0 = ((const uint4 *)q10)[qh & qmask];
-    if (is_s && (k == 0 || (int32_t)(s_vt[k][q] - s_vh[k][q]) >= nk)) {
+    if (is_s && (k == 0 || (int32_t)(s_vt[k][q] - s_vh[k][q]) >= ncap)) {
       const uint32_t x = svc + 1u;  // the segment's next service
       bh = bk[fastmod(x, dmg, (uint32_t)delta)];
       if (k >= 1) pf_vf = load_nrec(vr + (s_vh[k][q] & vmask));
       pf_ti = kNil;
-      if (nk == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1) {
+      if (nrow == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1) {
         pf_ti = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
         pf_tr = *(const uint2 *)((const uint8_t *)(rc + pf_ti) + 16);
       }
@@ -720,8 +740,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         stopped = true;
         break;
       }
-      const bool ok = gl == 0 ? (int64_t)(qt - qh) >= n0
-                              : (is_s && (int32_t)(s_vt[k][q] - s_vh[k][q]) >= nk);
+      const bool ok = gl == 0 ? (int64_t)(qt - qh) >= (capped ? ncap : n0)
+                              : (is_s && (int32_t)(s_vt[k][q] - s_vh[k][q]) >= ncap);
       const uint32_t okb = group_bits<G>(ok);
       if (okb & 1u) {
         kmax = __builtin_ctz(~okb);  // lanes >= L never meet it
@@ -766,15 +786,17 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     uint32_t pend_idx = kNil;
     const uint32_t bh0 = bh;
     NRec crec0 = yi;
-    const bool pre_ok = served && nk == 1 && bh0 != kNil;
+    const bool pre_ok = served && nrow == 1 && bh0 != kNil;
+    // prompts entering segment 1 now (the cap of its service)
+    const int32_t n0c = capped ? __shfl(ncap, 0, G) : n0;
     if (pre_ok) crec0 = load_nrec(rc + bh0);
     if (served) {
       const uint32_t slot = fastmod(x, dmg, (uint32_t)delta);
       tok = M;  // every interior prompt is processed at its stage
-      sel = (int64_t)I + nk;
+      sel = (int64_t)I + ncap;
       uint32_t suml = 0;
       // link in reverse selection order: traversal is then in key order
-      for (int32_t i = nk - 1; i >= 0; --i) {
+      for (int32_t i = ncap - 1; i >= 0; --i) {
         NRec e;
         if (k == 0) {
           QRec qr;
@@ -797,18 +819,18 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
         const uint32_t b = fastmod(x + (uint32_t)(pexit - ent), dmg, (uint32_t)delta);
-        const uint32_t idx = slot * (uint32_t)nk + (uint32_t)i;
+        const uint32_t idx = slot * (uint32_t)nrow + (uint32_t)i;
         // (the bucket served now was prefetched as bh: the same head)
         e.next = b == slot ? bh : bk[b];
         bk[b] = idx;
         if (b == slot) bh = idx;  // exits at this very service: heads the bucket served now
-        if (nk == 1) {
+        if (nrow == 1) {
           pend = e;
           pend_idx = idx;
         } else {
           rc[idx] = e;
         }
-        if (i == nk - 1) {  // the cohort's last record is the segment's youngest
+        if (i == ncap - 1) {  // the cohort's last record is the segment's youngest
           yi = e;
           yidx = idx;
         }
@@ -821,21 +843,21 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           eM += le + ent + 1;
         }
       }
-      if (k > 0) s_vh[k][q] += (uint32_t)nk;  // still charged in s_B until the completion
+      if (k > 0) s_vh[k][q] += (uint32_t)ncap;  // still charged in s_B until the completion
       // projected change of the segment's memory (no early completion)
       if (delta >= 2) {
         uint32_t T = 0, Tl = 0;
         if ((int64_t)x - (delta - 1) >= 1) {
           // the terminal cohort slot: its prompts still in the segment
-          if (nk == 1) {  // prefetched
+          if (nrow == 1) {  // prefetched
             const int32_t trL = (int32_t)pf_tr.y, trj = (int32_t)pf_tr.x;
             T = trL != 0 ? 1u : 0u;
             Tl = trL != 0 ? (uint32_t)s_l[trj] : 0u;
           } else {
             const uint32_t ts = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
-            for (int32_t i = 0; i < nk; ++i) {
+            for (int32_t i = 0; i < nrow; ++i) {
               // j and L (the second half's first two words) in one load
-              const uint2 jl = *(const uint2 *)((const uint8_t *)(rc + ts * (uint32_t)nk +
+              const uint2 jl = *(const uint2 *)((const uint8_t *)(rc + ts * (uint32_t)nrow +
                                                                   (uint32_t)i) + 16);
               const bool live = (int32_t)jl.y != 0;
               T += live ? 1u : 0u;
@@ -846,14 +868,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         dplus = (int32_t)I - (int32_t)T;
         if (k == L - 1) dplus -= (int32_t)Tl + (int32_t)T * rk;
         if (k == 0)
-          dplus += (int32_t)suml + nk;  // prefills land at stage 1
+          dplus += (int32_t)suml + ncap;  // prefills land at stage 1
         else
-          dplus += 2 * nk;              // l + r_{k-1} -> l + r_{k-1} + 2
+          dplus += 2 * ncap;            // l + r_{k-1} -> l + r_{k-1} + 2
       } else {                          // entering prompts are processed at r_k
         if (k < L - 1)
-          dplus = nk;                   // l + r_{k-1} -> l + r_k
+          dplus = ncap;                 // l + r_{k-1} -> l + r_k
         else
-          dplus = -((int32_t)suml + nk * rprev);
+          dplus = -((int32_t)suml + ncap * rprev);
       }
     }
     const int64_t tokens = group_sum<G>(tok);
@@ -862,7 +884,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     int64_t mplus = Mres + group_sum32<G>(dplus);
     int64_t bt_sel = 0;
     if constexpr (TV) bt_sel = group_sum<G>(sel);
-    qh += (uint32_t)n0;
+    qh += (uint32_t)n0c;
     const int64_t bt_ev0 = evicts;
     wave_lds_sync();
 
@@ -916,6 +938,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     if (pend_idx != kNil) rc[pend_idx] = pend;  // the entering record (n_k = 1)
     if (served) {
       svc = x;
+      if (capped) ncap = cap_at(svc);  // the cap of the next service
       Mk = M + (int64_t)I + eM;  // every interior prompt advances
       Ik = I + eI;
       if (k > 0) {  // entering prompts leave the boundary queue's charge
@@ -942,7 +965,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     // a bucket lists at most the segment's delta_k * n_k records: a longer
     // walk could only follow a corrupted link, so it stops the replica
     uint32_t steps = 0;
-    const uint32_t max_steps = (uint32_t)delta * (uint32_t)nk;
+    const uint32_t max_steps = (uint32_t)delta * (uint32_t)nrow;
     for (;;) {
       while (node != kNil && nbuf < KL) {
         if (++steps > max_steps) {
@@ -1042,7 +1065,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           br.t_launch = t_end - tau;
           br.tau = tau;
           br.tokens = tokens;
-          br.prefills = n0;
+          br.prefills = n0c;
           br.selected = bt_sel;
           br.completions = comps - bt_comps0;
           br.evict_pre = bt_ev1 - bt_ev0;

@@ -253,7 +253,7 @@ uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 struct JobHost {
   JobDev d;
   int64_t reserve_tok;
-  uint64_t edges_bytes, cdf_bytes, trace_bytes, rate_bytes;
+  uint64_t edges_bytes, cdf_bytes, trace_bytes, rate_bytes, caps_bytes;
 };
 
 struct Layout {
@@ -373,6 +373,8 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   int64_t reserve_tok = 0;
   if (kind != WS_FCFS && p.fcfs_chunk != 0)
     return fail_job(WS_EINVAL, idx, "fcfs_chunk applies to FCFS only");
+  if (kind != WS_NESTED_WAIT && p.stage_caps)
+    return fail_job(WS_EINVAL, idx, "stage_caps apply to Nested WAIT only");
   if (kind == WS_WAIT) {
     if (!known) return fail_job(WS_EINVAL, idx, "WAIT needs known output lengths");
     if (!p.n) return fail_job(WS_EINVAL, idx, "thresholds required");
@@ -402,6 +404,19 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
     if (p.seg_end[p.L - 1] != maxL)
       return fail_job(WS_EINVAL, idx, "last segment must end at the largest output length");
+    if (p.stage_caps) {  // per-stage caps: n_k is the largest of segment k's
+      for (int k = 0; k < p.L; ++k) {
+        int32_t mx = 0;
+        for (int32_t st = k == 0 ? 0 : p.seg_end[k - 1]; st < p.seg_end[k]; ++st) {
+          const int32_t cp = p.stage_caps[st];
+          if (cp < 0 || (k == 0 && cp < 1))
+            return fail_job(WS_EINVAL, idx, "stage caps must be >= 0, and >= 1 in segment 1");
+          mx = std::max(mx, cp);
+        }
+        if (mx != p.n[k])
+          return fail_job(WS_EINVAL, idx, "n[k] must be the largest stage cap of segment k");
+      }
+    }
   } else {
     return fail_job(WS_EINVAL, idx, "unknown policy kind");
   }
@@ -468,6 +483,8 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
                     : 0;
   H.trace_bytes = c.n_trace > 0 ? align_up(16ull * (uint64_t)c.n_trace, 256) : 0;
   H.rate_bytes = align_up(8ull * (uint64_t)c.n_rate_pts * (uint64_t)(c.m + 1), 256);
+  H.caps_bytes = p.stage_caps ? align_up(4ull * (uint64_t)maxL, 256) : 0;
+  d.has_caps = p.stage_caps ? 1 : 0;
   // ring block of one replica
   uint64_t off = 0;
   const uint64_t qrec = (kind == WS_WAIT) ? 8 : 16;
@@ -589,6 +606,8 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
     off += H.trace_bytes;
     H.d.off_rate = off;
     off += H.rate_bytes;
+    H.d.off_caps = off;
+    off += H.caps_bytes;
   }
   off = align_up(off, 256);
   Lo.off_state = off;
@@ -708,6 +727,8 @@ void build_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *
       std::memcpy(img + d.off_tr_type, c.trace_type, 4ull * c.n_trace);
       if (c.trace_out_len) std::memcpy(img + d.off_tr_len, c.trace_out_len, 4ull * c.n_trace);
     }
+    if (Lo.jobs[i].caps_bytes)
+      std::memcpy(img + d.off_caps, jb.pol->stage_caps, 4ull * (uint64_t)d.seg_end[d.nseg - 1]);
     if (c.n_rate_pts > 0) {  // rate_t [P], then rate_f [m][P]
       std::memcpy(img + d.off_rate, c.rate_t, 8ull * c.n_rate_pts);
       std::memcpy(img + d.off_rate + 8ull * c.n_rate_pts, c.rate_f, 8ull * c.n_rate_pts * c.m);
@@ -796,12 +817,13 @@ int advance_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, int64_t h
     B.off_list = Lo.list_off[pk];
     B.n_list = Lo.list_count[pk];
     B.lanes = Lo.lanes[pk];
-    B.any_trace = B.any_tv = 0;
+    B.any_trace = B.any_tv = B.any_caps = 0;
     B.unit_n = pk == WS_WAIT ? 1 : 0;
     for (int i = 0; i < n_jobs; ++i) {
       if (launch_kind(jobs[i].pol) != pk) continue;
       if (jobs[i].cfg->n_trace > 0) B.any_trace = 1;
       if (jobs[i].cfg->n_rate_pts > 0) B.any_tv = 1;
+      if (jobs[i].pol->stage_caps) B.any_caps = 1;
       if (pk == WS_WAIT)
         for (int j = 0; j < jobs[i].cfg->m; ++j)
           if (jobs[i].pol->n[j] != 1) B.unit_n = 0;

@@ -25,7 +25,7 @@ def test_library_exports_header_symbols():
     assert "wait_sim_run" in names and "wait_sim_advance" in names
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.wait_sim_abi_version() == B.WS_ABI_VERSION == 3
+    assert lib.wait_sim_abi_version() == B.WS_ABI_VERSION == 4
 
 
 def _err(jobs):
@@ -185,6 +185,31 @@ def test_checkpoint_entries_validate_on_the_host():
     bad = B.JobArray(_job(d0=0.0))
     assert L.wait_sim_run_batch_ex(bad.ptr, bad.n_jobs, 10, fake, need, fake, res, None,
                                    None, 0, None, 0, None) == B.WS_EINVAL
+
+
+def test_stage_caps_validation():
+    """Per-stage caps: Nested WAIT only, >= 0, >= 1 in segment 1, and n[k]
+    the largest cap of segment k."""
+    from paper_2504_11320_amd import binding as B
+    base = W.config_p512_mix(replicas=2, rates=[0.02])
+    ja = B.JobArray(base)
+    assert B.workspace_bytes(ja) > 0
+
+    def with_caps(caps, n=None, policy="nested"):
+        j = base[0]
+        wl = W.Workload(**{**j.wl.__dict__, "stage_caps": caps})
+        if n is not None:
+            wl.n = n
+        if policy != "nested":
+            wl = W.config2(replicas=2, rate_index=[3])[0].wl
+            wl.stage_caps = caps
+        return [W.Job(wl, 0, W.ids(2))]
+
+    caps = list(W.P512MIX_CAPS_TL30)
+    assert _err(with_caps(caps[:20] + [-1] + caps[21:])).code == B.WS_EINVAL
+    assert _err(with_caps([0] + caps[1:])).code == B.WS_EINVAL  # segment 1 needs >= 1
+    assert _err(with_caps(caps, n=[1, 1])).code == B.WS_EINVAL  # n_1 is not the largest
+    assert _err(with_caps(caps, policy="wait")).code == B.WS_EINVAL
 
 
 def test_host_allocation_failure_is_an_error_code():
