@@ -92,6 +92,10 @@ __device__ __forceinline__ NRec load_nrec(const NRec *p) {
 __device__ __forceinline__ uint64_t nrec_key(const NRec &r) {
   return ((uint64_t)r.kb << 32) | r.kp;
 }
+// A record's type word carries the prompt length with the type, so the
+// charges a record implies need no table lookup: (l << 8) | type.
+__device__ __forceinline__ int32_t type_word(int32_t l, int32_t j) { return (l << 8) | j; }
+__device__ __forceinline__ int32_t plen(int32_t jw) { return jw >> 8; }
 
 // ---------------------------------------------------------- group lanes --
 // DPP lane permutations inside 16-lane rows (gfx9 encodings): swap neighbours
@@ -171,7 +175,7 @@ __device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)
 // G: lanes per replica (types and segments per group); TV: jobs with
 // time-varying rates are supported (compiled out of the common kernels).
 template <int G, bool TV>
-__global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) sim_nested_kernel(KArgs A) {
   constexpr int NR = 64 / G;  // replicas per wavefront
   constexpr int MT = G;       // type slots
   constexpr int LT = G;       // segment slots
@@ -295,11 +299,13 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   const uint32_t qmask = (1u << J.qcap_log2) - 1u;
   const uint32_t rec_cap = (uint32_t)J.rec_cap;
   uint8_t *blk = A.ws + J.off_ring + (uint64_t)(r - J.replica_begin) * J.ring_stride;
-  QRec *q10 = (QRec *)(blk + J.off_q[0]);
+  const uint32_t o_q10 = (uint32_t)J.off_q[0];
+#define q10 ((QRec *)(blk + opaque(o_q10)))
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
 
   // this lane's type and segment
   const bool is_t = gl < m;
+  const int32_t tword = is_t ? type_word(J.l[gl], gl) : 0;  // this lane's type
   const bool is_s = gl < L;
   const int k = gl;
   const SegConst sc = s_seg[gl];
@@ -317,16 +323,18 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   };
   const int32_t rprev = k >= 1 ? ent - 1 : 0;  // r_{k-1}
   const uint64_t dmg = sc.dmagic;
-  NRec *rc = (NRec *)(blk + sc.off_rec);
-  uint32_t *bk = (uint32_t *)(blk + sc.off_bkt);
-  NRec *vr = (NRec *)(blk + sc.off_v);
+  const uint32_t o_rc = sc.off_rec, o_bk = sc.off_bkt, o_vr = sc.off_v;
+#define rc ((NRec *)(blk + opaque(o_rc)))
+#define bk ((uint32_t *)(blk + opaque(o_bk)))
+#define vr ((NRec *)(blk + opaque(o_vr)))
   const uint32_t vmask = sc.vmask;
   const int32_t n0 = s_seg[0].n;
   // the next segment (survivors of this one join its boundary queue)
   const bool has_next = is_s && k + 1 < L;
   const int kn = has_next ? k + 1 : gl;
   const SegConst scn = s_seg[kn];
-  NRec *vrn = (NRec *)(blk + scn.off_v);
+  const uint32_t o_vrn = scn.off_v;
+#define vrn ((NRec *)(blk + opaque(o_vrn)))
   const uint32_t vmaskn = scn.vmask;
 
   auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
@@ -340,8 +348,9 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
   // replica-wide scalars, identical in every lane of the group (lat_sum:
   // group lane 0 only)
   double t, lat_area, ttft_area, lat_sum, mem_area, busy;
-  int64_t batches, arrivals, comps, ctok, evicts, etok, fallback, btok, peak, idle, N, U,
-      Mres, tridx, pendft;
+  int64_t batches, arrivals, comps, ctok, evicts, etok, fallback, btok, peak, idle, Mres, tridx;
+  // requests in the system and without a first token (bounded by the rings)
+  int32_t N, U, pendft;
   uint32_t flags, qh, qt;
   // type lane: next arrival time, its counter and output length, ring end
   double tn = INFINITY;
@@ -409,11 +418,11 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     btok = slot_i(A, S_BTOK, r);
     peak = slot_i(A, S_PEAK, r);
     idle = slot_i(A, S_IDLE, r);
-    N = slot_i(A, S_N, r);
-    U = slot_i(A, S_U, r);
+    N = (int32_t)slot_i(A, S_N, r);
+    U = (int32_t)slot_i(A, S_U, r);
     Mres = slot_i(A, S_MRES, r);
     tridx = slot_i(A, S_TRIDX, r);
-    pendft = slot_i(A, S_PENDFT, r);
+    pendft = (int32_t)slot_i(A, S_PENDFT, r);
     flags = (uint32_t)slot_i(A, S_FLAGS, r);
     qh = (uint32_t)slot_i(A, S_QH, r);
     qt = (uint32_t)slot_i(A, S_QT, r);
@@ -461,6 +470,14 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
 
   // ---- arrivals --------------------------------------------------------------
   // The group's next arrival: its time, and its type (ties: the lowest type).
+  double tmin = INFINITY;
+  int jmin = 0;
+  auto next_arrival = [&]() __attribute__((always_inline)) {
+    const double v = is_t ? tn : INFINITY;
+    tmin = group_min<G>(v);
+    const uint32_t b = group_bits<G>(is_t && v == tmin);
+    jmin = b != 0 ? __builtin_ctz(b) : 0;
+  };
   auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
     if (trace) {
       if (tridx >= J.n_trace) {
@@ -470,11 +487,8 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       jn = tr_type[tridx];
       return tr_time[tridx];
     }
-    const double v = is_t ? tn : INFINITY;
-    const double mn = group_min<G>(v);
-    const uint32_t b = group_bits<G>(is_t && v == mn);
-    jn = b != 0 ? __builtin_ctz(b) : 0;
-    return mn;
+    jn = jmin;
+    return tmin;
   };
 
   // Append a record to Q_{1,0}: the counters in every lane, the record by the
@@ -546,11 +560,13 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         }
       }
       if constexpr (TV) flags = group_or<G>(flags);  // thinning limit
+      next_arrival();
     }
     arrivals++;
     N++;
     U++;
-    push_q10(writer, a, jn, Lr);
+    // the writer's type word: its own type's (non-trace), or a lookup (trace)
+    push_q10(writer, a, trace ? type_word(s_l[jn], jn) : tword, Lr);
   };
 
   // ---- evictions -------------------------------------------------------------
@@ -607,7 +623,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
         // charge l + r_{h-1} from LDS
         const NRec rec = s_vb[h][q];
         const int64_t gen = s_seg[h].entry - 1;
-        const int64_t ch = (int64_t)s_l[rec.j] + gen;
+        const int64_t ch = (int64_t)plen(rec.j) + gen;
         wave_lds_sync();
         if (me) {
           const uint32_t vt = s_vt[k][q] - 1u;
@@ -643,7 +659,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
       yidx = kNil;
       ydead = idx;
       const int32_t stage = ent + (int32_t)(svc - rec.c) + 1;
-      ch = s_l[rec.j] + stage;
+      ch = plen(rec.j) + stage;
       gen = stage - 1;
       NRec hole = rec;
       hole.L = 0;  // leaves a hole; the calendar skips it
@@ -692,6 +708,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
     }
   };
   bool stopped = (flags & (kFlagCap | kFlagStall)) != 0;
+  if (!trace) next_arrival();
   if (!stopped) prefetch();
 
   for (int64_t it = 0; it < A.horizon && !stopped; ++it) {
@@ -809,12 +826,12 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           e.L = qr.L;
           e.kb = bidx;
           e.kp = (uint32_t)i;
-          tok += s_l[qr.j];
-          pre_l += s_l[qr.j];
+          tok += plen(qr.j);
+          pre_l += plen(qr.j);
           if (!has_ft(qr.a_ft)) pend_new++;
         } else {
           e = i == 0 ? pf_vf : load_nrec(vr + ((s_vh[k][q] + (uint32_t)i) & vmask));
-          tok += (int64_t)s_l[e.j] + ent;  // processed at stage r_{k-1} + 1
+          tok += (int64_t)plen(e.j) + ent;  // processed at stage r_{k-1} + 1
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
@@ -834,7 +851,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           yi = e;
           yidx = idx;
         }
-        const int32_t le = s_l[e.j];
+        const int32_t le = plen(e.j);
         suml += (uint32_t)le;
         // what the completion step does with the entering prompts
         if (k > 0) eB += le + rprev;
@@ -852,7 +869,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
           if (nrow == 1) {  // prefetched
             const int32_t trL = (int32_t)pf_tr.y, trj = (int32_t)pf_tr.x;
             T = trL != 0 ? 1u : 0u;
-            Tl = trL != 0 ? (uint32_t)s_l[trj] : 0u;
+            Tl = trL != 0 ? (uint32_t)plen(trj) : 0u;
           } else {
             const uint32_t ts = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
             for (int32_t i = 0; i < nrow; ++i) {
@@ -861,7 +878,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
                                                                   (uint32_t)i) + 16);
               const bool live = (int32_t)jl.y != 0;
               T += live ? 1u : 0u;
-              Tl += live ? (uint32_t)s_l[(int32_t)jl.x] : 0u;
+              Tl += live ? (uint32_t)plen((int32_t)jl.x) : 0u;
             }
           }
         }
@@ -986,7 +1003,7 @@ __global__ void __launch_bounds__(64) sim_nested_kernel(KArgs A) {
             ydead = node;
             yidx = kNil;
           }
-          const int64_t le = s_l[rec.j];
+          const int64_t le = plen(rec.j);
           const int32_t p = rec.L < rk ? rec.L : rk;
           if (rec.c != x) {  // an interior prompt: it had advanced to p + 1
             Mk -= le + p + 1;

@@ -404,6 +404,9 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
     if (p.seg_end[p.L - 1] != maxL)
       return fail_job(WS_EINVAL, idx, "last segment must end at the largest output length");
+    for (int j = 0; j < c.m; ++j)  // records carry the prompt length in 24 bits
+      if (c.prompt_len[j] >= (1 << 23))
+        return fail_job(WS_EUNSUPPORTED, idx, "Nested WAIT prompt lengths must stay below 2^23");
     if (p.stage_caps) {  // per-stage caps: n_k is the largest of segment k's
       for (int k = 0; k < p.L; ++k) {
         int32_t mx = 0;
