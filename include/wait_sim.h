@@ -93,8 +93,11 @@ typedef enum {
 } ws_policy_kind;
 
 /* Per-replica flags (result field "flags"). */
-#define WS_FLAG_CAPACITY 1u /* an external queue exceeded record_capacity;
-                               the replica stopped at its next decision     */
+#define WS_FLAG_CAPACITY 1u /* an external queue exceeded record_capacity
+                               (FCFS with drawn lengths: also its resident
+                               ring, which holds record_capacity entries,
+                               or 2^31 - 2^24 batches reached); the replica
+                               stopped at its next decision                 */
 #define WS_FLAG_STALL 2u    /* nothing eligible and no further arrival       */
 #define WS_FLAG_OVERFLOW 4u /* Nested WAIT launched with a projected state
                                above C after every allowed eviction          */
@@ -117,7 +120,12 @@ typedef struct {
   const int32_t *prompt_len;    /* l_j >= 1                         [m]      */
   const double *lambda;         /* lambda_j >= 0, per ms            [m]      */
   const int32_t *out_len;       /* known output length l'_j >= 1    [m], or
-                                   NULL for the distribution mode below      */
+                                   NULL for the distribution mode below (the
+                                   unknown-length model of Section 5.1: each
+                                   request's length drawn at arrival, never
+                                   read by the scheduler; Nested WAIT, and
+                                   FCFS without chunked prefill and with
+                                   constant rates)                           */
   int32_t out_cap;              /* distribution mode: largest output length  */
   const uint32_t *out_cdf_u32;  /* distribution mode: [m][out_cap-1] row j,
                                    entry s-1 = T_j[s], nondecreasing in s    */

@@ -53,6 +53,10 @@ struct JobDev {
   uint64_t off_v[kMaxSeg];      // Nested: boundary-queue rings (k >= 1)
   uint64_t off_caps;            // Nested per-stage caps: int32 [r_L]
   int32_t has_caps, pad2_;
+  // FCFS with drawn output lengths: resident ring (32-byte records), its exit
+  // batches (u32), calendar of 2^cal_log2 buckets (u32 heads)
+  uint64_t off_res, off_exit, off_cal;
+  int32_t cal_log2, pad3_;
 };
 
 // Per-replica state slots (8 bytes each), stored [slot][R].
@@ -536,6 +540,7 @@ __host__ __device__ constexpr int nested_group_width(int max_m, int max_seg) {
 hipError_t launch_known_wait(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_known_fcfs(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s);
+hipError_t launch_fcfs_dist(int max_m, const KArgs &A, hipStream_t s);
 // the kernels for launches with time-varying rates or an arrival list
 hipError_t launch_known_wait_tv(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_known_fcfs_tv(int max_m, const KArgs &A, hipStream_t s);

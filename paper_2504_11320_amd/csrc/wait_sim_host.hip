@@ -2,6 +2,7 @@
 // model and policy (arXiv 2504.11320, Sections 2, 4 and 5), workspace layout,
 // table upload, kernel launches and the C ABI declared in include/wait_sim.h.
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstddef>
 #include <cstring>
@@ -39,6 +40,8 @@ __global__ void __launch_bounds__(256) export_kernel(KArgs A, uint8_t *out) {
       resident += slot_i(A, S_KI + k, r);
       if (k > 0) resident += slot_i(A, S_KVT + k, r) - slot_i(A, S_KVH + k, r);
     }
+  } else if (J.policy == WS_FCFS && J.known == 0) {
+    resident = slot_i(A, S_KI, r);  // live residents (the ring also holds released ones)
   } else {
     for (int j = 0; j < J.m; ++j) resident += slot_i(A, S_DT + j, r) - slot_i(A, S_DH + j, r);
     if (J.policy == WS_FCFS && slot_i(A, S_PARTJ, r) >= 0) resident += 1;  // partial prefill
@@ -93,6 +96,13 @@ __device__ __forceinline__ void for_each_segment(const KArgs &A, int64_t r, F f)
       f(blk + J.off_bkt[k], ~0u, 0, 0u, (uint32_t)J.seg_delta[k]);
       if (k >= 1) ring(blk + J.off_v[k], J.vcap_log2[k], 3, S_KVH + k, S_KVT + k);
     }
+    return;
+  }
+  if (J.policy == WS_FCFS && J.known == 0) {  // FCFS with drawn lengths
+    ring(blk + J.off_q[0], J.qcap_log2, 2, S_QH, S_QT);
+    ring(blk + J.off_res, J.qcap_log2, 3, S_DH, S_DT);
+    ring(blk + J.off_exit, J.qcap_log2, 0, S_DH, S_DT);
+    f(blk + J.off_cal, ~0u, 0, 0u, 1u << J.cal_log2);
     return;
   }
   const bool wait = J.policy == WS_WAIT;
@@ -250,6 +260,10 @@ int ceil_log2(uint64_t x) {
 
 uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
+// Launch kinds: the policy kinds, and FCFS with drawn lengths.
+constexpr int kKinds = 4;
+constexpr int kFcfsDist = 3;
+
 struct JobHost {
   JobDev d;
   int64_t reserve_tok;
@@ -269,15 +283,19 @@ struct Layout {
            off_dir = 0, off_rings = 0, total = 0;
   JobHost *jobs = nullptr;     // [n_jobs]: `own`, or storage of the caller
   std::vector<JobHost> own;
-  int32_t list_count[3] = {0, 0, 0};
-  int32_t lanes[3] = {64, 64, 64};  // replicas per wavefront, per launch
-  uint64_t list_off[3] = {0, 0, 0};
-  int32_t max_m[3] = {0, 0, 0};
+  int32_t list_count[kKinds] = {0, 0, 0, 0};
+  int32_t lanes[kKinds] = {64, 64, 64, 64};  // replicas per wavefront, per launch
+  uint64_t list_off[kKinds] = {0, 0, 0, 0};
+  int32_t max_m[kKinds] = {0, 0, 0, 0};
   int32_t max_seg = 0;
 };
 
-// The launch (kernel family and replica list) a policy runs in.
-int launch_kind(const ws_policy *p) {
+// The launch (kernel family and replica list) a job runs in: WAIT (and
+// WAIT-no-wait), Nested WAIT, FCFS with known output lengths, FCFS with
+// lengths drawn per request.
+int launch_kind(const ws_job &jb) {
+  const ws_policy *p = jb.pol;
+  if (p->kind == WS_FCFS && jb.cfg->out_len == nullptr) return kFcfsDist;
   return p->kind == WS_WAIT_NOWAIT ? (int)WS_WAIT : (int)p->kind;
 }
 
@@ -393,7 +411,11 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     for (int j = 0; j < c.m; ++j)
       if (c.prompt_len[j] > c.C - reserve_tok)
         return fail_job(WS_EINVAL, idx, "a prompt does not fit below the FCFS reserve");
-    if (!known) return fail_job(WS_EUNSUPPORTED, idx, "FCFS with unknown lengths is not supported");
+    if (!known && p.fcfs_chunk != 0)
+      return fail_job(WS_EUNSUPPORTED, idx, "chunked prefill needs known output lengths");
+    if (!known && c.n_rate_pts > 0)
+      return fail_job(WS_EUNSUPPORTED, idx,
+                      "FCFS with drawn output lengths takes constant rates only");
   } else if (kind == WS_NESTED_WAIT) {
     if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail_job(WS_EINVAL, idx, "L out of range");
     if (!p.n || !p.seg_end) return fail_job(WS_EINVAL, idx, "thresholds and seg_end required");
@@ -508,6 +530,15 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
         off += align_up(sizeof(NRec) << d.vcap_log2[k], 256);
       }
     }
+  } else if (kind == WS_FCFS && !known) {
+    // resident ring in admission order, its exit batches, exit calendar
+    d.cal_log2 = ceil_log2((uint64_t)c.out_cap + 1);
+    d.off_res = off;
+    off += align_up(sizeof(NRec) << d.qcap_log2, 256);
+    d.off_exit = off;
+    off += align_up(4ull << d.qcap_log2, 256);
+    d.off_cal = off;
+    off += align_up(4ull << d.cal_log2, 256);
   } else {
     for (int j = 0; j < c.m; ++j) {
       d.off_d[j] = off;
@@ -539,24 +570,24 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
     Lo.jobs[i].d.replica_begin = R;
     R += jobs[i].n;
     hmax = std::max(hmax, jobs[i].cfg->n_hist + 1);
-    const int pk = launch_kind(jobs[i].pol);
+    const int pk = launch_kind(jobs[i]);
     Lo.max_m[pk] = std::max(Lo.max_m[pk], jobs[i].cfg->m);
     if (pk == WS_NESTED_WAIT) Lo.max_seg = std::max(Lo.max_seg, jobs[i].pol->L);
   }
-  for (int pk = 0; pk < 3; ++pk) {
+  for (int pk = 0; pk < kKinds; ++pk) {
     auto waves = [&](int lanes) {
       // each job starts a new wavefront: its constants are wavefront-uniform
       int64_t w = 0;
       for (int i = 0; i < n_jobs; ++i)
-        if (launch_kind(jobs[i].pol) == pk) w += (jobs[i].n + lanes - 1) / lanes;
+        if (launch_kind(jobs[i]) == pk) w += (jobs[i].n + lanes - 1) / lanes;
       return w;
     };
     bool any_trace = false;
     for (int i = 0; i < n_jobs; ++i)
-      any_trace |= launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_trace > 0;
+      any_trace |= launch_kind(jobs[i]) == pk && jobs[i].cfg->n_trace > 0;
     int32_t nmax = 0;  // largest job: no wavefront needs more lanes
     for (int i = 0; i < n_jobs; ++i)
-      if (launch_kind(jobs[i].pol) == pk) nmax = std::max(nmax, jobs[i].n);
+      if (launch_kind(jobs[i]) == pk) nmax = std::max(nmax, jobs[i].n);
     // the known-length kernels with up to 4 types stop at 32 replicas per
     // wavefront (their 64-lane LDS footprint would leave half of a CU's SIMDs
     // idle), except replays
@@ -564,8 +595,9 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
     const int min_lanes = 8;
     bool any_tv = false;
     for (int i = 0; i < n_jobs; ++i)
-      any_tv |= launch_kind(jobs[i].pol) == pk && jobs[i].cfg->n_rate_pts > 0;
+      any_tv |= launch_kind(jobs[i]) == pk && jobs[i].cfg->n_rate_pts > 0;
     const int64_t target = any_tv ? kTargetWavesNested : kTargetWaves;
+    if (pk == kFcfsDist) lanes = 64;  // per-lane state in registers and LDS columns
     if (pk == WS_NESTED_WAIT) {
       // a group of lanes per replica: 64 / G replicas per wavefront
       lanes = 64 / nested_group_width(Lo.max_m[pk], Lo.max_seg);
@@ -592,7 +624,7 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
   Lo.off_job_of = off;
   off = align_up(off + 4ull * R, 256);
   Lo.off_list = off;
-  for (int pk = 0; pk < 3; ++pk) {
+  for (int pk = 0; pk < kKinds; ++pk) {
     Lo.list_off[pk] = off;
     off = align_up(off + 4ull * (uint64_t)Lo.list_count[pk], 256);
   }
@@ -650,30 +682,30 @@ uint64_t results_hist_offset(const Layout &Lo) {
   } while (0)
 
 // Side streams (default priority) on which the launches of a call's second
-// and third policy kinds run beside the first: the kinds touch disjoint
+// and later launch kinds run beside the first: the kinds touch disjoint
 // replicas, so they can share the GPU.  Created once per device and kept for
 // the life of the process; each call orders them with events of its own.
-hipError_t side_streams(hipStream_t out[2]) {
+constexpr int kSide = kKinds - 1;
+hipError_t side_streams(hipStream_t out[kSide]) {
   static std::mutex mu;
-  static std::map<int, std::pair<hipStream_t, hipStream_t>> streams;
+  static std::map<int, std::array<hipStream_t, kSide>> streams;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lock(mu);
   auto it = streams.find(dev);
   if (it == streams.end()) {
-    hipStream_t a = nullptr, b = nullptr;
-    e = hipStreamCreateWithFlags(&a, hipStreamNonBlocking);
-    if (e != hipSuccess) return e;
-    e = hipStreamCreateWithFlags(&b, hipStreamNonBlocking);
-    if (e != hipSuccess) {
-      (void)hipStreamDestroy(a);
-      return e;
+    std::array<hipStream_t, kSide> made{};
+    for (int i = 0; i < kSide; ++i) {
+      e = hipStreamCreateWithFlags(&made[i], hipStreamNonBlocking);
+      if (e != hipSuccess) {
+        for (int x = 0; x < i; ++x) (void)hipStreamDestroy(made[x]);
+        return e;
+      }
     }
-    it = streams.emplace(dev, std::make_pair(a, b)).first;
+    it = streams.emplace(dev, made).first;
   }
-  out[0] = it->second.first;
-  out[1] = it->second.second;
+  for (int i = 0; i < kSide; ++i) out[i] = it->second[i];
   return hipSuccess;
 }
 
@@ -701,7 +733,7 @@ void build_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *
     std::memcpy(img + Lo.off_jobs + sizeof(JobDev) * i, &Lo.jobs[i].d, sizeof(JobDev));
   // replica lists per launch kind: each job starts a new wavefront, whose
   // lanes beyond the launch's width are padding (-1)
-  int64_t pos[3] = {0, 0, 0};
+  int64_t pos[kKinds] = {0, 0, 0, 0};
   auto put = [&](int pk, int32_t v) {
     std::memcpy(img + Lo.list_off[pk] + 4 * pos[pk], &v, 4);
     pos[pk]++;
@@ -709,7 +741,7 @@ void build_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *
   int64_t r = 0;
   for (int i = 0; i < n_jobs; ++i) {
     const ws_job &jb = jobs[i];
-    const int pk = launch_kind(jb.pol);
+    const int pk = launch_kind(jb);
     for (int x = 0; x < jb.n; ++x, ++r) {
       std::memcpy(img + Lo.off_seed + 8 * r, &jb.streams[x].seed, 8);
       std::memcpy(img + Lo.off_rid + 4 * r, &jb.streams[x].replica_id, 4);
@@ -757,7 +789,7 @@ int prepare_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t 
 struct SideJoin {
   hipStream_t main = nullptr;
   hipEvent_t fork = nullptr;
-  hipStream_t pending[2] = {nullptr, nullptr};
+  hipStream_t pending[kSide] = {};
   int n_pending = 0;
 
   static hipError_t join_one(hipStream_t main, hipStream_t side) {
@@ -799,8 +831,8 @@ int advance_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, int64_t h
   // a call with several policy kinds runs the second and third kinds on side
   // streams, forked from and joined back into the caller's stream
   int kinds = 0;
-  for (int pk = 0; pk < 3; ++pk) kinds += Lo.list_count[pk] > 0 ? 1 : 0;
-  hipStream_t side[2] = {nullptr, nullptr};
+  for (int pk = 0; pk < kKinds; ++pk) kinds += Lo.list_count[pk] > 0 ? 1 : 0;
+  hipStream_t side[kSide] = {};
   SideJoin sj;
   sj.main = s;
   if (kinds > 1) {
@@ -809,7 +841,7 @@ int advance_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, int64_t h
     HIP_TRY(hipEventRecord(sj.fork, s));
   }
   int launched = 0;
-  for (int pk = 0; pk < 3; ++pk) {
+  for (int pk = 0; pk < kKinds; ++pk) {
     if (Lo.list_count[pk] == 0) continue;
     hipStream_t ls = s;
     if (launched > 0) {
@@ -823,7 +855,7 @@ int advance_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, int64_t h
     B.any_trace = B.any_tv = B.any_caps = 0;
     B.unit_n = pk == WS_WAIT ? 1 : 0;
     for (int i = 0; i < n_jobs; ++i) {
-      if (launch_kind(jobs[i].pol) != pk) continue;
+      if (launch_kind(jobs[i]) != pk) continue;
       if (jobs[i].cfg->n_trace > 0) B.any_trace = 1;
       if (jobs[i].cfg->n_rate_pts > 0) B.any_tv = 1;
       if (jobs[i].pol->stage_caps) B.any_caps = 1;
@@ -835,6 +867,8 @@ int advance_impl(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, int64_t h
     hipError_t e = hipSuccess;
     if (pk == WS_NESTED_WAIT)
       e = launch_nested(Lo.max_m[pk], Lo.max_seg, B, ls);
+    else if (pk == kFcfsDist)
+      e = launch_fcfs_dist(Lo.max_m[pk], B, ls);
     else
       e = pk == WS_WAIT ? launch_known_wait(Lo.max_m[pk], B, ls)
                         : launch_known_fcfs(Lo.max_m[pk], B, ls);

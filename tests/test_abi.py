@@ -126,6 +126,20 @@ def test_chunk_validation():
     assert B.workspace_bytes(B.JobArray(_job(policy="fcfs", n=[], chunk=64))) > 0
 
 
+def test_fcfs_drawn_lengths_validation():
+    """FCFS with output lengths drawn per request is accepted (its own
+    kernel); with chunked prefill or a rate profile it is WS_EUNSUPPORTED."""
+    from paper_2504_11320_amd import binding as B
+    wl = W.config3(replicas=2, rate_index=[3])[0].wl
+    fc = W.Workload(**{**wl.__dict__, "policy": "fcfs", "n": [], "seg_end": None})
+    assert B.workspace_bytes(B.JobArray([W.Job(fc, 0, W.ids(2))])) > 0
+    ch = W.Workload(**{**fc.__dict__, "chunk": 256})
+    assert _err([W.Job(ch, 0, W.ids(2))]).code == B.WS_EUNSUPPORTED
+    rt, rf = W.diurnal_profile(3, 1e6, points=5)
+    tv = W.with_profile(fc, rt, rf)
+    assert _err([W.Job(tv, 0, W.ids(2))]).code == B.WS_EUNSUPPORTED
+
+
 def test_wait_admission_bound():
     """WAIT: one batch may admit sum_j n_j (l_j + 1) tokens; at 2^29 or more the
     library's 32-bit resident-memory counters could overflow:
