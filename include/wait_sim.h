@@ -105,8 +105,12 @@ typedef enum {
                                  in a row; it has no further arrivals       */
 
 /* Limits of the library. */
-#define WS_MAX_TYPES 16
-#define WS_MAX_TYPES_KNOWN 16 /* WAIT and FCFS (the same as WS_MAX_TYPES)       */
+#define WS_MAX_TYPES 64
+#define WS_MAX_TYPES_KNOWN 16 /* WAIT (both forms) takes at most this many
+                                 types; FCFS with known output lengths and
+                                 more types runs in the kernel for drawn
+                                 lengths (no chunked prefill or rate profile
+                                 there)                                     */
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255
 #define WS_MAX_RATE_PTS 32

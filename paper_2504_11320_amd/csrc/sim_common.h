@@ -56,7 +56,8 @@ struct JobDev {
   // FCFS with drawn output lengths: resident ring (32-byte records), its exit
   // batches (u32), calendar of 2^cal_log2 buckets (u32 heads)
   uint64_t off_res, off_exit, off_cal;
-  int32_t cal_log2, pad3_;
+  int32_t cal_log2;
+  int32_t fdist;  // FCFS job run by the kernel for per-request lengths
 };
 
 // Per-replica state slots (8 bytes each), stored [slot][R].
@@ -532,8 +533,11 @@ hipError_t launch_checked(Kernel kernel, dim3 g, hipStream_t s, const KArgs &A) 
 // Lanes per replica of the Nested WAIT kernel: the smallest of 4, 8, 16 that
 // covers the types and the segments (one type and one segment per lane).
 __host__ __device__ constexpr int nested_group_width(int max_m, int max_seg) {
-  return (max_m > max_seg ? max_m : max_seg) <= 4 ? 4
-         : (max_m > max_seg ? max_m : max_seg) <= 8 ? 8 : 16;
+  return (max_m > max_seg ? max_m : max_seg) <= 4    ? 4
+         : (max_m > max_seg ? max_m : max_seg) <= 8  ? 8
+         : (max_m > max_seg ? max_m : max_seg) <= 16 ? 16
+         : (max_m > max_seg ? max_m : max_seg) <= 32 ? 32
+                                                     : 64;
 }
 
 // Launchers, one per kernel family (defined next to their kernels).

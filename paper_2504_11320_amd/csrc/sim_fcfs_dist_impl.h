@@ -1,7 +1,10 @@
 // sim_fcfs_dist_impl.h -- simulation kernel for FCFS when output lengths are
 // unknown to the scheduler (arXiv 2504.11320: Section 4.1's FCFS with LIFO
 // eviction on overflow; the unknown-length model of Section 5.1, each
-// request's length drawn once at arrival from its type's distribution).
+// request's length drawn once at arrival from its type's distribution).  It
+// also runs FCFS with known lengths l'_j for more types than the
+// known-length kernels hold: the structure below takes any per-request
+// length.
 //
 // One lane per replica.  FCFS batches every resident every iteration, so a
 // prompt admitted (prefilled) at batch kb with output length L completes at
@@ -58,7 +61,7 @@ __global__ void __launch_bounds__(64) sim_fcfs_dist_kernel(KArgs A) {
   __shared__ double s_tn[MT][64];
   __shared__ uint32_t s_k[MT][64];
   __shared__ int32_t s_len[MT][64];
-  __shared__ int32_t s_l[MT];
+  __shared__ int32_t s_l[MT], s_lp[MT];
   __shared__ double s_lam[MT];
 
   const int tx = threadIdx.x;
@@ -72,13 +75,15 @@ __global__ void __launch_bounds__(64) sim_fcfs_dist_kernel(KArgs A) {
   const int m = J.m;
   const int n_hist = J.n_hist;
   const int32_t cap = J.out_cap;
+  const bool known = J.known != 0;  // lengths l'_j of the type
   const uint32_t *cdf = (const uint32_t *)(A.ws + J.off_cdf);
-  const bool use_guide = J.n_trace == 0 && cap > 1 && cap <= 65535;
+  const bool use_guide = !known && J.n_trace == 0 && cap > 1 && cap <= 65535;
   {
     const double *edges_g = (const double *)(A.ws + J.off_edges);
     for (int b = tx; b <= n_hist; b += 64) s_edges[b] = b < n_hist ? edges_g[b] : INFINITY;
     for (int j = tx; j < MT; j += 64) {
       s_l[j] = j < m ? J.l[j] : 0;
+      s_lp[j] = j < m ? J.lp[j] : 1;
       s_lam[j] = j < m ? J.lambda[j] : 0.0;
     }
     if (use_guide) {
@@ -112,7 +117,7 @@ __global__ void __launch_bounds__(64) sim_fcfs_dist_kernel(KArgs A) {
   uint32_t *cal = (uint32_t *)(blk + J.off_cal);
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
   auto row_of = [&](int j) __attribute__((always_inline)) -> const uint32_t * {
-    return cap <= 1 ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
+    return known || cap <= 1 ? nullptr : cdf + (size_t)j * (size_t)(cap - 1);
   };
   auto guide_of = [&](int j) __attribute__((always_inline)) -> const uint16_t * {
     return use_guide ? s_cdfg[j] : nullptr;
@@ -134,7 +139,7 @@ __global__ void __launch_bounds__(64) sim_fcfs_dist_kernel(KArgs A) {
                                                &Lj, nullptr, guide_of(j));
       s_tn[j][tx] = tn;
       s_k[j][tx] = 0;
-      s_len[j][tx] = cap <= 1 ? 1 : Lj;
+      s_len[j][tx] = known ? s_lp[j] : (cap <= 1 ? 1 : Lj);
     }
     for (uint32_t b = 0; b <= wmask; ++b) cal[b] = kNil;
     for (int b = 0; b < A.hist_stride; ++b) hist[b] = 0;  // whole row, padding included
@@ -216,7 +221,7 @@ __global__ void __launch_bounds__(64) sim_fcfs_dist_kernel(KArgs A) {
   auto take = [&](int jn, double a) __attribute__((always_inline)) {
     int32_t Lr;
     if (trace) {
-      Lr = tr_len[tridx];
+      Lr = known ? s_lp[jn] : tr_len[tridx];
       tridx++;
     } else {
       Lr = s_len[jn][tx];
@@ -226,7 +231,7 @@ __global__ void __launch_bounds__(64) sim_fcfs_dist_kernel(KArgs A) {
                                 nullptr, guide_of(jn));
       s_k[jn][tx] = k;
       s_tn[jn][tx] = s_tn[jn][tx] + g;
-      s_len[jn][tx] = cap <= 1 ? 1 : Lj;
+      s_len[jn][tx] = known ? s_lp[jn] : (cap <= 1 ? 1 : Lj);
       next_arrival();
     }
     arrivals++;
@@ -463,6 +468,7 @@ hipError_t launch_fcfs_dist_k(int max_m, const KArgs &A, hipStream_t s) {
   if (A.n_list % 64 != 0) return hipErrorInvalidValue;
   if (max_m <= 4) return launch_fd<4, TV>(A, s);
   if (max_m <= 16) return launch_fd<16, TV>(A, s);
+  if (max_m <= 64) return launch_fd<64, TV>(A, s);
   return hipErrorInvalidValue;  // the host admits at most WS_MAX_TYPES types
 }
 

@@ -2,8 +2,9 @@
 // Algorithm 2, Section 5.1; event-driven form Algorithm 4, Appendix B.1;
 // coarse segments with heterogeneous prompts, Appendix A).
 //
-// A group of G lanes (G = 4, 8 or 16, a power of two >= the job's types and
-// segments) runs one replica; a 64-lane wavefront holds 64/G replicas.  Lane
+// A group of G lanes (G = 4, 8, 16, 32 or 64, a power of two >= the job's
+// types and segments) runs one replica; a 64-lane wavefront holds 64/G
+// replicas.  Lane
 // g of a group owns request type g (its arrival clock, draw counter and the
 // length of its pending arrival) and segment g (its service count, interior
 // count and memory, calendar, cohort slots and the cache of its youngest
@@ -119,12 +120,25 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t v) {
   return ((uint64_t)dpp32<CTRL>((uint32_t)(v >> 32)) << 32) | dpp32<CTRL>((uint32_t)v);
 }
 
+// Groups of 32 or 64 lanes combine the 16-lane rows with lane-index XOR
+// exchanges (16, then 32).
+template <int MASK>
+__device__ __forceinline__ uint32_t xor32(uint32_t v) {
+  return (uint32_t)__shfl_xor((int)v, MASK, 64);
+}
+template <int MASK>
+__device__ __forceinline__ uint64_t xor64(uint64_t v) {
+  return ((uint64_t)xor32<MASK>((uint32_t)(v >> 32)) << 32) | xor32<MASK>((uint32_t)v);
+}
+
 template <int G, typename Op>
 __device__ __forceinline__ uint64_t group_reduce64(uint64_t v, Op op) {
   v = op(v, dpp64<kDppSwap1>(v));
   v = op(v, dpp64<kDppSwap2>(v));
   if constexpr (G >= 8) v = op(v, dpp64<kDppHalfMirror>(v));
   if constexpr (G >= 16) v = op(v, dpp64<kDppMirror>(v));
+  if constexpr (G >= 32) v = op(v, xor64<16>(v));
+  if constexpr (G >= 64) v = op(v, xor64<32>(v));
   return v;
 }
 template <int G>
@@ -137,6 +151,8 @@ __device__ __forceinline__ uint32_t group_reduce32(uint32_t v, Op op) {
   v = op(v, dpp32<kDppSwap2>(v));
   if constexpr (G >= 8) v = op(v, dpp32<kDppHalfMirror>(v));
   if constexpr (G >= 16) v = op(v, dpp32<kDppMirror>(v));
+  if constexpr (G >= 32) v = op(v, xor32<16>(v));
+  if constexpr (G >= 64) v = op(v, xor32<32>(v));
   return v;
 }
 // Sum of values whose group total fits in 32 bits (per-batch memory changes
@@ -163,9 +179,13 @@ __device__ __forceinline__ double group_min(double v) {
 }
 // The group's G bits of a wavefront ballot (bit g = group lane g).
 template <int G>
-__device__ __forceinline__ uint32_t group_bits(bool pred) {
+__device__ __forceinline__ uint64_t group_bits(bool pred) {
   const uint64_t b = __ballot(pred);
-  return (uint32_t)((b >> (threadIdx.x & (64 - G))) & ((1ull << G) - 1ull));
+  if constexpr (G == 64) {
+    return b;
+  } else {
+    return (b >> (threadIdx.x & (64 - G))) & ((1ull << G) - 1ull);
+  }
 }
 
 // Wait for every outstanding memory operation of the wavefront; also a
@@ -475,8 +495,8 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   auto next_arrival = [&]() __attribute__((always_inline)) {
     const double v = is_t ? tn : INFINITY;
     tmin = group_min<G>(v);
-    const uint32_t b = group_bits<G>(is_t && v == tmin);
-    jmin = b != 0 ? __builtin_ctz(b) : 0;
+    const uint64_t b = group_bits<G>(is_t && v == tmin);
+    jmin = b != 0 ? __builtin_ctzll(b) : 0;
   };
   auto peek = [&](int &jn) __attribute__((always_inline)) -> double {
     if (trace) {
@@ -613,11 +633,11 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     if (boundary) {
       const bool cand = is_s && k >= 1 && s_vt[k][q] != s_vh[k][q];
       const uint64_t key = cand ? nrec_key(s_vb[k][q]) : 0ull;
-      const uint32_t cb = group_bits<G>(cand);
+      const uint64_t cb = group_bits<G>(cand);
       if (cb != 0) {
         const uint64_t mx = group_max<G>(key);
-        const uint32_t wb = group_bits<G>(cand && key == mx);
-        const int h = __builtin_ctz(wb);  // keys are unique: one lane
+        const uint64_t wb = group_bits<G>(cand && key == mx);
+        const int h = __builtin_ctzll(wb);  // keys are unique: one lane
         const bool me = gl == h;
         // every lane reads the victim (the back of boundary queue h) and its
         // charge l + r_{h-1} from LDS
@@ -645,11 +665,11 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     if (k >= klo) idx = youngest_interior();
     const bool cand = idx != kNil;
     const uint64_t key = cand ? nrec_key(yi) : 0ull;
-    const uint32_t cb = group_bits<G>(cand);
+    const uint64_t cb = group_bits<G>(cand);
     if (cb == 0) return 0;
     const uint64_t mx = group_max<G>(key);
-    const uint32_t wb = group_bits<G>(cand && key == mx);
-    const int w = __builtin_ctz(wb);
+    const uint64_t wb = group_bits<G>(cand && key == mx);
+    const int w = __builtin_ctzll(wb);
     const bool me = gl == w;
     int32_t ch = 0, gen = 0, dpend = 0;
     const NRec rec = yi;
@@ -759,9 +779,9 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       }
       const bool ok = gl == 0 ? (int64_t)(qt - qh) >= (capped ? ncap : n0)
                               : (is_s && (int32_t)(s_vt[k][q] - s_vh[k][q]) >= ncap);
-      const uint32_t okb = group_bits<G>(ok);
+      const uint64_t okb = group_bits<G>(ok);
       if (okb & 1u) {
-        kmax = __builtin_ctz(~okb);  // lanes >= L never meet it
+        kmax = __builtin_ctzll(~okb);  // lanes >= L never meet it
         break;
       }
       int jn;
@@ -1131,12 +1151,14 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   put_f(A, S_TNEXT + gl, r, is_t ? tn : INFINITY);
   put_i(A, S_K + gl, r, kj);
   put_i(A, S_LNEXT + gl, r, Lnj);
-  put_i(A, S_KSVC + k, r, svc);
-  put_i(A, S_KI + k, r, I);
-  put_i(A, S_KM + k, r, M);
-  put_i(A, S_KB + k, r, is_s ? s_B[k][q] : 0);
-  put_i(A, S_KVH + k, r, is_s ? s_vh[k][q] : 0);
-  put_i(A, S_KVT + k, r, is_s ? s_vt[k][q] : 0);
+  if (k < kMaxSeg) {  // groups wider than the segment limit: lanes without one
+    put_i(A, S_KSVC + k, r, svc);
+    put_i(A, S_KI + k, r, I);
+    put_i(A, S_KM + k, r, M);
+    put_i(A, S_KB + k, r, is_s ? s_B[k][q] : 0);
+    put_i(A, S_KVH + k, r, is_s ? s_vh[k][q] : 0);
+    put_i(A, S_KVT + k, r, is_s ? s_vt[k][q] : 0);
+  }
 }
 
 template <int G, bool TV>
@@ -1151,7 +1173,9 @@ hipError_t launch_nested_k(int max_m, int max_seg, const KArgs &A, hipStream_t s
   if (A.lanes != 64 / G || A.n_list % 64 != 0) return hipErrorInvalidValue;
   if (G == 4) return launch_g<4, TV>(A, s);
   if (G == 8) return launch_g<8, TV>(A, s);
-  return launch_g<16, TV>(A, s);
+  if (G == 16) return launch_g<16, TV>(A, s);
+  if (G == 32) return launch_g<32, TV>(A, s);
+  return launch_g<64, TV>(A, s);
 }
 
 }  // namespace

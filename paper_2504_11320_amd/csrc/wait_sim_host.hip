@@ -40,7 +40,7 @@ __global__ void __launch_bounds__(256) export_kernel(KArgs A, uint8_t *out) {
       resident += slot_i(A, S_KI + k, r);
       if (k > 0) resident += slot_i(A, S_KVT + k, r) - slot_i(A, S_KVH + k, r);
     }
-  } else if (J.policy == WS_FCFS && J.known == 0) {
+  } else if (J.fdist) {
     resident = slot_i(A, S_KI, r);  // live residents (the ring also holds released ones)
   } else {
     for (int j = 0; j < J.m; ++j) resident += slot_i(A, S_DT + j, r) - slot_i(A, S_DH + j, r);
@@ -98,7 +98,7 @@ __device__ __forceinline__ void for_each_segment(const KArgs &A, int64_t r, F f)
     }
     return;
   }
-  if (J.policy == WS_FCFS && J.known == 0) {  // FCFS with drawn lengths
+  if (J.fdist) {  // FCFS in the kernel for per-request lengths
     ring(blk + J.off_q[0], J.qcap_log2, 2, S_QH, S_QT);
     ring(blk + J.off_res, J.qcap_log2, 3, S_DH, S_DT);
     ring(blk + J.off_exit, J.qcap_log2, 0, S_DH, S_DT);
@@ -295,7 +295,8 @@ struct Layout {
 // lengths drawn per request.
 int launch_kind(const ws_job &jb) {
   const ws_policy *p = jb.pol;
-  if (p->kind == WS_FCFS && jb.cfg->out_len == nullptr) return kFcfsDist;
+  if (p->kind == WS_FCFS && (jb.cfg->out_len == nullptr || jb.cfg->m > WS_MAX_TYPES_KNOWN))
+    return kFcfsDist;
   return p->kind == WS_WAIT_NOWAIT ? (int)WS_WAIT : (int)p->kind;
 }
 
@@ -393,8 +394,15 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     return fail_job(WS_EINVAL, idx, "fcfs_chunk applies to FCFS only");
   if (kind != WS_NESTED_WAIT && p.stage_caps)
     return fail_job(WS_EINVAL, idx, "stage_caps apply to Nested WAIT only");
+  // FCFS jobs the kernel for per-request lengths runs (drawn lengths, or
+  // more types than the known-length kernels hold)
+  const bool fdist = kind == WS_FCFS && (!known || c.m > WS_MAX_TYPES_KNOWN);
   if (kind == WS_WAIT) {
     if (!known) return fail_job(WS_EINVAL, idx, "WAIT needs known output lengths");
+    if (c.m > WS_MAX_TYPES_KNOWN)
+      return fail_job(WS_EUNSUPPORTED, idx,
+                      std::string("WAIT takes at most ") + std::to_string(WS_MAX_TYPES_KNOWN) +
+                          " types");
     if (!p.n) return fail_job(WS_EINVAL, idx, "thresholds required");
     int64_t fresh = 0;  // memory one batch can admit
     for (int j = 0; j < c.m; ++j) {
@@ -411,11 +419,13 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     for (int j = 0; j < c.m; ++j)
       if (c.prompt_len[j] > c.C - reserve_tok)
         return fail_job(WS_EINVAL, idx, "a prompt does not fit below the FCFS reserve");
-    if (!known && p.fcfs_chunk != 0)
-      return fail_job(WS_EUNSUPPORTED, idx, "chunked prefill needs known output lengths");
-    if (!known && c.n_rate_pts > 0)
+    if (fdist && p.fcfs_chunk != 0)
       return fail_job(WS_EUNSUPPORTED, idx,
-                      "FCFS with drawn output lengths takes constant rates only");
+                      "chunked prefill needs known output lengths and at most 16 types");
+    if (fdist && c.n_rate_pts > 0)
+      return fail_job(WS_EUNSUPPORTED, idx,
+                      "FCFS with drawn output lengths or more than 16 types takes constant "
+                      "rates only");
   } else if (kind == WS_NESTED_WAIT) {
     if (p.L < 1 || p.L > WS_MAX_SEGMENTS) return fail_job(WS_EINVAL, idx, "L out of range");
     if (!p.n || !p.seg_end) return fail_job(WS_EINVAL, idx, "thresholds and seg_end required");
@@ -530,9 +540,10 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
         off += align_up(sizeof(NRec) << d.vcap_log2[k], 256);
       }
     }
-  } else if (kind == WS_FCFS && !known) {
+  } else if (fdist) {
     // resident ring in admission order, its exit batches, exit calendar
-    d.cal_log2 = ceil_log2((uint64_t)c.out_cap + 1);
+    d.fdist = 1;
+    d.cal_log2 = ceil_log2((uint64_t)maxL + 1);
     d.off_res = off;
     off += align_up(sizeof(NRec) << d.qcap_log2, 256);
     d.off_exit = off;

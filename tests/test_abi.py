@@ -72,7 +72,8 @@ def test_fcfs_reserve_validation():
 
 
 def test_type_limits():
-    """Every policy takes up to 16 request types; more than 16 is invalid."""
+    """Nested WAIT and FCFS take up to 64 request types, WAIT up to 16 (more:
+    WS_EUNSUPPORTED); more than 64 is invalid for every policy."""
     from paper_2504_11320_amd import binding as B
 
     def model(m, policy):
@@ -88,7 +89,10 @@ def test_type_limits():
 
     for policy in ("wait", "fcfs", "nested"):
         assert B.workspace_bytes(B.JobArray(model(16, policy))) > 0
-        assert _err(model(17, policy)).code == B.WS_EINVAL
+        assert _err(model(65, policy)).code == B.WS_EINVAL
+    assert _err(model(17, "wait")).code == B.WS_EUNSUPPORTED
+    for policy in ("fcfs", "nested"):
+        assert B.workspace_bytes(B.JobArray(model(64, policy))) > 0
 
 
 def test_rate_profile_validation():

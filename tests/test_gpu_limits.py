@@ -101,3 +101,37 @@ def test_sixteen_types_wait_and_fcfs(B):
                       out_len=lp, reserve=0.01, hist_edges=edges, record_capacity=1 << 12)
     jobs = [W.Job(wait, 11, W.ids(37)), W.Job(fcfs, 12, W.ids(29, start=500))]
     check(B, jobs, 1200, "16 types, WAIT and FCFS, 255 edges")
+
+
+def test_many_types_nested_and_fcfs(B):
+    """Beyond 16 types: Nested WAIT with 40 types and 12 segments (lane groups
+    of 64) and with 24 types (groups of 32), FCFS with 64 types, known and
+    drawn output lengths (the kernel for per-request lengths), against the
+    oracle."""
+    rng = np.random.default_rng(64)
+    jobs = []
+    for m, nseg in ((40, 12), (24, 5)):
+        l, lam = _types(rng, m)
+        cap = 96
+        cuts = sorted(rng.choice(np.arange(1, cap), size=nseg - 1, replace=False).tolist())
+        cdf = np.stack([W.geometric_cdf_table(float(rng.uniform(2.0, 40.0)), cap)
+                        for _ in range(m)])
+        C = int((max(l) + cap) * 3)
+        wl = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="nested",
+                        n=[int(x) for x in rng.integers(1, 3, nseg)], out_cap=cap,
+                        out_cdf=cdf, seg_end=[int(c) for c in cuts] + [cap],
+                        hist_edges=W.default_edges(5.0, 128), record_capacity=1 << 12)
+        jobs.append(W.Job(wl, 21, W.ids(6)))
+    l, lam = _types(rng, 64)
+    lp = [int(x) for x in rng.integers(1, 48, 64)]
+    C = 3 * max(a + b for a, b in zip(l, lp))
+    known = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="fcfs", n=[],
+                       out_len=lp, reserve=0.01, hist_edges=W.default_edges(5.0, 128),
+                       record_capacity=1 << 12)
+    cdf = np.stack([W.geometric_cdf_table(float(rng.uniform(2.0, 30.0)), 48) for _ in range(64)])
+    drawn = W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="fcfs", n=[],
+                       out_cap=48, out_cdf=cdf, hist_edges=W.default_edges(5.0, 128),
+                       record_capacity=1 << 12)
+    jobs += [W.Job(known, 22, W.ids(9)), W.Job(drawn, 23, W.ids(9))]
+    g, _ = check(B, jobs, 1500, "40/24-type Nested WAIT, 64-type FCFS")
+    assert g["evictions"].sum() > 0
