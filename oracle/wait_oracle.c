@@ -254,7 +254,7 @@ typedef struct {
   int64_t kb;   /* admission key: batch of last prefill          */
   int64_t kp;   /* admission key: position within that batch    */
   int64_t id;   /* request id (arrival order)                    */
-  int32_t cap_in; /* Nested: size of the cohort it entered its segment with */
+  int32_t cap_in; /* WAIT, Nested: the cap of the cohort it was admitted with */
 } req_t;
 
 typedef struct {
@@ -552,6 +552,19 @@ static void select_by_stage(sim_t *S, int64_t lo, int64_t hi, int32_t cap,
 
 /* Algorithm 1: eligible types J = {j : n_j0 >= n_j}; for every j in J and
  * every stage s select min(n_j, n_js).  Returns 1 if a batch was formed. */
+/* Threshold of type j at its next service under WAIT: n_j, or with per-stage
+ * caps (Section 6: tl spread over the type's l'_j + 1 prefill and decode
+ * stages) the caps of its stages taken in turn, the x-th service (x = 1, 2,
+ * ...) taking the cap of stage (x-1) mod (l'_j + 1).  The admitted cohort has
+ * that size. */
+static int32_t wait_cap(const sim_t *S, int32_t j) {
+  const or_config *c = S->cfg;
+  if (!c->stage_caps) return c->n[j];
+  int64_t lo = 0;
+  for (int32_t i = 0; i < j; i++) lo += c->lp[i] + 1;
+  return c->stage_caps[lo + S->nsvc[j] % (c->lp[j] + 1)];
+}
+
 static int decide_wait(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   const or_config *c = S->cfg;
   const int nowait = c->policy == OR_WAIT_NOWAIT;
@@ -563,19 +576,21 @@ static int decide_wait(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
   for (int64_t i = 0; i < S->res.len; i++) nres[S->R[S->res.v[i]].j]++;
   int any = 0;
   for (int32_t j = 0; j < c->m; j++) {
-    elig[j] = nowait ? (S->q[j].len > 0 || nres[j] > 0) : (S->q[j].len >= c->n[j]);
+    elig[j] = nowait ? (S->q[j].len > 0 || nres[j] > 0) : (S->q[j].len >= wait_cap(S, j));
     if (elig[j]) any = 1;
   }
   if (!any) return 0;
   int64_t p = 0;
   for (int32_t j = 0; j < c->m; j++) {
     if (!elig[j]) continue;
-    const int64_t admit = nowait ? (S->q[j].len < c->n[j] ? S->q[j].len : c->n[j]) : c->n[j];
+    const int32_t cap = nowait ? c->n[j] : wait_cap(S, j);
+    const int64_t admit = nowait ? (S->q[j].len < c->n[j] ? S->q[j].len : c->n[j]) : cap;
     for (int64_t i = 0; i < admit; i++) {
       int64_t r = dq_pop_front(&S->q[j]);
       S->R[r].kb = S->b;
       S->R[r].kp = p++;
       S->R[r].s = 0;
+      S->R[r].cap_in = cap;
       select_req(S, r, 0, tokens);
       *prefill_l += c->l[j];
     }
@@ -586,7 +601,8 @@ static int decide_wait(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
       if (S->R[S->res.v[i]].j == j) S->tmp[cnt++] = S->res.v[i];
     t_sort_R = S->R;
     sort_ids(S->tmp, cnt, cmp_stage_key);
-    select_by_stage(S, 0, cnt, c->n[j], tokens);
+    select_by_stage(S, 0, cnt, -1, tokens);
+    S->nsvc[j]++;
   }
   return 1;
 }
@@ -967,7 +983,7 @@ int oracle_run(const or_config *cfg, uint64_t seed, uint32_t replica_id,
   S.q = (dq_t *)calloc((size_t)S.nq, sizeof(dq_t));
   S.bnd = (dq_t *)calloc((size_t)(c->policy == OR_NESTED ? c->nseg + 2 : 1),
                          sizeof(dq_t));
-  S.nsvc = (int64_t *)calloc((size_t)(c->policy == OR_NESTED ? c->nseg + 2 : 1),
+  S.nsvc = (int64_t *)calloc((size_t)(c->policy == OR_NESTED ? c->nseg + 2 : c->m + 1),
                              sizeof(int64_t));
   S.t_next = (double *)calloc((size_t)c->m, sizeof(double));
   S.L_next = (int32_t *)calloc((size_t)c->m, sizeof(int32_t));

@@ -63,11 +63,13 @@ typedef struct {
   const double *rate_f;
   int32_t chunk;            /* FCFS: prefill tokens per iteration (chunked
                                prefill), 0 = whole prefills                   */
-  /* NESTED: per-stage caps (Section 6, "WAIT and Nested WAIT settings"):
-   * stage_caps[s - 1] is the cap of decode stage s = 1..seg_end[nseg-1];
+  /* Per-stage caps (Section 6, "WAIT and Nested WAIT settings"), or NULL.
+   * NESTED: stage_caps[s - 1] is the cap of decode stage s = 1..seg_end[nseg-1];
    * segment k's stages r_{k-1}+1..r_k hold its caps, taken in turn, one per
-   * service of the segment, as the size of the entering cohort.  NULL: every
-   * service of segment k admits n[k-1]. */
+   * service of the segment, as the size of the entering cohort (NULL: every
+   * service of segment k admits n[k-1]).  WAIT: per type j in turn, l'_j + 1
+   * caps (its prefill and decode stages), taken in turn, one per service of
+   * the type (NULL: n_j). */
   const int32_t *stage_caps;
 } or_config;
 

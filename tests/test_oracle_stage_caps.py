@@ -1,5 +1,5 @@
-"""Per-stage caps of Nested WAIT (Section 6, "WAIT and Nested WAIT settings"),
-in the oracle.
+"""Per-stage caps of Nested WAIT and WAIT (Section 6, "WAIT and Nested WAIT
+settings"), in the oracle.
 
 The experiments turn a system-wide batch-size cap tl into segment caps B_k
 and spread each over the segment's decode stages, so caps inside a segment
@@ -9,7 +9,9 @@ service).  Pinned by a hand trace (golden/nested_stage_caps.json: caps
 (2, 1) and (1, 0) on two segments, batch by batch), by the reduction to the
 one-threshold policy when every cap of a segment equals n_k, by the prefill
 sequence of the tl = 30 calibration, and by copies of the oracle with a
-planted misreading that the hand trace rejects.
+planted misreading that the hand trace rejects.  WAIT (one type: tl spread over
+its prefill and decode stages) has the same four kinds of pins
+(golden/wait_stage_caps.json, caps (2, 1, 1)).
 """
 import json
 import os
@@ -164,3 +166,124 @@ def test_hand_trace_rejects_planted_misreading(oracle_lib, tmp_path, name):
     g = _gold()
     lib = _mutant(oracle_lib, tmp_path, name)
     assert _mismatches(_run(oracle_lib, g, library=lib), g), name
+
+
+# ----------------------------------------------------------------- WAIT ----
+
+WAIT_GOLD = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                         "wait_stage_caps.json")
+WAIT_FIELDS = tuple(f for f in FIELDS if f != "mplus")
+
+
+def _wait_gold():
+    with open(WAIT_GOLD) as f:
+        return json.load(f)
+
+
+def _wait_workload(g):
+    i = g["instance"]
+    n = len(i["arrivals"])
+    return W.trace_workload("wait", [i["prompt_len"]], [i["out_len"]], i["d0"], i["d1"], i["C"],
+                            i["n"], i["arrivals"], [0] * n, stage_caps=i["stage_caps"])
+
+
+def _wait_mismatches(r, g):
+    bad = []
+    bt = r["batches_trace"]
+    if len(bt) != len(g["batches"]):
+        bad.append(f"{len(bt)} batches")
+    for b, (got, want) in enumerate(zip(bt, g["batches"])):
+        for f in WAIT_FIELDS + ("t_launch",):
+            if got[f] != want[f]:
+                bad.append(f"batch {b} {f}: {got[f]} != {want[f]}")
+    for k, v in g["final"].items():
+        if r[k] != v:
+            bad.append(f"{k}: {r[k]} != {v}")
+    return bad
+
+
+def _wait_run(O, g, library=None):
+    h = g["instance"]["horizon"]
+    return O.run_one(_wait_workload(g), 0, 0, h, btrace_cap=h, library=library)
+
+
+def test_wait_golden_is_consistent():
+    g = _wait_gold()
+    fin = g["final"]
+    assert fin["batch_tokens_sum"] == sum(b["tokens"] for b in g["batches"])
+    assert fin["completions"] == sum(b["completions"] for b in g["batches"])
+    assert fin["arrivals"] == len(g["instance"]["arrivals"])
+
+
+def test_wait_stage_caps_hand_trace(oracle_lib):
+    g = _wait_gold()
+    assert _wait_mismatches(_wait_run(oracle_lib, g), g) == []
+
+
+def _random_wait(rng):
+    m = int(rng.integers(1, 4))
+    l = [int(x) for x in rng.integers(1, 40, m)]
+    lp = [int(x) for x in rng.integers(1, 20, m)]
+    n = [int(x) for x in rng.integers(1, 4, m)]
+    C = int(max(a + b for a, b in zip(l, lp)) * rng.uniform(1.0, 5.0))
+    return W.Workload(prompt_len=l, lam=[float(x) for x in rng.uniform(0.02, 1.0, m)],
+                      d0=float(rng.uniform(0.5, 5.0)), d1=float(rng.uniform(0.0, 0.02)),
+                      C=C, policy="wait", n=n, out_len=lp,
+                      hist_edges=W.default_edges(1.0, 64), record_capacity=1 << 14)
+
+
+def test_wait_uniform_caps_are_the_one_threshold_policy(oracle_lib):
+    """Caps all equal to n_j over type j's l'_j + 1 stages reproduce WAIT
+    without caps, bit for bit (random models, evictions included)."""
+    O = oracle_lib
+    rng = np.random.default_rng(41)
+    for _ in range(12):
+        wl = _random_wait(rng)
+        a = O.run(wl, 4, W.ids(4), 1500)
+        wl.stage_caps = sum(([nj] * (lpj + 1) for nj, lpj in zip(wl.n, wl.out_len)), [])
+        b = O.run(wl, 4, W.ids(4), 1500)
+        for k in a:
+            assert np.array_equal(a[k], b[k]), k
+
+
+def test_wait_tl30_calibration_sets_the_prefill_sequence(oracle_lib):
+    """Single-type p512d20 WAIT with the caps tl = 30 gives (30 over 21
+    stages: 2 on the first nine, 1 on the rest): while the queue never runs
+    short of the next cap, the admissions follow the caps with period 21."""
+    from paper_2504_11320_amd import calibrate as Cal
+    cal = Cal.calibrate_wait(30, 20)
+    assert cal["stage_caps"] == [2] * 9 + [1] * 12
+    wl = W.config_p512d20(replicas=1)[6].wl  # the boundary rate under WAIT
+    wl.stage_caps = cal["stage_caps"]
+    wl.n = [2]
+    wl.lam = [0.5]  # a queue that never empties
+    r = oracle_lib.run_one(wl, 0, 0, 300, btrace_cap=300)
+    pre = [b["prefills"] for b in r["batches_trace"]]
+    assert pre == [cal["stage_caps"][b % 21] for b in range(300)]
+
+
+WAIT_MUTATIONS = {
+    "wait_cap_offset": ("return c->stage_caps[lo + S->nsvc[j] % (c->lp[j] + 1)];",
+                        "return c->stage_caps[lo + (S->nsvc[j] + 1) % (c->lp[j] + 1)];"),
+    "wait_no_rotation": ("    select_by_stage(S, 0, cnt, -1, tokens);\n    S->nsvc[j]++;\n",
+                         "    select_by_stage(S, 0, cnt, -1, tokens);\n"),
+    "wait_cell_limit": ("    select_by_stage(S, 0, cnt, -1, tokens);\n    S->nsvc[j]++;\n",
+                        "    select_by_stage(S, 0, cnt, cap, tokens);\n    S->nsvc[j]++;\n"),
+    "wait_one_threshold": ("  if (!c->stage_caps) return c->n[j];",
+                           "  if (c->stage_caps) return c->n[j];"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(WAIT_MUTATIONS))
+def test_wait_hand_trace_rejects_planted_misreading(oracle_lib, tmp_path, name):
+    g = _wait_gold()
+    src = open(oracle_lib.SRC).read()
+    old, new = WAIT_MUTATIONS[name]
+    assert src.count(old) == 1, name
+    path = tmp_path / f"wait_oracle_{name}.c"
+    path.write_text(src.replace(old, new))
+    lib = tmp_path / f"liboracle_{name}.so"
+    subprocess.run(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math",
+                    "-fPIC", "-shared", "-I", os.path.dirname(oracle_lib.SRC), "-o", str(lib),
+                    str(path), "-lpthread", "-lm"], check=True)
+    assert _wait_mismatches(_wait_run(oracle_lib, g, library=oracle_lib.load(str(lib))), g), name
