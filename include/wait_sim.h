@@ -173,17 +173,20 @@ typedef struct {
                             it; a partial prompt holds its cached tokens, is
                             evicted first and restarts.  0: whole prefills.
                             Must be 0 for the other policies.             */
-  const int32_t *stage_caps; /* NESTED, optional: per-stage caps (Section 6,
-                            the batch-size cap tl spread over segments and
-                            their decode stages).  stage_caps[s-1] >= 0 is
-                            the cap of decode stage s = 1..r_L; segment k
-                            takes the caps of its stages r_{k-1}+1..r_k in
-                            turn, one per service, as its threshold and the
-                            size of the cohort it admits; n[k] must be the
-                            largest cap of segment k and segment 1's caps
-                            must be >= 1.  NULL: every service of segment k
-                            admits n_k.  Must be NULL for the other
-                            policies.                                     */
+  const int32_t *stage_caps; /* optional per-stage caps (Section 6, the
+                            batch-size cap tl spread over the stages).
+                            NESTED: stage_caps[s-1] >= 0 is the cap of
+                            decode stage s = 1..r_L; segment k takes the
+                            caps of its stages r_{k-1}+1..r_k in turn, one
+                            per service, as its threshold and the size of
+                            the cohort it admits; n[k] must be the largest
+                            cap of segment k and segment 1's caps must be
+                            >= 1.  WAIT: for each type j in turn, l'_j + 1
+                            caps >= 1 (its prefill and decode stages), taken
+                            in turn, one per service of the type, as its
+                            threshold and cohort size; n[j] must be the
+                            largest.  NULL: every service admits n_k (n_j).
+                            Must be NULL for the other policies.          */
 } ws_policy;
 
 /* One replica's random stream. */

@@ -142,6 +142,12 @@ sim_known_kernel(KArgs A) {
   uint32_t *hist = (uint32_t *)(A.ws + A.off_hist) + r * (int64_t)A.hist_stride;
 
   int32_t l[MT], lp[MT], nth[MT];
+  // WAIT per-stage caps (Section 6; general instantiation only): type j takes
+  // the caps of its l'_j + 1 stages in turn, one per service, as its
+  // threshold and cohort size; ncap[j] is the cap of its next service
+  const bool capped = TV && WAIT && J->has_caps != 0;
+  const int32_t *capt = (const int32_t *)(A.ws + J->off_caps);
+  int32_t coff[MT], ncap[MT];
   double lam[MT];
   uint32_t dmask[MT];
   uint32_t qoff[MT], doff[MT];  // ring offsets inside the replica block
@@ -151,6 +157,7 @@ sim_known_kernel(KArgs A) {
     l[j] = on ? J->l[j] : 0;
     lp[j] = on ? J->lp[j] : 1;
     nth[j] = on ? J->n[j] : 0;
+    coff[j] = j == 0 ? 0 : coff[j - 1] + lp[j - 1] + 1;
     lam[j] = on ? J->lambda[j] : 0.0;
     dmask[j] = on ? (1u << J->dcap_log2[j]) - 1u : 0u;
     qoff[j] = (uint32_t)J->off_q[on && WAIT ? j : 0];
@@ -261,6 +268,9 @@ sim_known_kernel(KArgs A) {
       pend[j] = (uint32_t)slot_i(A, S_LNEXT + j, r);
     }
   }
+#pragma unroll
+  for (int j = 0; j < MT; ++j)
+    ncap[j] = capped && j < m ? capt[coff[j] + (int32_t)(svc[j] % (uint32_t)(lp[j] + 1))] : nth[j];
   // caches of the ring ends; the gap rings start empty; profile cursors start
   // before the first piece
 #pragma unroll
@@ -585,7 +595,7 @@ sim_known_kernel(KArgs A) {
 #pragma unroll
         for (int j = 0; j < MT; ++j)
           if (j < m && (nowait ? (qt[j] != qh[j] || dt[j] != dh[j])
-                               : (qt[j] - qh[j]) >= (uint32_t)nth[j]))
+                               : (qt[j] - qh[j]) >= (uint32_t)ncap[j]))
             elig |= 1u << j;
       } else {
         uint32_t resident = 0;
@@ -633,7 +643,7 @@ sim_known_kernel(KArgs A) {
         const uint32_t c = svc[j] + 1u;
         // admissions: n_j (WAIT), at most n_j of those waiting (no-wait)
         const uint32_t waiting = qt[j] - qh[j];
-        const int32_t na = nowait && waiting < (uint32_t)nth[j] ? (int32_t)waiting : nth[j];
+        const int32_t na = nowait ? (waiting < (uint32_t)nth[j] ? (int32_t)waiting : nth[j]) : ncap[j];
         // each admission takes the cached head and loads the next one (ONE:
         // at most one admission, and the reload follows all admissions)
         for (int x = 0; x < (ONE ? min(na, 1) : na); ++x) {
@@ -762,6 +772,7 @@ sim_known_kernel(KArgs A) {
       // stage reached: WAIT counts services of the type, FCFS counts batches
       const uint32_t now = WAIT ? svc[j] + 1u : bidx;
       if (WAIT) svc[j] = now;
+      if (capped) ncap[j] = capt[coff[j] + (int32_t)(now % (uint32_t)(lp[j] + 1))];
       const uint32_t before = (dt[j] - dh[j]) - fresh[j];  // residents at launch
       uint32_t done = 0;
       // completions: processed at stage l'_j (fresh records never qualify)

@@ -5,7 +5,10 @@
 namespace wsim {
 
 hipError_t launch_known_wait(int max_m, const KArgs &A, hipStream_t s) {
-  if (A.any_trace || A.any_tv || A.btrace != nullptr) return launch_known_wait_tv(max_m, A, s);
+  // arrival lists, time-varying rates, per-batch traces and per-stage caps
+  // run in the general instantiation
+  if (A.any_trace || A.any_tv || A.btrace != nullptr || A.any_caps)
+    return launch_known_wait_tv(max_m, A, s);
   return launch_pol<WS_WAIT, false>(max_m, A, s);
 }
 

@@ -268,6 +268,7 @@ struct JobHost {
   JobDev d;
   int64_t reserve_tok;
   uint64_t edges_bytes, cdf_bytes, trace_bytes, rate_bytes, caps_bytes;
+  int64_t caps_count;  // per-stage caps in the job's table
 };
 
 struct Layout {
@@ -392,8 +393,9 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   int64_t reserve_tok = 0;
   if (kind != WS_FCFS && p.fcfs_chunk != 0)
     return fail_job(WS_EINVAL, idx, "fcfs_chunk applies to FCFS only");
-  if (kind != WS_NESTED_WAIT && p.stage_caps)
-    return fail_job(WS_EINVAL, idx, "stage_caps apply to Nested WAIT only");
+  if (p.stage_caps && !(kind == WS_NESTED_WAIT || p.kind == WS_WAIT))
+    return fail_job(WS_EINVAL, idx, "stage_caps apply to WAIT and Nested WAIT only");
+  int64_t caps_count = 0;
   // FCFS jobs the kernel for per-request lengths runs (drawn lengths, or
   // more types than the known-length kernels hold)
   const bool fdist = kind == WS_FCFS && (!known || c.m > WS_MAX_TYPES_KNOWN);
@@ -411,6 +413,18 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
     }
     if (fresh >= (int64_t(1) << 29))
       return fail_job(WS_EUNSUPPORTED, idx, "sum_j n_j (l_j + 1) must stay below 2^29");
+    if (p.stage_caps) {  // per type j, l'_j + 1 caps >= 1 whose largest is n_j
+      for (int j = 0; j < c.m; ++j) {
+        int32_t mx = 0;
+        for (int32_t st = 0; st <= c.out_len[j]; ++st) {
+          const int32_t cp = p.stage_caps[caps_count + st];
+          if (cp < 1) return fail_job(WS_EINVAL, idx, "WAIT stage caps must be >= 1");
+          mx = std::max(mx, cp);
+        }
+        if (mx != p.n[j]) return fail_job(WS_EINVAL, idx, "n[j] must be the largest stage cap of type j");
+        caps_count += c.out_len[j] + 1;
+      }
+    }
   } else if (kind == WS_FCFS) {
     if (!(p.fcfs_reserve >= 0.0 && p.fcfs_reserve < 1.0))
       return fail_job(WS_EINVAL, idx, "fcfs_reserve must be in [0,1)");
@@ -451,6 +465,7 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
         if (mx != p.n[k])
           return fail_job(WS_EINVAL, idx, "n[k] must be the largest stage cap of segment k");
       }
+      caps_count = maxL;
     }
   } else {
     return fail_job(WS_EINVAL, idx, "unknown policy kind");
@@ -518,7 +533,8 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
                     : 0;
   H.trace_bytes = c.n_trace > 0 ? align_up(16ull * (uint64_t)c.n_trace, 256) : 0;
   H.rate_bytes = align_up(8ull * (uint64_t)c.n_rate_pts * (uint64_t)(c.m + 1), 256);
-  H.caps_bytes = p.stage_caps ? align_up(4ull * (uint64_t)maxL, 256) : 0;
+  H.caps_count = caps_count;
+  H.caps_bytes = p.stage_caps ? align_up(4ull * (uint64_t)caps_count, 256) : 0;
   d.has_caps = p.stage_caps ? 1 : 0;
   // ring block of one replica
   uint64_t off = 0;
@@ -774,7 +790,7 @@ void build_image(const ws_job *jobs, int32_t n_jobs, const Layout &Lo, uint8_t *
       if (c.trace_out_len) std::memcpy(img + d.off_tr_len, c.trace_out_len, 4ull * c.n_trace);
     }
     if (Lo.jobs[i].caps_bytes)
-      std::memcpy(img + d.off_caps, jb.pol->stage_caps, 4ull * (uint64_t)d.seg_end[d.nseg - 1]);
+      std::memcpy(img + d.off_caps, jb.pol->stage_caps, 4ull * (uint64_t)Lo.jobs[i].caps_count);
     if (c.n_rate_pts > 0) {  // rate_t [P], then rate_f [m][P]
       std::memcpy(img + d.off_rate, c.rate_t, 8ull * c.n_rate_pts);
       std::memcpy(img + d.off_rate + 8ull * c.n_rate_pts, c.rate_f, 8ull * c.n_rate_pts * c.m);

@@ -223,11 +223,23 @@ def test_stage_caps_validation():
             wl.stage_caps = caps
         return [W.Job(wl, 0, W.ids(2))]
 
+    # WAIT: l'_j + 1 caps per type, each >= 1, n_j the largest; not WAIT-no-wait
+    wt = W.config2(replicas=2, rate_index=[3])[0].wl
+    wcaps = sum(([1] * (lp + 1) for lp in wt.out_len), [])
+    ok = W.Workload(**{**wt.__dict__, "stage_caps": wcaps})
+    assert B.workspace_bytes(B.JobArray([W.Job(ok, 0, W.ids(2))])) > 0
+    zero = W.Workload(**{**wt.__dict__, "stage_caps": [0] + wcaps[1:]})
+    assert _err([W.Job(zero, 0, W.ids(2))]).code == B.WS_EINVAL
+    big = W.Workload(**{**wt.__dict__, "stage_caps": [2] + wcaps[1:]})  # n_1 = 1 < 2
+    assert _err([W.Job(big, 0, W.ids(2))]).code == B.WS_EINVAL
+    nw = W.Workload(**{**wt.__dict__, "stage_caps": wcaps, "policy": "wait-nowait"})
+    assert _err([W.Job(nw, 0, W.ids(2))]).code == B.WS_EINVAL
+
     caps = list(W.P512MIX_CAPS_TL30)
     assert _err(with_caps(caps[:20] + [-1] + caps[21:])).code == B.WS_EINVAL
     assert _err(with_caps([0] + caps[1:])).code == B.WS_EINVAL  # segment 1 needs >= 1
     assert _err(with_caps(caps, n=[1, 1])).code == B.WS_EINVAL  # n_1 is not the largest
-    assert _err(with_caps(caps, policy="wait")).code == B.WS_EINVAL
+    assert _err(with_caps(caps, policy="wait")).code == B.WS_EINVAL  # wrong length for WAIT
 
 
 def test_host_allocation_failure_is_an_error_code():
