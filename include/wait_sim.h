@@ -106,11 +106,12 @@ typedef enum {
 
 /* Limits of the library. */
 #define WS_MAX_TYPES 64
-#define WS_MAX_TYPES_KNOWN 16 /* WAIT (both forms) takes at most this many
-                                 types; FCFS with known output lengths and
-                                 more types runs in the kernel for drawn
-                                 lengths (no chunked prefill or rate profile
-                                 there)                                     */
+#define WS_MAX_TYPES_KNOWN 16 /* the known-length kernels hold this many types
+                                 in registers; WAIT jobs with more run in a
+                                 kernel with per-type state in LDS, FCFS jobs
+                                 in the kernel for per-request lengths (both
+                                 with constant rates only; FCFS without
+                                 chunked prefill)                           */
 #define WS_MAX_SEGMENTS 16
 #define WS_MAX_HIST_EDGES 255
 #define WS_MAX_RATE_PTS 32

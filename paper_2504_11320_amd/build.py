@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SRC_NAMES = ("wait_sim_host.hip", "sim_known_wait.hip", "sim_known_fcfs.hip",
              "sim_nested.hip", "sim_known_wait_tv.hip", "sim_known_fcfs_tv.hip",
-             "sim_nested_tv.hip", "sim_fcfs_dist.hip")
+             "sim_nested_tv.hip", "sim_fcfs_dist.hip", "sim_wait_many.hip")
 SRCS = [os.path.join(CSRC, f) for f in SRC_NAMES]
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libwait_sim.so")

@@ -545,6 +545,7 @@ hipError_t launch_known_wait(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_known_fcfs(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_nested(int max_m, int max_seg, const KArgs &A, hipStream_t s);
 hipError_t launch_fcfs_dist(int max_m, const KArgs &A, hipStream_t s);
+hipError_t launch_wait_many(int max_m, const KArgs &A, hipStream_t s);
 // the kernels for launches with time-varying rates or an arrival list
 hipError_t launch_known_wait_tv(int max_m, const KArgs &A, hipStream_t s);
 hipError_t launch_known_fcfs_tv(int max_m, const KArgs &A, hipStream_t s);

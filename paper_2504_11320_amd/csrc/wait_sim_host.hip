@@ -401,10 +401,9 @@ int validate_job(const ws_job &jb, int idx, JobHost &H) {
   const bool fdist = kind == WS_FCFS && (!known || c.m > WS_MAX_TYPES_KNOWN);
   if (kind == WS_WAIT) {
     if (!known) return fail_job(WS_EINVAL, idx, "WAIT needs known output lengths");
-    if (c.m > WS_MAX_TYPES_KNOWN)
+    if (c.m > WS_MAX_TYPES_KNOWN && c.n_rate_pts > 0)
       return fail_job(WS_EUNSUPPORTED, idx,
-                      std::string("WAIT takes at most ") + std::to_string(WS_MAX_TYPES_KNOWN) +
-                          " types");
+                      "WAIT with more than 16 types takes constant rates only");
     if (!p.n) return fail_job(WS_EINVAL, idx, "thresholds required");
     int64_t fresh = 0;  // memory one batch can admit
     for (int j = 0; j < c.m; ++j) {
@@ -625,6 +624,7 @@ int make_layout(const ws_job *jobs, int32_t n_jobs, Layout &Lo, JobHost *storage
       any_tv |= launch_kind(jobs[i]) == pk && jobs[i].cfg->n_rate_pts > 0;
     const int64_t target = any_tv ? kTargetWavesNested : kTargetWaves;
     if (pk == kFcfsDist) lanes = 64;  // per-lane state in registers and LDS columns
+    if (pk == WS_WAIT && Lo.max_m[pk] > WS_MAX_TYPES_KNOWN) lanes = 16;  // LDS columns
     if (pk == WS_NESTED_WAIT) {
       // a group of lanes per replica: 64 / G replicas per wavefront
       lanes = 64 / nested_group_width(Lo.max_m[pk], Lo.max_seg);

@@ -72,8 +72,8 @@ def test_fcfs_reserve_validation():
 
 
 def test_type_limits():
-    """Nested WAIT and FCFS take up to 64 request types, WAIT up to 16 (more:
-    WS_EUNSUPPORTED); more than 64 is invalid for every policy."""
+    """Every policy takes up to 64 request types; more than 64 is invalid.
+    WAIT with more than 16 types takes constant rates only."""
     from paper_2504_11320_amd import binding as B
 
     def model(m, policy):
@@ -90,9 +90,12 @@ def test_type_limits():
     for policy in ("wait", "fcfs", "nested"):
         assert B.workspace_bytes(B.JobArray(model(16, policy))) > 0
         assert _err(model(65, policy)).code == B.WS_EINVAL
-    assert _err(model(17, "wait")).code == B.WS_EUNSUPPORTED
-    for policy in ("fcfs", "nested"):
+    for policy in ("wait", "fcfs", "nested"):
         assert B.workspace_bytes(B.JobArray(model(64, policy))) > 0
+    tv = model(17, "wait")
+    rt, rf = W.diurnal_profile(17, 1e6, points=5)
+    tv[0].wl.rate_t, tv[0].wl.rate_f = rt, rf
+    assert _err(tv).code == B.WS_EUNSUPPORTED
 
 
 def test_rate_profile_validation():

@@ -135,3 +135,41 @@ def test_many_types_nested_and_fcfs(B):
     jobs += [W.Job(known, 22, W.ids(9)), W.Job(drawn, 23, W.ids(9))]
     g, _ = check(B, jobs, 1500, "40/24-type Nested WAIT, 64-type FCFS")
     assert g["evictions"].sum() > 0
+
+
+def test_many_types_wait(B):
+    """WAIT beyond 16 types (per-type state in LDS columns): 20 and 64 types,
+    thresholds up to 3, tight memory; WAIT-no-wait with 24 types; per-stage
+    caps on 20 types; an arrival list with 40 types; against the oracle."""
+    rng = np.random.default_rng(65)
+    jobs = []
+    for m, pol in ((20, "wait"), (64, "wait"), (24, "wait-nowait")):
+        l, lam = _types(rng, m)
+        lp = [int(x) for x in rng.integers(1, 40, m)]
+        C = int(max(a + b for a, b in zip(l, lp)) * rng.uniform(2.0, 4.0))
+        wl = W.Workload(prompt_len=l, lam=[x * 3 for x in lam], d0=5.0, d1=0.01, C=C,
+                        policy=pol, n=[int(x) for x in rng.integers(1, 4, m)], out_len=lp,
+                        hist_edges=W.default_edges(5.0, 128), record_capacity=1 << 12)
+        jobs.append(W.Job(wl, 31, W.ids(10)))
+    l, lam = _types(rng, 20)
+    lp = [int(x) for x in rng.integers(1, 30, 20)]
+    caps, n = [], []
+    for lpj in lp:
+        seg = [2] * int(rng.integers(0, lpj + 1)) + [1] * (lpj + 1)
+        seg = seg[:lpj + 1]
+        caps += seg
+        n.append(max(seg))
+    C = int(max(a + b for a, b in zip(l, lp)) * 3)
+    jobs.append(W.Job(W.Workload(prompt_len=l, lam=lam, d0=5.0, d1=0.01, C=C, policy="wait",
+                                 n=n, out_len=lp, stage_caps=caps,
+                                 hist_edges=W.default_edges(5.0, 128), record_capacity=1 << 12),
+                      32, W.ids(10)))
+    g, _ = check(B, jobs, 1500, "WAIT with 20-64 types")
+    assert g["evictions"].sum() > 0
+    times = np.sort(rng.uniform(0.0, 400.0, 600))
+    types = rng.integers(0, 40, 600)
+    lp = [int(x) for x in rng.integers(1, 12, 40)]
+    wl = W.trace_workload("wait", [int(x) for x in rng.integers(1, 20, 40)], lp, 1.0, 0.01, 300,
+                          [int(x) for x in rng.integers(1, 3, 40)], times, types,
+                          record_capacity=1 << 10)
+    check(B, [W.Job(wl, 0, W.ids(3))], 400, "WAIT, 40 types, arrival list")
