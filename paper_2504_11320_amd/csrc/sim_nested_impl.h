@@ -7,8 +7,10 @@
 // replicas.  Lane
 // g of a group owns request type g (its arrival clock, draw counter and the
 // length of its pending arrival) and segment g (its service count, interior
-// count and memory, calendar, cohort slots and the cache of its youngest
-// interior prompt).  What a batch does segment by segment -- the entering
+// count and memory, calendar, cohort slots, the cache of its youngest
+// interior prompt, and its boundary queue's ends, memory and back record, in
+// registers: the survivors lane g-1 pushes are handed over by a lane shift
+// after the walk).  What a batch does segment by segment -- the entering
 // cohorts, the calendar links, the projected state Q+ of the pre-launch
 // repair, the completion walk -- runs on the segment lanes at once; the sums
 // over segments and types (batch tokens, Q+, the earliest arrival, the prefix
@@ -120,6 +122,11 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t v) {
   return ((uint64_t)dpp32<CTRL>((uint32_t)(v >> 32)) << 32) | dpp32<CTRL>((uint32_t)v);
 }
 
+// Shift by one lane inside the 16-lane rows: row_shl:1 (lane i takes lane
+// i+1) and row_shr:1 (lane i takes lane i-1); a row's end lane keeps 0.
+constexpr int kDppShl1 = 0x101;
+constexpr int kDppShr1 = 0x111;
+
 // Groups of 32 or 64 lanes combine the 16-lane rows with lane-index XOR
 // exchanges (16, then 32).
 template <int MASK>
@@ -177,6 +184,27 @@ __device__ __forceinline__ double group_min(double v) {
   });
   return __longlong_as_double((long long)r);
 }
+// The value of segment lane k+1 (seg_next) or k-1 (seg_prev) of the group;
+// the group's end lanes get values they do not use.
+template <int G>
+__device__ __forceinline__ uint32_t seg_next(uint32_t v) {
+  if constexpr (G <= 16)
+    return dpp32<kDppShl1>(v);
+  else
+    return (uint32_t)__shfl_down((int)v, 1u, G);
+}
+template <int G>
+__device__ __forceinline__ uint32_t seg_prev(uint32_t v) {
+  if constexpr (G <= 16)
+    return dpp32<kDppShr1>(v);
+  else
+    return (uint32_t)__shfl_up((int)v, 1u, G);
+}
+template <int G>
+__device__ __forceinline__ uint64_t seg_prev64(uint64_t v) {
+  return ((uint64_t)seg_prev<G>((uint32_t)(v >> 32)) << 32) | seg_prev<G>((uint32_t)v);
+}
+
 // The group's G bits of a wavefront ballot (bit g = group lane g).
 template <int G>
 __device__ __forceinline__ uint64_t group_bits(bool pred) {
@@ -223,11 +251,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   __shared__ double s_lam[MT];
   __shared__ int32_t s_l[MT], s_lp[MT];
   __shared__ SegConst s_seg[LT];
-  // per segment and replica: boundary-queue ring ends, boundary memory and
-  // back record (survivors of segment k-1 are pushed by lane k-1)
-  __shared__ uint32_t s_vh[LT][NR], s_vt[LT][NR];
-  __shared__ int64_t s_B[LT][NR];
-  __shared__ NRec s_vb[LT][NR];
   // completion latencies of one batch, per segment, in traversal order
   __shared__ double s_lat[LT][KL][NR];
   __shared__ int32_t s_latn[LT][NR];
@@ -380,6 +403,20 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   // segment lane: services, interior prompts and their memory
   uint32_t svc = 0, I = 0;
   int64_t M = 0;
+  // segment lane k >= 2 (1-based): its boundary queue's ring ends and memory,
+  // and what LIFO eviction needs of its back record (admission key, arrival
+  // with first-token mark, type word, length)
+  uint32_t vh = 0, vt = 0;
+  int64_t Bk = 0;
+  uint64_t vbkey = 0;
+  double vba = 0.0;
+  int32_t vbj = 0, vbL = 0;
+  auto set_back = [&](const NRec &b) __attribute__((always_inline)) {
+    vbkey = nrec_key(b);
+    vba = b.a_ft;
+    vbj = b.j;
+    vbL = b.L;
+  };
 
   if (!A.resume) {
     t = lat_area = ttft_area = lat_sum = mem_area = busy = 0.0;
@@ -404,10 +441,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     }
     // flags are replica-wide
     flags = group_or<G>(flags);
-    if (is_s) {
-      s_vh[k][q] = s_vt[k][q] = 0;
-      s_B[k][q] = 0;
-    }
     // calendar buckets start empty: each segment's buckets by the whole group
     for (int kk = 0; kk < L; ++kk) {
       uint32_t *b = (uint32_t *)(blk + s_seg[kk].off_bkt);
@@ -455,9 +488,9 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       svc = (uint32_t)slot_i(A, S_KSVC + k, r);
       I = (uint32_t)slot_i(A, S_KI + k, r);
       M = slot_i(A, S_KM + k, r);
-      s_B[k][q] = slot_i(A, S_KB + k, r);
-      s_vh[k][q] = (uint32_t)slot_i(A, S_KVH + k, r);
-      s_vt[k][q] = (uint32_t)slot_i(A, S_KVT + k, r);
+      Bk = slot_i(A, S_KB + k, r);
+      vh = (uint32_t)slot_i(A, S_KVH + k, r);
+      vt = (uint32_t)slot_i(A, S_KVT + k, r);
     }
   }
   gend = kj + 1u;  // draw rings start empty
@@ -476,9 +509,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   yi.L = 0;
   yi.c = 0;
   yi.next = kNil;
-  if (is_s && k >= 1 && s_vt[k][q] != s_vh[k][q])
-    s_vb[k][q] = load_nrec(vr + ((s_vt[k][q] - 1u) & vmask));
-  wave_lds_sync();
+  if (is_s && k >= 1 && vt != vh) set_back(load_nrec(vr + ((vt - 1u) & vmask)));
 
   // What the next launch reads first, loaded ahead (see prefetch below).
   uint4 pf_q0 = make_uint4(0u, 0u, 0u, 0u);
@@ -631,30 +662,30 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   auto evict_lifo = [&](int klo, bool allow_interior, bool &boundary)
                         __attribute__((always_inline)) -> int64_t {
     if (boundary) {
-      const bool cand = is_s && k >= 1 && s_vt[k][q] != s_vh[k][q];
-      const uint64_t key = cand ? nrec_key(s_vb[k][q]) : 0ull;
+      const bool cand = is_s && k >= 1 && vt != vh;
+      const uint64_t key = cand ? vbkey : 0ull;
       const uint64_t cb = group_bits<G>(cand);
       if (cb != 0) {
         const uint64_t mx = group_max<G>(key);
         const uint64_t wb = group_bits<G>(cand && key == mx);
         const int h = __builtin_ctzll(wb);  // keys are unique: one lane
         const bool me = gl == h;
-        // every lane reads the victim (the back of boundary queue h) and its
-        // charge l + r_{h-1} from LDS
-        const NRec rec = s_vb[h][q];
-        const int64_t gen = s_seg[h].entry - 1;
-        const int64_t ch = (int64_t)plen(rec.j) + gen;
-        wave_lds_sync();
+        // the victim is the back of boundary queue h: its charge l + r_{h-1}
+        // and lost tokens r_{h-1}, from lane h
+        const uint64_t cg = group_sum<G>(
+            me ? ((uint64_t)(uint32_t)rprev << 32) | (uint32_t)(plen(vbj) + rprev) : 0ull);
+        const int64_t ch = (int64_t)(uint32_t)cg, gen = (int64_t)(cg >> 32);
+        const double va = vba;
+        const int32_t vj = vbj, vL = vbL;
         if (me) {
-          const uint32_t vt = s_vt[k][q] - 1u;
-          s_vt[k][q] = vt;
-          if (vt != s_vh[k][q]) s_vb[k][q] = load_nrec(vr + ((vt - 1u) & vmask));  // the new back
-          s_B[k][q] -= ch;
+          vt -= 1u;
+          if (vt != vh) set_back(load_nrec(vr + ((vt - 1u) & vmask)));  // the new back
+          Bk -= ch;
         }
         Mres -= ch;
         evicts++;
         etok += gen;
-        push_q10(me, with_ft(rec.a_ft), rec.j, rec.L);  // it has produced r_{h-1} >= 1 tokens
+        push_q10(me, with_ft(va), vj, vL);  // it has produced r_{h-1} >= 1 tokens
         wave_lds_sync();
         return ch;
       }
@@ -691,10 +722,12 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       if (stage == 1 && !ft) dpend = 1;
     }
     // the victim's charge, lost tokens and first-token state, from its lane
-    ch = __shfl(ch, w, G);
-    const int32_t gd = __shfl(gen * 2 + dpend, w, G);
-    gen = gd >> 1;
-    dpend = gd & 1;
+    // (the other lanes hold zeros)
+    const uint64_t cg =
+        group_sum<G>(((uint64_t)(uint32_t)(gen * 2 + dpend) << 32) | (uint32_t)ch);
+    ch = (int32_t)(uint32_t)cg;
+    gen = (int32_t)(cg >> 33);
+    dpend = (int32_t)(cg >> 32) & 1;
     Mres -= ch;
     evicts++;
     fallback++;
@@ -716,10 +749,10 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   auto prefetch = [&]() __attribute__((always_inline)) {
     pf_q0_ok = qt != qh;
     if (gl == 0 && pf_q0_ok) pf_q0 = ((const uint4 *)q10)[qh & qmask];
-    if (is_s && (k == 0 || (int32_t)(s_vt[k][q] - s_vh[k][q]) >= ncap)) {
+    if (is_s && (k == 0 || (int32_t)(vt - vh) >= ncap)) {
       const uint32_t x = svc + 1u;  // the segment's next service
       bh = bk[fastmod(x, dmg, (uint32_t)delta)];
-      if (k >= 1) pf_vf = load_nrec(vr + (s_vh[k][q] & vmask));
+      if (k >= 1) pf_vf = load_nrec(vr + (vh & vmask));
       pf_ti = kNil;
       if (nrow == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1) {
         pf_ti = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
@@ -778,7 +811,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         break;
       }
       const bool ok = gl == 0 ? (int64_t)(qt - qh) >= (capped ? ncap : n0)
-                              : (is_s && (int32_t)(s_vt[k][q] - s_vh[k][q]) >= ncap);
+                              : (is_s && (int32_t)(vt - vh) >= ncap);
       const uint64_t okb = group_bits<G>(ok);
       if (okb & 1u) {
         kmax = __builtin_ctzll(~okb);  // lanes >= L never meet it
@@ -850,7 +883,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
           pre_l += plen(qr.j);
           if (!has_ft(qr.a_ft)) pend_new++;
         } else {
-          e = i == 0 ? pf_vf : load_nrec(vr + ((s_vh[k][q] + (uint32_t)i) & vmask));
+          e = i == 0 ? pf_vf : load_nrec(vr + ((vh + (uint32_t)i) & vmask));
           tok += (int64_t)plen(e.j) + ent;  // processed at stage r_{k-1} + 1
         }
         e.c = x;
@@ -880,7 +913,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
           eM += le + ent + 1;
         }
       }
-      if (k > 0) s_vh[k][q] += (uint32_t)ncap;  // still charged in s_B until the completion
+      if (k > 0) vh += (uint32_t)ncap;  // still charged in Bk until the completion
       // projected change of the segment's memory (no early completion)
       if (delta >= 2) {
         uint32_t T = 0, Tl = 0;
@@ -979,7 +1012,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       Mk = M + (int64_t)I + eM;  // every interior prompt advances
       Ik = I + eI;
       if (k > 0) {  // entering prompts leave the boundary queue's charge
-        s_B[k][q] -= eB;
+        Bk -= eB;
         dM -= eB;
       }
       node = bh;
@@ -989,6 +1022,12 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     // Walk the buckets served now.  A lane stops after KL completions until
     // the group's latency sum has taken them: the sum runs over segments in
     // order, each segment's latencies in traversal order.
+    // survivors join the back of segment k+1's boundary queue: its ring ends,
+    // from lane k+1; what was pushed goes to lane k+1 after the walk
+    const uint32_t vtn = seg_next<G>(vt), vhn = seg_next<G>(vh);
+    uint32_t npush = 0;
+    int32_t bpush = 0;
+    NRec vlast = yi;
     NRec crec = yi;
     if (node != kNil) {
       if (node == pend_idx)
@@ -1040,15 +1079,15 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
           } else {  // survivor joins the boundary queue of segment k+1
             NRec v = rec;
             v.a_ft = with_ft(rec.a_ft);
-            const uint32_t vt = s_vt[kn][q];
-            if (vt - s_vh[kn][q] <= vmaskn) {
-              vrn[vt & vmaskn] = v;
-              s_vt[kn][q] = vt + 1u;
-              s_vb[kn][q] = v;
+            const uint32_t vp = vtn + npush;
+            if (vp - vhn <= vmaskn) {
+              vrn[vp & vmaskn] = v;
+              npush++;
+              vlast = v;
             } else {
               lflags |= kFlagCap;  // bounded by construction; guards the ring
             }
-            s_B[kn][q] += le + rk;
+            bpush += (int32_t)(le + rk);
             dM += (int32_t)(le + rk);
           }
           rc[node].L = 0;  // no longer in the segment
@@ -1076,6 +1115,25 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       }
       if (group_bits<G>(node != kNil || nbuf != 0) == 0) break;
     }
+    {
+      const uint32_t np = seg_prev<G>(npush);
+      const int32_t bp = (int32_t)seg_prev<G>((uint32_t)bpush);
+      const uint64_t lk = seg_prev64<G>(nrec_key(vlast));
+      const double la = __longlong_as_double((long long)seg_prev64<G>(
+          (uint64_t)__double_as_longlong(vlast.a_ft)));
+      const int32_t lj = (int32_t)seg_prev<G>((uint32_t)vlast.j);
+      const int32_t lL = (int32_t)seg_prev<G>((uint32_t)vlast.L);
+      if (is_s && k >= 1) {
+        Bk += bp;
+        if (np != 0) {
+          vt += np;
+          vbkey = lk;
+          vba = la;
+          vbj = lj;
+          vbL = lL;
+        }
+      }
+    }
     Mres += group_sum32<G>((int32_t)(Mk - M) + dM);
     const int32_t nc = group_sum32<G>(dcomp);
     comps += nc;
@@ -1096,7 +1154,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     if constexpr (TV) {
       if (A.btrace != nullptr && batches < A.btrace_cap) {
         const int64_t res = group_sum<G>(
-            is_s ? (int64_t)I + (k > 0 ? (int64_t)(s_vt[k][q] - s_vh[k][q]) : 0) : 0);
+            is_s ? (int64_t)I + (k > 0 ? (int64_t)(vt - vh) : 0) : 0);
         if (gl == 0) {
           BatchRec br;
           br.t_launch = t_end - tau;
@@ -1155,9 +1213,9 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     put_i(A, S_KSVC + k, r, svc);
     put_i(A, S_KI + k, r, I);
     put_i(A, S_KM + k, r, M);
-    put_i(A, S_KB + k, r, is_s ? s_B[k][q] : 0);
-    put_i(A, S_KVH + k, r, is_s ? s_vh[k][q] : 0);
-    put_i(A, S_KVT + k, r, is_s ? s_vt[k][q] : 0);
+    put_i(A, S_KB + k, r, is_s ? Bk : 0);
+    put_i(A, S_KVH + k, r, is_s ? vh : 0);
+    put_i(A, S_KVT + k, r, is_s ? vt : 0);
   }
 }
 
