@@ -404,18 +404,28 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   uint32_t svc = 0, I = 0;
   int64_t M = 0;
   // segment lane k >= 2 (1-based): its boundary queue's ring ends and memory,
-  // and what LIFO eviction needs of its back record (admission key, arrival
-  // with first-token mark, type word, length)
+  // and what LIFO eviction needs of its back record and of the record before
+  // it (admission key, arrival with first-token mark, type word, length): an
+  // eviction takes the back and promotes the second at once, and the next
+  // second is loaded while the repair goes on
   uint32_t vh = 0, vt = 0;
   int64_t Bk = 0;
-  uint64_t vbkey = 0;
-  double vba = 0.0;
-  int32_t vbj = 0, vbL = 0;
+  uint64_t vbkey = 0, v2key = 0;
+  double vba = 0.0, v2a = 0.0;
+  int32_t vbj = 0, vbL = 0, v2j = 0, v2L = 0;
   auto set_back = [&](const NRec &b) __attribute__((always_inline)) {
     vbkey = nrec_key(b);
     vba = b.a_ft;
     vbj = b.j;
     vbL = b.L;
+  };
+  // the record before the back (valid while the queue holds two)
+  auto load_second = [&]() __attribute__((always_inline)) {
+    const NRec b = load_nrec(vr + ((vt - 2u) & vmask));
+    v2key = nrec_key(b);
+    v2a = b.a_ft;
+    v2j = b.j;
+    v2L = b.L;
   };
 
   if (!A.resume) {
@@ -510,6 +520,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   yi.c = 0;
   yi.next = kNil;
   if (is_s && k >= 1 && vt != vh) set_back(load_nrec(vr + ((vt - 1u) & vmask)));
+  if (is_s && k >= 1 && vt - vh >= 2u) load_second();
 
   // What the next launch reads first, loaded ahead (see prefetch below).
   uint4 pf_q0 = make_uint4(0u, 0u, 0u, 0u);
@@ -679,7 +690,13 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         const int32_t vj = vbj, vL = vbL;
         if (me) {
           vt -= 1u;
-          if (vt != vh) set_back(load_nrec(vr + ((vt - 1u) & vmask)));  // the new back
+          if (vt != vh) {  // the second is the new back
+            vbkey = v2key;
+            vba = v2a;
+            vbj = v2j;
+            vbL = v2L;
+            if (vt - vh >= 2u) load_second();
+          }
           Bk -= ch;
         }
         Mres -= ch;
@@ -1127,6 +1144,14 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         Bk += bp;
         if (np != 0) {
           vt += np;
+          if (np == 1) {  // the old back (if any) is the second
+            v2key = vbkey;
+            v2a = vba;
+            v2j = vbj;
+            v2L = vbL;
+          } else {
+            load_second();
+          }
           vbkey = lk;
           vba = la;
           vbj = lj;
