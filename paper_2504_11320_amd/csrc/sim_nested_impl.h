@@ -504,6 +504,13 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     }
   }
   gend = kj + 1u;  // draw rings start empty
+  // cohort slot of the segment's last service (svc mod delta_k), kept step by
+  // step: the next service's slot, its exit buckets and the terminal slot
+  // follow from it without a division
+  uint32_t xs = is_s ? fastmod(svc, dmg, (uint32_t)delta) : 0u;
+  auto slot_after = [&](uint32_t v) __attribute__((always_inline)) -> uint32_t {
+    return v + 1u == (uint32_t)delta ? 0u : v + 1u;
+  };
   // size of the cohort this segment admits at its next service
   int32_t ncap = cap_at(svc);
   // youngest live interior record of this segment and its index (kNil: not
@@ -768,11 +775,12 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     if (gl == 0 && pf_q0_ok) pf_q0 = ((const uint4 *)q10)[qh & qmask];
     if (is_s && (k == 0 || (int32_t)(vt - vh) >= ncap)) {
       const uint32_t x = svc + 1u;  // the segment's next service
-      bh = bk[fastmod(x, dmg, (uint32_t)delta)];
+      const uint32_t nx = slot_after(xs);
+      bh = bk[nx];
       if (k >= 1) pf_vf = load_nrec(vr + (vh & vmask));
       pf_ti = kNil;
       if (nrow == 1 && delta >= 2 && (int64_t)x - (delta - 1) >= 1) {
-        pf_ti = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
+        pf_ti = slot_after(nx);  // x - (delta - 1) = x + 1 mod delta
         pf_tr = *(const uint2 *)((const uint8_t *)(rc + pf_ti) + 16);
       }
     }
@@ -878,7 +886,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     // prompts entering segment 1 now (the cap of its service)
     const int32_t n0c = capped ? __shfl(ncap, 0, G) : n0;
     if (served) {
-      const uint32_t slot = fastmod(x, dmg, (uint32_t)delta);
+      const uint32_t slot = slot_after(xs);
       tok = M;  // every interior prompt is processed at its stage
       sel = (int64_t)I + ncap;
       uint32_t suml = 0;
@@ -905,7 +913,9 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         }
         e.c = x;
         const int32_t pexit = e.L < rk ? e.L : rk;
-        const uint32_t b = fastmod(x + (uint32_t)(pexit - ent), dmg, (uint32_t)delta);
+        // entry stage <= pexit <= r_k: the exit is 0..delta-1 services ahead
+        uint32_t b = slot + (uint32_t)(pexit - ent);
+        b = b >= (uint32_t)delta ? b - (uint32_t)delta : b;
         const uint32_t idx = slot * (uint32_t)nrow + (uint32_t)i;
         // (the bucket served now was prefetched as bh: the same head)
         e.next = b == slot ? bh : bk[b];
@@ -941,7 +951,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
             T = trL != 0 ? 1u : 0u;
             Tl = trL != 0 ? (uint32_t)plen(trj) : 0u;
           } else {
-            const uint32_t ts = fastmod(x - (uint32_t)(delta - 1), dmg, (uint32_t)delta);
+            const uint32_t ts = slot_after(slot);  // x - (delta - 1) = x + 1 mod delta
             for (int32_t i = 0; i < nrow; ++i) {
               // j and L (the second half's first two words) in one load
               const uint2 jl = *(const uint2 *)((const uint8_t *)(rc + ts * (uint32_t)nrow +
@@ -1038,7 +1048,8 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         dM -= eB;
       }
       node = bh;
-      bk[fastmod(x, dmg, (uint32_t)delta)] = kNil;
+      xs = slot_after(xs);  // the slot of service x
+      bk[xs] = kNil;
     }
     wave_lds_sync();
     // Walk the buckets served now.  A lane stops after KL completions until
