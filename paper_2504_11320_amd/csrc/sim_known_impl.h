@@ -44,9 +44,15 @@ namespace {
 // ONE: WAIT with every threshold n_j = 1 (at most one admission and one
 // completion per type and batch), which defers ring reloads to the ends of
 // the admission and completion phases.
+// Wavefronts of at most 16 replicas with up to 3 types run two per SIMD
+// (their LDS allows it), so their register budget is stated to the compiler:
+// one register past it would halve their occupancy.
+template <int MT, int LN>
+constexpr int kKnownMinWaves = MT <= 3 && LN <= 16 ? 2 : 1;
+
 template <int MT, int POL, bool TRACE, int LN, bool TV, bool ONE>
-__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 2)))
-sim_known_kernel(KArgs A) {
+__global__ void __launch_bounds__(64)
+    __attribute__((amdgpu_waves_per_eu(kKnownMinWaves<MT, LN>, 2))) sim_known_kernel(KArgs A) {
   constexpr bool WAIT = POL == WS_WAIT;
   // Inter-arrival gaps are drawn ahead of use by the whole wavefront at once
   // (64 draws per pass, no divergence) into a ring of GR gaps per type and
