@@ -82,6 +82,11 @@ def test_sample_path_identities(oracle_lib, data):
     assert abs(math.fsum((c - a)[done]) - r["lat_completed_sum"]) <= 1e-10 * max(
         1.0, r["lat_completed_sum"])
     assert r["hist"].sum() == r["completions"]
+    # latency histogram (reading A21): bin = number of edges <= latency, here by
+    # numpy's binary search over every completed request's latency
+    edges = np.asarray(wl.hist_edges, dtype=np.float64)
+    bins = np.searchsorted(edges, (c - a)[done], side="right")
+    assert np.array_equal(np.bincount(bins, minlength=len(edges) + 1), r["hist"])
     # first token is produced no later than completion
     assert np.all(f[done] <= c[done]) and np.all(f[done] >= 0)
     # iteration time identity
@@ -190,3 +195,72 @@ def test_nested_eviction_probability_bound(oracle_lib):
     assert r["t_end"].max() <= zT
     frac = np.mean(r["evictions"] > 0)
     assert frac <= 0.1
+
+
+def test_histogram_bin_at_an_edge(oracle_lib):
+    """Reading A21: a latency equal to an edge counts that edge (bin = number
+    of edges <= latency), so it lands in the bin above the edge."""
+    import dataclasses
+    O = oracle_lib
+    # one prompt arriving at 0 under WAIT-no-wait (served while resident), tau = 1 ms:
+    # it passes its l'_j + 1 = 4 stages in four batches, latency 4 ms
+    base = Workload(prompt_len=[4], lam=[0.0], d0=1.0, d1=0.0, C=1000, policy="wait-nowait",
+                    n=[1], out_len=[3], hist_edges=np.array([0.5]), record_capacity=16,
+                    trace=(np.array([0.0]), np.array([0], np.int32), np.array([3], np.int32)))
+    r = O.run_one(base, 0, 0, 10, rlog_cap=4)
+    assert r["completions"] == 1
+    lat = r["req_done"][0] - r["req_arr"][0]
+    assert lat == 4.0
+    for edges, want in (([lat - 0.5, lat, lat + 0.5], 2), ([lat], 1),
+                        ([np.nextafter(lat, np.inf)], 0), ([np.nextafter(lat, -np.inf)], 1)):
+        wl = dataclasses.replace(base, hist_edges=np.array(edges, dtype=np.float64))
+        h = O.run_one(wl, 0, 0, 10)["hist"]
+        assert h.sum() == 1 and h[want] == 1, (edges, h)
+
+
+HIST_MUTATIONS = {
+    # an edge equal to the latency not counted
+    "strict": ("while (b < c->n_edges && c->edges[b] <= lat) b++;",
+               "while (b < c->n_edges && c->edges[b] < lat) b++;"),
+    # the index of the last edge <= latency instead of their number
+    "last_edge": ("  return b;\n}\n\nstatic void complete(",
+                  "  return b > 0 ? b - 1 : 0;\n}\n\nstatic void complete("),
+}
+
+
+def _hist_mismatch(O, library) -> bool:
+    """Run the edge-equality case and a random WAIT path through `library`
+    and report whether any histogram disagrees with the definition."""
+    import dataclasses
+    base = Workload(prompt_len=[4], lam=[0.0], d0=1.0, d1=0.0, C=1000, policy="wait-nowait",
+                    n=[1], out_len=[3], hist_edges=np.array([4.0]), record_capacity=16,
+                    trace=(np.array([0.0]), np.array([0], np.int32), np.array([3], np.int32)))
+    h = O.run_one(base, 0, 0, 10, library=library)["hist"]
+    if h.sum() != 1 or h[1] != 1:
+        return True
+    wl = Workload(prompt_len=[16, 40], lam=[0.3, 0.2], d0=2.0, d1=0.01, C=4000, policy="wait",
+                  n=[2, 1], out_len=[6, 20], hist_edges=default_edges(2.0, 96),
+                  record_capacity=1 << 14)
+    r = O.run_one(wl, 3, 5, 400, rlog_cap=1 << 14, library=library)
+    a, c = r["req_arr"][:r["arrivals"]], r["req_done"][:r["arrivals"]]
+    done = c >= 0
+    bins = np.searchsorted(wl.hist_edges, (c - a)[done], side="right")
+    return not np.array_equal(np.bincount(bins, minlength=len(wl.hist_edges) + 1), r["hist"])
+
+
+@pytest.mark.parametrize("name", sorted(HIST_MUTATIONS))
+def test_histogram_pins_reject_planted_mistakes(oracle_lib, tmp_path, name):
+    import os
+    import subprocess
+    O = oracle_lib
+    assert not _hist_mismatch(O, None)
+    src = open(O.SRC).read()
+    old, new = HIST_MUTATIONS[name]
+    assert src.count(old) == 1, name
+    path = tmp_path / f"wait_oracle_{name}.c"
+    path.write_text(src.replace(old, new))
+    lib = tmp_path / f"liboracle_{name}.so"
+    subprocess.run(["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math",
+                    "-fPIC", "-shared", "-I", os.path.dirname(O.SRC), "-o", str(lib),
+                    str(path), "-lpthread", "-lm"], check=True)
+    assert _hist_mismatch(O, O.load(str(lib))), name
