@@ -986,6 +986,10 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     wave_lds_sync();
 
     // ---- pre-launch repair on the projected state ----------------------------
+    // The repairs and the walk chase dependent loads: at raised priority the
+    // wavefront issues ahead of the other one on its SIMD, so each of its
+    // next loads leaves sooner.
+    __builtin_amdgcn_s_setprio(2);
     bool bnd_pre = true;
     while (mplus > C) {
       const int64_t freed = evict_lifo(kmax, false, bnd_pre);
@@ -998,6 +1002,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       mplus -= freed;
     }
     if (mplus > C) flags |= kFlagOverflow;
+    __builtin_amdgcn_s_setprio(0);
     // the walk's first record, loaded only now: memory operations complete in
     // issue order, so a load issued before the repair would hold up the
     // repair's own short loads (the pre-launch repair leaves the served
@@ -1070,6 +1075,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       else
         crec = load_nrec(rc + node);
     }
+    __builtin_amdgcn_s_setprio(2);  // the walk (see the pre-launch repair)
     int32_t nbuf = 0;
     // a bucket lists at most the segment's delta_k * n_k records: a longer
     // walk could only follow a corrupted link, so it stops the replica
@@ -1175,6 +1181,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         }
       }
     }
+    __builtin_amdgcn_s_setprio(0);
     Mres += group_sum32<G>((int32_t)(Mk - M) + dM);
     const int32_t nc = group_sum32<G>(dcomp);
     comps += nc;
@@ -1188,10 +1195,12 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     prefetch();
 
     // ---- repair: boundary prompts first, then interior prompts -------------
+    __builtin_amdgcn_s_setprio(2);
     bool bnd_post = true;
     while (Mres > C) {
       if (evict_lifo(0, true, bnd_post) == 0) break;
     }
+    __builtin_amdgcn_s_setprio(0);
     if constexpr (TV) {
       if (A.btrace != nullptr && batches < A.btrace_cap) {
         const int64_t res = group_sum<G>(
