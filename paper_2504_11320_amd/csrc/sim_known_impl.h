@@ -745,6 +745,10 @@ __global__ void __launch_bounds__(64)
     const int64_t N0 = N, U0 = U;
 
     // ---- arrivals during the batch ------------------------------------
+    // This loop and the repair chase dependent LDS reads one event at a time:
+    // at raised priority the wavefront issues ahead of the other one on its
+    // SIMD (launches of 16 replicas per wavefront run two per SIMD).
+    __builtin_amdgcn_s_setprio(2);
     for (;;) {
       if (flags & kFlagCap) break;  // the replica stops at its next decision
       int jn;
@@ -754,6 +758,7 @@ __global__ void __launch_bounds__(64)
       lat_area += t_end - ta;
       ttft_area += t_end - ta;
     }
+    __builtin_amdgcn_s_setprio(0);
     lat_area += (double)N0 * tau;
     ttft_area += (double)U0 * tau;
     mem_area += (double)m_launch * tau;
@@ -835,6 +840,7 @@ __global__ void __launch_bounds__(64)
       part_j = -1;
       part_pp = 0;
     }
+    __builtin_amdgcn_s_setprio(2);
     while (Mres > C) {
       int jb = -1;
       uint32_t bb = 0, bp = 0;
@@ -856,6 +862,7 @@ __global__ void __launch_bounds__(64)
       for (int j = 0; j < MT; ++j)
         if (jb == j) evict(j);
     }
+    __builtin_amdgcn_s_setprio(0);
     if constexpr (TV) {
       if (A.btrace != nullptr && batches < A.btrace_cap) {
         BatchRec br;
