@@ -229,8 +229,11 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   constexpr int LT = G;       // segment slots
   // Inter-arrival gaps and output lengths are drawn ahead of use by the
   // whole wavefront at once into a ring of GR draws per type and replica; a
-  // type lane whose ring runs dry draws for itself.
-  constexpr int GR = 4;
+  // type lane whose ring runs dry draws for itself.  Eight draws keep refill
+  // passes (whose table lookups wait for every outstanding memory operation)
+  // rare and still leave LDS for two wavefronts per SIMD; the general
+  // instantiation (more LDS per draw) and 64-lane groups keep four.
+  constexpr int GR = TV || G > 32 ? 4 : 8;
   constexpr int GU = GR / 2;         // draws added per refill
   constexpr uint32_t kLow = GU / 2;  // a ring below this triggers a refill
   // completion latencies buffered per segment lane before they are summed
