@@ -175,6 +175,10 @@ __global__ void __launch_bounds__(64)
   uint32_t kk[MT], qh[MT], qt[MT], dh[MT], dt[MT], svc[MT], pend[MT];
   uint32_t gend[MT];  // gaps of arrivals kk+1 .. gend-1 are in the ring
   uint32_t wv[MT];    // deque records dt-wv .. dt-1 are also in the LDS window
+  // WAIT with general thresholds, constant rates: the records of deque j
+  // admitted in the current batch and still resident (the last fr[j] ones)
+  constexpr bool BULK = WAIT && !ONE && !TV;
+  uint32_t fr[MT];
   int32_t Mj[MT];  // resident memory per type (< 2C <= 2^31)
   // Queue heads.  WAIT: the head of queue j is qpu[j] if bit j of qsrc is
   // set (pushed into an empty queue), else qld[j] (loaded when the previous
@@ -284,6 +288,7 @@ __global__ void __launch_bounds__(64)
     if constexpr (TV) s_cur[j][tx] = -1;
     gend[j] = kk[j] + 1u;
     wv[j] = 0;
+    fr[j] = 0;
     // unconditional loads: a slot past the tail holds a stale record that is
     // never used (the masks keep every index inside its ring)
     if (WAIT) qld[j] = qring(j)[qh[j] & qmask];
@@ -452,6 +457,50 @@ __global__ void __launch_bounds__(64)
     } else {
       push_fcfs(a_ft, j, lp[j]);
     }
+    if constexpr (BULK) fr[j] -= fr[j] > 0u ? 1u : 0u;  // the back was admitted now
+  };
+  // LIFO eviction of the last k records of deque j (static j, WAIT), all
+  // admitted in the current batch: they share the key (batch, type), are at
+  // stage 1 with the charge l_j + 1 and lose no decode token, so they leave
+  // back first, one after another as single evictions would, and join the
+  // tail of queue j in that order with their own first-token flags.
+  auto evict_fresh = [&](int j, uint32_t k) __attribute__((always_inline)) {
+    const int32_t ch = l[j] + 1;
+    const uint32_t h = qh[j], tq2 = qt[j], t0 = dt[j];
+    double* qr = qring(j);
+    uint32_t nopend = 0;
+    double a0 = 0.0;
+    for (uint32_t i = 0; i < k; ++i) {
+      const uint32_t p = t0 - 1u - i;
+      const double a = i < wv[j] ? s_win[j][p % WB][tx].a_ft : dring(j)[p & dmask[j]].a_ft;
+      nopend += has_ft(a) ? 0u : 1u;
+      a0 = i == 0 ? a : a0;
+      // unconditional, as in evict: a full queue ends the replica
+      qr[(tq2 + i) & qmask] = a;
+    }
+    flags |= tq2 + k - h > rec_cap ? kFlagCap : 0u;
+    const bool first = tq2 == h;  // the queue was empty: the first one is its head
+    qpu[j] = first ? a0 : qpu[j];
+    qsrc |= (first ? 1u : 0u) << j;
+    qt[j] = tq2 + k;
+    const uint32_t tq = t0 - k;
+    dt[j] = tq;
+    fr[j] -= k;
+    wv[j] = wv[j] > k ? wv[j] - k : 0u;
+    if (tq != dh[j]) {  // the new back record
+      if (wv[j] < 1u) {  // not in the window: copy it in from HBM
+        s_win[j][(tq - 1u) % WB][tx] = dring(j)[(tq - 1u) & dmask[j]];
+        wv[j] = 1u;
+      }
+      const DRec b = s_win[j][(tq - 1u) % WB][tx];
+      ba[j] = b.a_ft;
+      bkb[j] = b.kb;
+      bkc[j] = b.kc;
+    }
+    pend[j] -= nopend;
+    Mj[j] -= (int32_t)k * ch;
+    Mres -= (int32_t)k * ch;
+    evicts += k;
   };
 
   // ---- arrivals ---------------------------------------------------------------
@@ -833,6 +882,10 @@ __global__ void __launch_bounds__(64)
     // ---- repair: evict the most recently admitted resident ------------
     // (FCFS: a partially prefilled prompt first; it restarts from scratch)
     const int64_t bt_ev0 = evicts;
+    if constexpr (BULK) {
+#pragma unroll
+      for (int j = 0; j < MT; ++j) fr[j] = fresh[j];
+    }
     if (!WAIT && part_j >= 0 && Mres > C) {
       Mres -= part_pp;
       evicts++;
@@ -857,10 +910,21 @@ __global__ void __launch_bounds__(64)
       if (jb < 0) break;
       // one unrolled body per type, each with static register indices; the
       // lanes of a wavefront mostly evict the same type, so usually one body
-      // runs
+      // runs.  Records admitted in this batch leave as many at a time as the
+      // memory in excess needs.
 #pragma unroll
-      for (int j = 0; j < MT; ++j)
-        if (jb == j) evict(j);
+      for (int j = 0; j < MT; ++j) {
+        if (jb != j) continue;
+        if constexpr (BULK) {
+          if (fr[j] >= 2u) {
+            const int32_t ch = l[j] + 1;
+            const uint32_t need = (uint32_t)((Mres - C + ch - 1) / ch);
+            evict_fresh(j, need < fr[j] ? need : fr[j]);
+            continue;
+          }
+        }
+        evict(j);
+      }
     }
     __builtin_amdgcn_s_setprio(0);
     if constexpr (TV) {

@@ -90,3 +90,27 @@ def test_unit_thresholds(m):
     idx = np.concatenate([R * k + picks.astype(np.int64) for k in range(len(jobs))])
     for k in g:
         assert np.array_equal(g[k][idx], small[k]), k
+
+
+def test_large_cohorts_under_tight_memory():
+    """WAIT and WAIT-no-wait with thresholds up to 16 and memory just above
+    the largest request: a service admits a whole cohort and the repair
+    evicts most of it again, several prompts of one cohort at a time; every
+    field against the oracle."""
+    B = sim_module()
+    rng = np.random.default_rng(4242)
+    jobs = []
+    for i in range(16):
+        m = int(rng.integers(1, 4))
+        l = [int(x) for x in rng.integers(1, 60, m)]
+        lp = [int(x) for x in rng.integers(1, 30, m)]
+        n = [int(x) for x in rng.integers(2, 17, m)]
+        C = int(max(a + b for a, b in zip(l, lp)) * rng.uniform(1.0, 2.5))
+        wl = W.Workload(prompt_len=l, lam=[float(x) for x in rng.uniform(0.1, 1.0, m)],
+                        d0=float(rng.uniform(0.5, 3.0)), d1=float(rng.uniform(0.0, 0.02)),
+                        C=C, policy="wait" if i % 4 else "wait-nowait", n=n, out_len=lp,
+                        hist_edges=W.default_edges(1.0, 64), record_capacity=1 << 16)
+        jobs.append(W.Job(wl, int(rng.integers(0, 2**63)), W.ids(int(rng.integers(8, 40)))))
+    g, _ = check(B, jobs, 1500, "WAIT, cohorts up to 16, tight memory")
+    assert g["evictions"].sum() > g["batches"].sum()  # more than one eviction per batch
+    assert (g["flags"] == 0).all()
