@@ -699,15 +699,67 @@ __global__ void __launch_bounds__(64)
         // admissions: n_j (WAIT), at most n_j of those waiting (no-wait)
         const uint32_t waiting = qt[j] - qh[j];
         const int32_t na = nowait ? (waiting < (uint32_t)nth[j] ? (int32_t)waiting : nth[j]) : ncap[j];
-        // each admission takes the cached head and loads the next one (ONE:
-        // at most one admission, and the reload follows all admissions)
-        for (int x = 0; x < (ONE ? min(na, 1) : na); ++x) {
-          const double a_ft = ((qsrc >> j) & 1u) ? qpu[j] : qld[j];
-          qsrc &= ~(1u << j);
-          qh[j]++;
-          if (!ONE) qld[j] = qring(j)[qh[j] & qmask];  // the next head
-          dpush(j, a_ft, bidx, c);
-          pendnew[j] += has_ft(a_ft) ? 0u : 1u;
+        if constexpr (BULK) {
+          // a cohort of na records (same batch and service): copied from the
+          // queue ring (the cached head, then the records behind it, read KA
+          // at a time) into the deque ring and the LDS window; the cached
+          // ends of the deque are set once
+          const double head = ((qsrc >> j) & 1u) ? qpu[j] : qld[j];
+          const double *qr = qring(j);
+          DRec *dr = dring(j);
+          const uint32_t d0 = dt[j], h0 = qh[j];
+          uint32_t nopend = 0;
+          double a1 = 0.0, alast = head;
+          for (int x = 0; x < na; x += 4) {
+            double nx[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              nx[u] = (x + u) == 0 ? head : qr[(h0 + (uint32_t)(x + u)) & qmask];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              if (x + u < na) {
+                DRec rec;
+                rec.a_ft = nx[u];
+                rec.kb = bidx;
+                rec.kc = c;
+                dr[(d0 + (uint32_t)(x + u)) & dmask[j]] = rec;
+                s_win[j][(d0 + (uint32_t)(x + u)) % WB][tx] = rec;
+                nopend += has_ft(nx[u]) ? 0u : 1u;
+                a1 = x + u == 1 ? nx[u] : a1;
+                alast = nx[u];
+              }
+            }
+          }
+          if (na > 0) {
+            qsrc &= ~(1u << j);
+            const bool was_empty = d0 == dh[j], was_one = d0 == dh[j] + 1u;
+            fa[j] = was_empty ? head : fa[j];
+            fadm[j] = was_empty ? c : fadm[j];
+            const bool sec = (was_empty && na >= 2) || was_one;
+            const double sa = was_one ? head : a1;
+            s1pa[j] = sec ? sa : s1pa[j];
+            s1padm[j] = sec ? c : s1padm[j];
+            s1src |= (sec ? 1u : 0u) << j;
+            ba[j] = alast;
+            bkb[j] = bidx;
+            bkc[j] = c;
+            dt[j] = d0 + (uint32_t)na;
+            wv[j] = wv[j] + (uint32_t)na < (uint32_t)WB ? wv[j] + (uint32_t)na : (uint32_t)WB;
+            qh[j] = h0 + (uint32_t)na;
+            qld[j] = qr[qh[j] & qmask];  // the next head
+            pendnew[j] += nopend;
+          }
+        } else {
+          // each admission takes the cached head and loads the next one (ONE:
+          // at most one admission, and the reload follows all admissions)
+          for (int x = 0; x < (ONE ? min(na, 1) : na); ++x) {
+            const double a_ft = ((qsrc >> j) & 1u) ? qpu[j] : qld[j];
+            qsrc &= ~(1u << j);
+            qh[j]++;
+            if (!ONE) qld[j] = qring(j)[qh[j] & qmask];  // the next head
+            dpush(j, a_ft, bidx, c);
+            pendnew[j] += has_ft(a_ft) ? 0u : 1u;
+          }
         }
         fresh[j] = (uint32_t)na;
         bt_pre += na;
