@@ -946,6 +946,13 @@ __global__ void __launch_bounds__(64)
       part_pp = 0;
     }
     __builtin_amdgcn_s_setprio(2);
+    if constexpr (ONE) {
+      // this batch's admissions (at most one per type) hold the largest keys,
+      // the type breaking the tie: they go first, highest type first
+#pragma unroll
+      for (int j = MT - 1; j >= 0; --j)
+        if (fresh[j] != 0u && Mres > C) evict(j);
+    }
     while (Mres > C) {
       int jb = -1;
       uint32_t bb = 0, bp = 0;
