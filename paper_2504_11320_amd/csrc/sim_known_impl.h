@@ -953,6 +953,23 @@ __global__ void __launch_bounds__(64)
       for (int j = MT - 1; j >= 0; --j)
         if (fresh[j] != 0u && Mres > C) evict(j);
     }
+    if constexpr (BULK) {
+      // this batch's cohorts hold the largest keys, the type breaking the
+      // tie: they go first, highest type first, each as many at a time as
+      // the memory in excess needs
+#pragma unroll
+      for (int j = MT - 1; j >= 0; --j) {
+        if (fr[j] != 0u && Mres > C) {
+          const int32_t ch = l[j] + 1;
+          const uint32_t need = (uint32_t)((Mres - C + ch - 1) / ch);
+          const uint32_t k = need < fr[j] ? need : fr[j];
+          if (k == 1u)
+            evict(j);
+          else
+            evict_fresh(j, k);
+        }
+      }
+    }
     while (Mres > C) {
       int jb = -1;
       uint32_t bb = 0, bp = 0;
