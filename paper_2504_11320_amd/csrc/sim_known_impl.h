@@ -953,6 +953,13 @@ __global__ void __launch_bounds__(64)
       for (int j = MT - 1; j >= 0; --j)
         if (fresh[j] != 0u && Mres > C) evict(j);
     }
+    if constexpr (WAIT && TV) {
+      // this batch's cohorts hold the largest keys, the type breaking the
+      // tie: they go first, highest type first
+#pragma unroll
+      for (int j = MT - 1; j >= 0; --j)
+        for (uint32_t x = 0; x < fresh[j] && Mres > C; ++x) evict(j);
+    }
     if constexpr (BULK) {
       // this batch's cohorts hold the largest keys, the type breaking the
       // tie: they go first, highest type first, each as many at a time as
