@@ -127,6 +127,20 @@ def build_sanitized(out: str) -> str:
     return out
 
 
+def build_order_checked(out: str) -> str:
+    """The oracle with the position-order counters of its Nested WAIT repairs
+    (OR_CHECK_POSITION_ORDER): oracle_order_checks(kind) and
+    oracle_order_misses(kind), kind 0 for boundary victims, 1 for interior."""
+    cmd = ["gcc", "-O2", "-std=gnu11", "-Wall", "-ffp-contract=off", "-fno-fast-math",
+           "-DOR_CHECK_POSITION_ORDER", "-fPIC", "-shared", "-o", out, SRC, "-lpthread", "-lm"]
+    subprocess.run(cmd, check=True)
+    L = load(out)
+    for f in (L.oracle_order_checks, L.oracle_order_misses):
+        f.argtypes = [C.c_int]
+        f.restype = C.c_long
+    return L
+
+
 def lib():
     global _lib
     if _lib is None:
@@ -209,9 +223,10 @@ def _to_dict(res_arr, hist):
     return out
 
 
-def run(wl, seed: int, replica_ids, horizon: int, threads: int = 0) -> dict:
-    """Simulate every replica of a workload; returns arrays per field."""
-    L = lib()
+def run(wl, seed: int, replica_ids, horizon: int, threads: int = 0, library=None) -> dict:
+    """Simulate every replica of a workload; returns arrays per field.
+    `library`: another build of the oracle (a handle from load())."""
+    L = library if library is not None else lib()
     pin = _Pinned(wl)
     ids = np.ascontiguousarray(np.asarray(replica_ids, dtype=np.uint32))
     n = len(ids)

@@ -675,6 +675,43 @@ static int64_t projected_charge(const or_config *c, int64_t l, int32_t k,
 
 static void evict(sim_t *S, int64_t r, int fallback);
 
+/* Test builds only (-DOR_CHECK_POSITION_ORDER): under Nested WAIT the most
+ * recently admitted prompt also stands first in position order (segment 1,
+ * boundary queue 2, segment 2, ...): cohorts enter a segment from the front
+ * of its FIFO queue, leave it after the same number of services, and their
+ * survivors join the next queue in admission order.  The GPU kernels choose
+ * the LIFO victim by that position alone; these counters confirm, at every
+ * eviction the repairs make, that the victim found by key comparison lies in
+ * the lowest non-empty boundary queue (boundary victims) or in the lowest
+ * segment holding a candidate (interior victims).  Not part of the model. */
+#ifdef OR_CHECK_POSITION_ORDER
+static long g_order_checks[2], g_order_misses[2];
+long oracle_order_checks(int interior) { return __atomic_load_n(&g_order_checks[interior], __ATOMIC_RELAXED); }
+long oracle_order_misses(int interior) { return __atomic_load_n(&g_order_misses[interior], __ATOMIC_RELAXED); }
+static void order_check(const sim_t *S, int64_t best, int interior, int only_unselected) {
+  const or_config *c = S->cfg;
+  int32_t low = 1 << 30;
+  if (interior) {
+    for (int64_t x = 0; x < S->res.len; x++) {
+      const req_t *r = &S->R[S->res.v[x]];
+      if (!(only_unselected && r->sel) && r->seg < low) low = r->seg;
+    }
+  } else {
+    for (int32_t k = 2; k <= c->nseg && low > k; k++)
+      for (int64_t x = 0; x < S->bnd[k].len; x++)
+        if (!(only_unselected && S->R[dq_at(&S->bnd[k], x)].sel)) {
+          low = k;
+          break;
+        }
+  }
+  __atomic_fetch_add(&g_order_checks[interior], 1, __ATOMIC_RELAXED);
+  if (S->R[best].seg != low) __atomic_fetch_add(&g_order_misses[interior], 1, __ATOMIC_RELAXED);
+}
+#define ORDER_CHECK(S, best, interior, unsel) order_check(S, best, interior, unsel)
+#else
+#define ORDER_CHECK(S, best, interior, unsel) ((void)0)
+#endif
+
 /* Threshold of segment k (1-based) at its next service: n_k, or with
  * per-stage caps (Section 6: the segment cap B_k spread over the segment's
  * decode stages) the cap of the segment's stages taken in turn, the x-th
@@ -762,6 +799,7 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
         if (best < 0 || key_less(&S->R[best], &S->R[r])) best = r;
       }
     if (best < 0) break;
+    ORDER_CHECK(S, best, 0, 1);
     mplus -= charge(S, &S->R[best]);
     evict(S, best, 0);
   }
@@ -774,6 +812,7 @@ static int decide_nested(sim_t *S, int64_t *tokens, int64_t *prefill_l) {
       if (best < 0 || key_less(&S->R[best], &S->R[r])) best = r;
     }
     if (best < 0) break;
+    ORDER_CHECK(S, best, 1, 1);
     mplus -= charge(S, &S->R[best]);
     evict(S, best, 1);
   }
@@ -949,6 +988,7 @@ static void repair(sim_t *S) {
           if (best < 0 || key_less(&S->R[best], &S->R[r])) best = r;
         }
       if (best >= 0) {
+        ORDER_CHECK(S, best, 0, 0);
         evict(S, best, 0);
         continue;
       }
@@ -958,6 +998,7 @@ static void repair(sim_t *S) {
       if (best < 0 || key_less(&S->R[best], &S->R[r])) best = r;
     }
     if (best < 0) break;
+    if (c->policy == OR_NESTED) ORDER_CHECK(S, best, 1, 0);
     evict(S, best, c->policy == OR_NESTED);
   }
 }

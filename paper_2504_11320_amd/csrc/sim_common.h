@@ -452,8 +452,10 @@ struct QRec {   // shared FIFO record, 16 bytes
 
 struct NRec {   // Nested WAIT boundary / interior record, 32 bytes
   double a_ft;  // arrival time, sign = first token produced
-  uint32_t kb;  // admission batch of the last prefill
-  uint32_t kp;  // position within that batch
+  uint32_t kb;  // admission batch of the last prefill (FCFS with drawn
+                // lengths; Nested WAIT leaves it unset: its record positions
+                // already give the admission order)
+  uint32_t kp;  // position within that batch (likewise)
   int32_t j;    // type
   int32_t L;    // output length; 0 marks an evicted interior slot
   uint32_t c;   // service of its segment at which it entered

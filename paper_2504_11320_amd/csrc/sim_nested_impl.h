@@ -14,16 +14,15 @@
 // cohorts, the calendar links, the projected state Q+ of the pre-launch
 // repair, the completion walk -- runs on the segment lanes at once; the sums
 // over segments and types (batch tokens, Q+, the earliest arrival, the prefix
-// of segments meeting their thresholds, the most recently admitted eviction
-// candidate) are group reductions with DPP lane permutations inside the
-// 16-lane rows, on the ALU.  Replica-wide scalars (clock, counters, censored
+// of segments meeting their thresholds) are group reductions with DPP lane
+// permutations inside the 16-lane rows, on the ALU; the most recently
+// admitted eviction candidate is found from its position alone (a ballot).  Replica-wide scalars (clock, counters, censored
 // areas, resident memory) are kept identical in every lane of the group.
 //
 // Request records live in HBM, in the replica's block of the workspace:
 //   - the external queue Q_{1,0} (FIFO ring of 16-byte records);
-//   - for segment k >= 2 the resident boundary queue (a ring in
-//     admission-key order: FIFO selection pops the front, LIFO eviction pops
-//     the back);
+//   - for segment k >= 2 the resident boundary queue (a ring in admission
+//     order: FIFO selection pops the front, LIFO eviction pops the back);
 //   - for every segment a ring of cohort slots indexed by the segment's
 //     service number modulo delta_k (its number of processing stages).  The
 //     prompts that entered the segment at one service form a cohort of at
@@ -91,9 +90,6 @@ __device__ __forceinline__ QRec qrec_of(uint4 a) {
 __device__ __forceinline__ NRec load_nrec(const NRec *p) {
   const uint4 lo = ((const uint4 *)p)[0], hi = ((const uint4 *)p)[1];
   return nrec_of(lo, hi);
-}
-__device__ __forceinline__ uint64_t nrec_key(const NRec &r) {
-  return ((uint64_t)r.kb << 32) | r.kp;
 }
 // A record's type word carries the prompt length with the type, so the
 // charges a record implies need no table lookup: (l << 8) | type.
@@ -167,10 +163,6 @@ __device__ __forceinline__ uint32_t group_reduce32(uint32_t v, Op op) {
 template <int G>
 __device__ __forceinline__ int32_t group_sum32(int32_t v) {
   return (int32_t)group_reduce32<G>((uint32_t)v, [](uint32_t a, uint32_t b) { return a + b; });
-}
-template <int G>
-__device__ __forceinline__ uint64_t group_max(uint64_t v) {
-  return group_reduce64<G>(v, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
 }
 template <int G>
 __device__ __forceinline__ uint32_t group_or(uint32_t v) {
@@ -408,16 +400,14 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   int64_t M = 0;
   // segment lane k >= 2 (1-based): its boundary queue's ring ends and memory,
   // and what LIFO eviction needs of its back record and of the record before
-  // it (admission key, arrival with first-token mark, type word, length): an
-  // eviction takes the back and promotes the second at once, and the next
-  // second is loaded while the repair goes on
+  // it (arrival with first-token mark, type word, length): an eviction takes
+  // the back and promotes the second at once, and the next second is loaded
+  // while the repair goes on
   uint32_t vh = 0, vt = 0;
   int64_t Bk = 0;
-  uint64_t vbkey = 0, v2key = 0;
   double vba = 0.0, v2a = 0.0;
   int32_t vbj = 0, vbL = 0, v2j = 0, v2L = 0;
   auto set_back = [&](const NRec &b) __attribute__((always_inline)) {
-    vbkey = nrec_key(b);
     vba = b.a_ft;
     vbj = b.j;
     vbL = b.L;
@@ -425,7 +415,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   // the record before the back (valid while the queue holds two)
   auto load_second = [&]() __attribute__((always_inline)) {
     const NRec b = load_nrec(vr + ((vt - 2u) & vmask));
-    v2key = nrec_key(b);
     v2a = b.a_ft;
     v2j = b.j;
     v2L = b.L;
@@ -680,16 +669,24 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   // nothing was left).  `boundary` is cleared once the boundary queues are
   // found empty: within one repair they stay empty (evicted prompts go back
   // to the entry queue), so later calls skip that step.
+  //
+  // Admission order is also position order: a prompt admitted later never
+  // stands further along than one admitted earlier (segment 1, boundary
+  // queue 2, segment 2, ..., in that order).  A cohort enters a segment from
+  // the front of its queue, every cohort of a segment leaves it after the
+  // same number of services, and the survivors of one exit join the next
+  // queue in admission order; a prompt evicted re-enters with a new key.  So
+  // the most recent boundary prompt is the back of the lowest non-empty
+  // boundary queue, and the most recent interior prompt of segments >= klo
+  // is the youngest of the lowest such segment that holds one: no key
+  // comparison across lanes, and only that lane looks for its youngest.
   auto evict_lifo = [&](int klo, bool allow_interior, bool &boundary)
                         __attribute__((always_inline)) -> int64_t {
     if (boundary) {
       const bool cand = is_s && k >= 1 && vt != vh;
-      const uint64_t key = cand ? vbkey : 0ull;
       const uint64_t cb = group_bits<G>(cand);
       if (cb != 0) {
-        const uint64_t mx = group_max<G>(key);
-        const uint64_t wb = group_bits<G>(cand && key == mx);
-        const int h = __builtin_ctzll(wb);  // keys are unique: one lane
+        const int h = __builtin_ctzll(cb);
         const bool me = gl == h;
         // the victim is the back of boundary queue h: its charge l + r_{h-1}
         // and lost tokens r_{h-1}, from lane h
@@ -701,7 +698,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         if (me) {
           vt -= 1u;
           if (vt != vh) {  // the second is the new back
-            vbkey = v2key;
             vba = v2a;
             vbj = v2j;
             vbL = v2L;
@@ -719,15 +715,12 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       boundary = false;
     }
     if (!allow_interior) return 0;
+    const uint64_t ib = group_bits<G>(is_s && k >= klo && I != 0u);
+    if (ib == 0) return 0;
+    const int w = __builtin_ctzll(ib);
     uint32_t idx = kNil;
-    if (k >= klo) idx = youngest_interior();
-    const bool cand = idx != kNil;
-    const uint64_t key = cand ? nrec_key(yi) : 0ull;
-    const uint64_t cb = group_bits<G>(cand);
-    if (cb == 0) return 0;
-    const uint64_t mx = group_max<G>(key);
-    const uint64_t wb = group_bits<G>(cand && key == mx);
-    const int w = __builtin_ctzll(wb);
+    if (gl == w) idx = youngest_interior();
+    if (group_bits<G>(idx != kNil) == 0) return 0;
     const bool me = gl == w;
     int32_t ch = 0, gen = 0, dpend = 0;
     const NRec rec = yi;
@@ -871,7 +864,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
 
     // ---- launch: entering cohorts, calendar links, batch tokens -----------
     const bool served = is_s && k < kmax;
-    const uint32_t bidx = (uint32_t)batches;
     const uint32_t x = svc + 1u;
     int64_t tok = 0, sel = 0;
     int32_t pre_l = 0, pend_new = 0, dplus = 0;
@@ -905,8 +897,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
           e.a_ft = qr.a_ft;
           e.j = qr.j;
           e.L = qr.L;
-          e.kb = bidx;
-          e.kp = (uint32_t)i;
           tok += plen(qr.j);
           pre_l += plen(qr.j);
           if (!has_ft(qr.a_ft)) pend_new++;
@@ -1160,7 +1150,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     {
       const uint32_t np = seg_prev<G>(npush);
       const int32_t bp = (int32_t)seg_prev<G>((uint32_t)bpush);
-      const uint64_t lk = seg_prev64<G>(nrec_key(vlast));
       const double la = __longlong_as_double((long long)seg_prev64<G>(
           (uint64_t)__double_as_longlong(vlast.a_ft)));
       const int32_t lj = (int32_t)seg_prev<G>((uint32_t)vlast.j);
@@ -1170,14 +1159,12 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
         if (np != 0) {
           vt += np;
           if (np == 1) {  // the old back (if any) is the second
-            v2key = vbkey;
             v2a = vba;
             v2j = vbj;
             v2L = vbL;
           } else {
             load_second();
           }
-          vbkey = lk;
           vba = la;
           vbj = lj;
           vbL = lL;
