@@ -679,7 +679,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   // the most recent boundary prompt is the back of the lowest non-empty
   // boundary queue, and the most recent interior prompt of segments >= klo
   // is the youngest of the lowest such segment that holds one: no key
-  // comparison across lanes, and only that lane looks for its youngest.
+  // comparison across lanes.
   auto evict_lifo = [&](int klo, bool allow_interior, bool &boundary)
                         __attribute__((always_inline)) -> int64_t {
     if (boundary) {
@@ -715,12 +715,14 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       boundary = false;
     }
     if (!allow_interior) return 0;
-    const uint64_t ib = group_bits<G>(is_s && k >= klo && I != 0u);
+    // every candidate segment refreshes its cache (the scans' loads overlap,
+    // and a later repair that starts at a higher segment finds its youngest
+    // known); the victim is the lowest one's
+    uint32_t idx = kNil;
+    if (k >= klo) idx = youngest_interior();
+    const uint64_t ib = group_bits<G>(idx != kNil);
     if (ib == 0) return 0;
     const int w = __builtin_ctzll(ib);
-    uint32_t idx = kNil;
-    if (gl == w) idx = youngest_interior();
-    if (group_bits<G>(idx != kNil) == 0) return 0;
     const bool me = gl == w;
     int32_t ch = 0, gen = 0, dpend = 0;
     const NRec rec = yi;
