@@ -162,10 +162,15 @@ def baseline_threads() -> int:
 
 
 def source_hash(workload: str = "wait-llama") -> str:
+    """Hash of the kernel sources a profiled workload runs and of the hipcc
+    options they are compiled with."""
+    from paper_2504_11320_amd import build as Bd
     h = hashlib.sha256()
     for name in PROFILES[workload][1]:
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
+        if name.endswith(".hip"):
+            h.update(" ".join(Bd.flags_for(name)).encode())
     return h.hexdigest()[:16]
 
 

@@ -31,6 +31,24 @@ HIPCC_FLAGS = [
 ]
 
 
+# Instruction-scheduling strategy per translation unit (LLVM's AMDGPU
+# scheduler), as measured: the known-length WAIT kernels gain from the
+# ILP-maximising one (the FCFS ones lose), the Nested WAIT kernels from the
+# one that keeps memory clauses together.
+SCHED_FLAGS = {
+    "sim_known_wait.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "sim_known_wait_tv.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "sim_wait_many.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "sim_nested.hip": ["-mllvm", "-amdgpu-sched-strategy=max-memory-clause"],
+    "sim_nested_tv.hip": ["-mllvm", "-amdgpu-sched-strategy=max-memory-clause"],
+}
+
+
+def flags_for(src: str) -> list:
+    """hipcc options for one source file."""
+    return HIPCC_FLAGS + SCHED_FLAGS.get(os.path.basename(src), [])
+
+
 def hipcc() -> str:
     for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", "hipcc"):
         if c and (os.path.exists(c) or c == "hipcc"):
@@ -53,7 +71,7 @@ def build(verbose: bool = False, defines=(), out: str = LIB, sanitize: bool = Fa
     with tempfile.TemporaryDirectory(prefix="wait_sim_build_") as tmp:
         def compile_one(src: str):
             obj = os.path.join(tmp, os.path.basename(src) + ".o")
-            cmd = [hipcc()] + HIPCC_FLAGS + dflags + ["-I", INC, "-I", CSRC, "-c", "-o", obj, src]
+            cmd = [hipcc()] + flags_for(src) + dflags + ["-I", INC, "-I", CSRC, "-c", "-o", obj, src]
             if verbose:
                 print(" ".join(cmd), flush=True)
             t0 = time.perf_counter()
