@@ -427,6 +427,9 @@ __device__ __forceinline__ int hist_bin_idx(const double *E, const uint8_t *T, c
   const int64_t key = (int64_t)(dbits(lat) >> H.shift) - H.kmin;
   const int kc = key < 0 ? 0 : (key >= H.K ? H.K - 1 : (int)key);
   int pos = T[kc];
+  // a few steps at most (the table lands within H.steps edges): a copy of
+  // the loop unrolled for run-time trip counts only adds branches and code
+#pragma unroll 1
   for (int s = 0; s < H.steps; ++s) pos += E[pos] <= lat ? 1 : 0;
   return pos;
 }
