@@ -518,6 +518,11 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   yi.L = 0;
   yi.c = 0;
   yi.next = kNil;
+  // the segment's second youngest live interior record and its index (kNil:
+  // not known): it takes the youngest's place when that one leaves, so a
+  // second eviction in a row waits for no load
+  uint32_t y2idx = kNil;
+  NRec y2 = yi;
   if (is_s && k >= 1 && vt != vh) set_back(load_nrec(vr + ((vt - 1u) & vmask)));
   if (is_s && k >= 1 && vt - vh >= 2u) load_second();
 
@@ -729,13 +734,20 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     bool ft = false;
     if (me) {
       // idx is the segment's youngest live interior record
-      yidx = kNil;
-      ydead = idx;
+      if (y2idx != kNil) {  // the second is the new youngest
+        yi = y2;
+        yidx = y2idx;
+        y2idx = kNil;
+      } else {
+        yidx = kNil;
+        ydead = idx;
+      }
       const int32_t stage = ent + (int32_t)(svc - rec.c) + 1;
       ch = plen(rec.j) + stage;
       gen = stage - 1;
       NRec hole = rec;
       hole.L = 0;  // leaves a hole; the calendar skips it
+      hole.kb = hole.kp = 0u;
       rc[idx] = hole;
       if (idx == pf_ti) pf_tr.y = 0u;  // the prefetched terminal record has left
       I -= 1u;
@@ -923,8 +935,13 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
           rc[idx] = e;
         }
         if (i == ncap - 1) {  // the cohort's last record is the segment's youngest
+          y2 = yi;  // the youngest so far is second (a cohort of one)
+          y2idx = yidx;
           yi = e;
           yidx = idx;
+        } else if (i == ncap - 2) {  // the cohort's record before it is second
+          y2 = e;
+          y2idx = idx;
         }
         const int32_t le = plen(e.j);
         suml += (uint32_t)le;
@@ -1092,9 +1109,16 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
             crec = load_nrec(rc + nxt);
         }
         if (rec.L != 0) {  // holes left by evictions are skipped
+          if (node == y2idx) y2idx = kNil;  // the second leaves
           if (node == yidx) {  // the youngest leaves
-            ydead = node;
-            yidx = kNil;
+            if (y2idx != kNil) {  // the second is the new youngest
+              yi = y2;
+              yidx = y2idx;
+              y2idx = kNil;
+            } else {
+              ydead = node;
+              yidx = kNil;
+            }
           }
           const int64_t le = plen(rec.j);
           const int32_t p = rec.L < rk ? rec.L : rk;
