@@ -745,10 +745,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
       const int32_t stage = ent + (int32_t)(svc - rec.c) + 1;
       ch = plen(rec.j) + stage;
       gen = stage - 1;
-      NRec hole = rec;
-      hole.L = 0;  // leaves a hole; the calendar skips it
-      hole.kb = hole.kp = 0u;
-      rc[idx] = hole;
+      rc[idx].L = 0;  // leaves a hole; the calendar skips it
       if (idx == pf_ti) pf_tr.y = 0u;  // the prefetched terminal record has left
       I -= 1u;
       M -= ch;
