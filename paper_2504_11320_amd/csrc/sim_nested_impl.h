@@ -882,13 +882,18 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     uint32_t eI = 0;
     // n_k = 1: the entering record is stored only at the completion step, so
     // the launch never waits for the bucket head it links to; the walk's
-    // first record (the head prefetched for this service) is loaded after
-    // the pre-launch repair
+    // first record (the head prefetched for this service) is loaded at once
     NRec pend = yi;
     uint32_t pend_idx = kNil;
     const uint32_t bh0 = bh;
     NRec crec0 = yi;
     const bool pre_ok = served && nrow == 1 && bh0 != kNil;
+    // the walk's first record, loaded now: the walk waits for it last, and
+    // with the boundary queues' back records and each segment's two youngest
+    // interior records at hand the repair seldom waits for a load of its own
+    // (memory operations complete in issue order); the pre-launch repair
+    // leaves the served segments' records alone
+    if (pre_ok) crec0 = load_nrec(rc + bh0);
     // prompts entering segment 1 now (the cap of its service)
     const int32_t n0c = capped ? __shfl(ncap, 0, G) : n0;
     if (served) {
@@ -1012,11 +1017,6 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     }
     if (mplus > C) flags |= kFlagOverflow;
     __builtin_amdgcn_s_setprio(0);
-    // the walk's first record, loaded only now: memory operations complete in
-    // issue order, so a load issued before the repair would hold up the
-    // repair's own short loads (the pre-launch repair leaves the served
-    // segments' records alone)
-    if (pre_ok) crec0 = load_nrec(rc + bh0);
     const int64_t bt_ev1 = evicts;
     const int64_t bt_comps0 = comps;
 
