@@ -32,15 +32,14 @@ HIPCC_FLAGS = [
 
 
 # Instruction-scheduling strategy per translation unit (LLVM's AMDGPU
-# scheduler), as measured: the known-length WAIT kernels gain from the
-# ILP-maximising one (the FCFS ones lose), the Nested WAIT kernels from the
-# one that keeps memory clauses together.
+# scheduler), as measured: the known-length WAIT and the Nested WAIT kernels
+# gain from the ILP-maximising one, the FCFS kernels lose.
 SCHED_FLAGS = {
     "sim_known_wait.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
     "sim_known_wait_tv.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
     "sim_wait_many.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
-    "sim_nested.hip": ["-mllvm", "-amdgpu-sched-strategy=max-memory-clause"],
-    "sim_nested_tv.hip": ["-mllvm", "-amdgpu-sched-strategy=max-memory-clause"],
+    "sim_nested.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+    "sim_nested_tv.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
 }
 
 
