@@ -7,17 +7,18 @@
 // replicas.  Lane
 // g of a group owns request type g (its arrival clock, draw counter and the
 // length of its pending arrival) and segment g (its service count, interior
-// count and memory, calendar, cohort slots, the cache of its youngest
-// interior prompt, and its boundary queue's ends, memory and back record, in
-// registers: the survivors lane g-1 pushes are handed over by a lane shift
-// after the walk).  What a batch does segment by segment -- the entering
-// cohorts, the calendar links, the projected state Q+ of the pre-launch
-// repair, the completion walk -- runs on the segment lanes at once; the sums
-// over segments and types (batch tokens, Q+, the earliest arrival, the prefix
-// of segments meeting their thresholds) are group reductions with DPP lane
-// permutations inside the 16-lane rows, on the ALU; the most recently
-// admitted eviction candidate is found from its position alone (a ballot).  Replica-wide scalars (clock, counters, censored
-// areas, resident memory) are kept identical in every lane of the group.
+// count and memory, calendar, cohort slots, the cache of its two youngest
+// interior prompts, and its boundary queue's ends, memory and back two
+// records, in registers: the survivors lane g-1 pushes are handed over by a
+// lane shift after the walk).  What a batch does segment by segment -- the
+// entering cohorts, the calendar links, the projected state Q+ of the
+// pre-launch repair, the completion walk -- runs on the segment lanes at
+// once; the sums over segments and types (batch tokens, Q+, the earliest
+// arrival, the prefix of segments meeting their thresholds) are group
+// reductions with DPP lane permutations inside the 16-lane rows, on the ALU;
+// the most recently admitted eviction candidate is found from its position
+// alone (a ballot).  Replica-wide scalars (clock, counters, censored areas,
+// resident memory) are kept identical in every lane of the group.
 //
 // Request records live in HBM, in the replica's block of the workspace:
 //   - the external queue Q_{1,0} (FIFO ring of 16-byte records);
