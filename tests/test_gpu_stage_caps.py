@@ -86,6 +86,9 @@ def test_random_capped_models(B):
     jobs = [W.Job(random_capped(rng), 9, W.ids(8)) for _ in range(16)]
     g, _ = check(B, jobs, 1500, "random capped Nested WAIT")
     assert g["evictions"].sum() > 0  # tight memory in some of the models
+    # interior (fallback) evictions, back to back and from partly filled
+    # cohort rows: the kernel's cached youngest records are exercised
+    assert g["fallback_evictions"].sum() > 1000
 
 
 def test_uniform_caps_equal_the_specialised_kernel(B):
