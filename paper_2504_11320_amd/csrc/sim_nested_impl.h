@@ -521,7 +521,8 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
   yi.next = kNil;
   // the segment's second youngest live interior record and its index (kNil:
   // not known): it takes the youngest's place when that one leaves, so a
-  // second eviction in a row waits for no load
+  // second eviction in a row waits for no load (the specialised
+  // instantiation only: the general one, short of registers, would spill it)
   uint32_t y2idx = kNil;
   NRec y2 = yi;
   if (is_s && k >= 1 && vt != vh) set_back(load_nrec(vr + ((vt - 1u) & vmask)));
@@ -735,7 +736,7 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
     bool ft = false;
     if (me) {
       // idx is the segment's youngest live interior record
-      if (y2idx != kNil) {  // the second is the new youngest
+      if (!TV && y2idx != kNil) {  // the second is the new youngest
         yi = y2;
         yidx = y2idx;
         y2idx = kNil;
@@ -938,11 +939,13 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
           rc[idx] = e;
         }
         if (i == ncap - 1) {  // the cohort's last record is the segment's youngest
-          y2 = yi;  // the youngest so far is second (a cohort of one)
-          y2idx = yidx;
+          if constexpr (!TV) {
+            y2 = yi;  // the youngest so far is second (a cohort of one)
+            y2idx = yidx;
+          }
           yi = e;
           yidx = idx;
-        } else if (i == ncap - 2) {  // the cohort's record before it is second
+        } else if (!TV && i == ncap - 2) {  // the cohort's record before it is second
           y2 = e;
           y2idx = idx;
         }
@@ -1107,9 +1110,9 @@ __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) si
             crec = load_nrec(rc + nxt);
         }
         if (rec.L != 0) {  // holes left by evictions are skipped
-          if (node == y2idx) y2idx = kNil;  // the second leaves
+          if (!TV && node == y2idx) y2idx = kNil;  // the second leaves
           if (node == yidx) {  // the youngest leaves
-            if (y2idx != kNil) {  // the second is the new youngest
+            if (!TV && y2idx != kNil) {  // the second is the new youngest
               yi = y2;
               yidx = y2idx;
               y2idx = kNil;
